@@ -1,0 +1,150 @@
+"""Seeded synthetic inputs for the slice -> token mix -> deslice path.
+
+This module only draws random numbers and rounds them to the storage dtype. It holds none of
+the method's arithmetic, so both the fp64 oracle (test side) and the HIP path (product side)
+can consume what it produces without sharing any code with each other.
+
+Every tensor comes from its own sub-stream ``numpy.random.default_rng([SEED, cfg_id, k])``
+so that adding a tensor never shifts another one. Values are drawn in fp32 and, for bf16
+storage, rounded to the nearest bf16 (ties to even) and kept as exactly representable fp32.
+
+Workloads (the readings of under-specified choices are listed in the design doc):
+
+=========  ======  =====  =========  ==  ==  ====  =====================================
+name       dtype   B      N          H   D   G     mix / special structure
+=========  ======  =====  =========  ==  ==  ====  =====================================
+tiny       f32     1      4096       8   16  32    fixed G x G matrix A ~ N(0, 1/G)
+surface    f32     1      32768      8   32  32    single-head G x G token self-attention
+volume     bf16    1      1048576    8   32  64    fixed G x G matrix
+stressG    bf16    1      262144     8   32  G     per-head tau ~ U[0.3, 1.0]; W_s with
+                                                   pre-temperature logit std 3; G in
+                                                   {128, 256, 512, 1024}
+stack      f32     4      131072     8   32  64    fixed G x G matrix (one layer's path)
+=========  ======  =====  =========  ==  ==  ====  =====================================
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, Optional
+
+import numpy as np
+
+SEED = 20261202
+
+MIX_IDENTITY, MIX_LINEAR_G, MIX_LINEAR_C, MIX_ATTN = 0, 1, 2, 3
+
+# sub-stream ids, one per tensor
+_K_X, _K_F, _K_WS, _K_B, _K_TAU, _K_A, _K_WC, _K_WQ, _K_WK, _K_WV, _K_DO = range(11)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    cfg_id: int
+    dtype: str            # "f32" or "bf16": storage of x, fx, out, dout, dx, dfx
+    B: int
+    N: int
+    H: int
+    D: int
+    V: int
+    G: int
+    mix: int
+    eps: float = 1e-5
+    tau_mode: str = "const"     # "const" (tau = 0.5 for every head) or "uniform" (U[0.3, 1])
+    ws_mode: str = "xavier"     # "xavier" or "std3" (pre-temperature logit std 3)
+    ws_per_head: bool = False
+    a_per_head: bool = False
+
+    def scaled(self, **kw) -> "Workload":
+        return dataclasses.replace(self, **kw)
+
+    @property
+    def points(self) -> int:
+        return self.B * self.N
+
+
+WORKLOADS: Dict[str, Workload] = {
+    "tiny": Workload("tiny", 0, "f32", 1, 4096, 8, 16, 16, 32, MIX_LINEAR_G),
+    "surface": Workload("surface", 1, "f32", 1, 32768, 8, 32, 32, 32, MIX_ATTN),
+    "volume": Workload("volume", 2, "bf16", 1, 1 << 20, 8, 32, 32, 64, MIX_LINEAR_G),
+    "stack": Workload("stack", 4, "f32", 4, 1 << 17, 8, 32, 32, 64, MIX_LINEAR_G),
+}
+for _g in (128, 256, 512, 1024):
+    WORKLOADS[f"stress{_g}"] = Workload(f"stress{_g}", 3, "bf16", 1, 1 << 18, 8, 32, 32, _g,
+                                        MIX_LINEAR_G, tau_mode="uniform", ws_mode="std3")
+
+
+def round_to_bf16(a: np.ndarray) -> np.ndarray:
+    """Nearest bf16 value of each fp32 entry (ties to even), returned as fp32."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    bits = a.view(np.uint32).astype(np.uint64)
+    rounded = ((bits + 0x7FFF + ((bits >> 16) & 1)) >> 16) << 16
+    out = rounded.astype(np.uint32).view(np.float32)
+    nan = np.isnan(a)
+    if nan.any():
+        out = out.copy()
+        out[nan] = np.float32("nan")
+    return out
+
+
+def _rng(w: Workload, k: int) -> np.random.Generator:
+    return np.random.default_rng([SEED, w.cfg_id, k, w.G])
+
+
+def _store(w: Workload, a: np.ndarray) -> np.ndarray:
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    return round_to_bf16(a) if w.dtype == "bf16" else a
+
+
+def _normal(rng, shape, std=1.0) -> np.ndarray:
+    out = rng.standard_normal(size=shape, dtype=np.float32)
+    if std != 1.0:
+        out *= np.float32(std)
+    return out
+
+
+def _xavier(rng, shape, fan_in, fan_out) -> np.ndarray:
+    lim = math.sqrt(6.0 / (fan_in + fan_out))
+    return rng.uniform(-lim, lim, size=shape).astype(np.float32)
+
+
+def make_inputs(w: Workload, with_grad: bool = True) -> Dict[str, Optional[np.ndarray]]:
+    """All inputs of one forward + backward as fp32 numpy arrays (exact stored values).
+
+    Keys: x (B,N,H,D), fx (B,N,H,V), Ws (D,G) or (H,D,G), b (G) or (H,G), tau (H),
+    A (G,G) or (H,G,G) for the fixed token matrix, Wc (V,V), Wq/Wk/Wv (V,V), scale, dout.
+    """
+    B, N, H, D, V, G = w.B, w.N, w.H, w.D, w.V, w.G
+    x = _store(w, _normal(_rng(w, _K_X), (B, N, H, D)))
+    fx = _store(w, _normal(_rng(w, _K_F), (B, N, H, V)))
+    ws_shape = (H, D, G) if w.ws_per_head else (D, G)
+    if w.ws_mode == "xavier":
+        Ws = _xavier(_rng(w, _K_WS), ws_shape, D, G)
+    else:  # pre-temperature logit std 3 for unit-variance x: W_s ~ N(0, 9/D)
+        Ws = _normal(_rng(w, _K_WS), ws_shape, 3.0 / math.sqrt(D))
+    b = np.zeros((H, G) if w.ws_per_head else (G,), dtype=np.float32)
+    if w.tau_mode == "const":
+        tau = np.full((H,), 0.5, dtype=np.float32)
+    else:
+        tau = _rng(w, _K_TAU).uniform(0.3, 1.0, size=(H,)).astype(np.float32)
+    out = dict(x=x, fx=fx, Ws=Ws, b=b, tau=tau, A=None, Wc=None, Wq=None, Wk=None, Wv=None,
+               scale=np.float32(1.0 / math.sqrt(V)), dout=None)
+    if w.mix == MIX_LINEAR_G:
+        out["A"] = _normal(_rng(w, _K_A), (H, G, G) if w.a_per_head else (G, G),
+                           1.0 / math.sqrt(G))
+    elif w.mix == MIX_LINEAR_C:
+        out["Wc"] = _xavier(_rng(w, _K_WC), (V, V), V, V)
+    elif w.mix == MIX_ATTN:
+        out["Wq"] = _xavier(_rng(w, _K_WQ), (V, V), V, V)
+        out["Wk"] = _xavier(_rng(w, _K_WK), (V, V), V, V)
+        out["Wv"] = _xavier(_rng(w, _K_WV), (V, V), V, V)
+    if with_grad:
+        out["dout"] = _store(w, _normal(_rng(w, _K_DO), (B, N, H, V)))
+    return out
+
+
+def random_like(w: Workload, seed_k: int, shape, std=1.0) -> np.ndarray:
+    """Extra seeded N(0, std^2) tensor (for tests that need more random data)."""
+    rng = np.random.default_rng([SEED, w.cfg_id, 1000 + seed_k, w.G])
+    return _normal(rng, shape, std)
