@@ -1,0 +1,161 @@
+/*
+ * flashslice.h - C ABI of the fused slice -> token mix -> deslice path of Transolver
+ * physics-attention on AMD Instinct MI355X (gfx950).
+ *
+ * What the calls compute, per sample b and head h (paper: Sec. 2 "The Transolver layer",
+ * Eq. (1), App. F.1 "Kernel design", App. F.2 "Temperature gradients"):
+ *
+ *   logits   a[n, g] = (x[n, :] . W_s[:, g] + bias[g]) / tau[h]
+ *   weights  w[n, :] = softmax over the G slices of a[n, :]      (never written to memory)
+ *   slice    s[g] = sum_n w[n, g];  z[g, :] = (sum_n w[n, g] fx[n, :]) / (s[g] + eps)
+ *   mix      zmix = Mix(z)   (identity, fixed G x G matrix, per-token channel map, or
+ *                              single-head softmax self-attention among the G tokens)
+ *   deslice  out[n, :] = sum_g w[n, g] zmix[g, :]
+ *
+ * and the exact backward of that composition. The N x G slice-weight tensor never exists in
+ * device memory: every pass recomputes the weights from x and the saved per-point
+ * normaliser `lse`.
+ *
+ * lse is stored in base 2, the unit the kernels compute in:
+ *   lse[n] = log2( sum_g 2^(a[n, g] * log2(e)) ) = log(sum_g exp(a[n, g])) * log2(e),
+ * so that w[n, g] = 2^(a[n, g] * log2(e) - lse[n]) with no unit conversion between passes.
+ *
+ * Conventions (all entry points):
+ *   - Pointers are device pointers (hipMalloc / torch), owned by the caller. The library never
+ *     allocates, frees, retains pointers or synchronises. All work is enqueued on `hip_stream`
+ *     (a hipStream_t; NULL means the default stream); buffers must stay alive until it
+ *     completes.
+ *   - Layouts are row-major and contiguous:
+ *       x (B,N,H,D), fx (B,N,H,V), out / dout / dfx (B,N,H,V), dx (B,N,H,D) in the storage
+ *       dtype; z, zmix, dzmix (B,H,G,V), s (B,H,G), lse (B,H,N), attn_probs (B,H,G,G),
+ *       W_s (D,G) [or (H,D,G) with ws_per_head], bias (G) [or (H,G)], tau (H): fp32.
+ *   - Every device pointer must be 16-byte aligned.
+ *   - Outputs are overwritten, never accumulated. Gradients of parameters shared by heads
+ *     are summed over samples and heads. Inputs are never modified. An output that overlaps
+ *     any input or another output is rejected (FS_ERR_ALIAS).
+ *   - Errors: a negative fs_status is returned after host-side validation, before anything
+ *     is enqueued; nothing is printed. A failed launch returns FS_ERR_HIP and records the
+ *     hipError_t for fs_last_hip_error() (per thread).
+ *   - tau > 0 is a precondition (tau lives in device memory and is not read by the host).
+ *   - Results are deterministic: no atomics; every reduction has a fixed order, so repeated
+ *     calls give bitwise identical outputs.
+ *   - Supported shapes: D == V in {16, 32, 64}; G a power of two in [16, 1024] (fp32
+ *     storage) or [32, 1024] (bf16 storage); attention mix for G <= 256 and G * V <= 8192;
+ *     B * H <= 65535. Anything else returns FS_ERR_UNSUPPORTED.
+ *   - Concurrent calls are safe as long as they do not share a workspace.
+ */
+#ifndef FLASHSLICE_H
+#define FLASHSLICE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Storage dtype of x, fx, out, dout, dx, dfx. Arithmetic always accumulates in fp32. */
+typedef enum { FS_F32 = 0, FS_BF16 = 1 } fs_dtype;
+
+typedef enum {
+  FS_OK = 0,
+  FS_ERR_NULL = -1,        /* a required pointer is NULL                                  */
+  FS_ERR_SHAPE = -2,       /* non-positive or inconsistent sizes                           */
+  FS_ERR_DTYPE = -3,       /* unknown dtype                                                */
+  FS_ERR_UNSUPPORTED = -4, /* valid problem outside the shapes this library implements     */
+  FS_ERR_WORKSPACE = -5,   /* workspace missing or smaller than fs_workspace_bytes()       */
+  FS_ERR_ARG = -6,         /* other invalid argument (eps < 0 or not finite, mix kind ...) */
+  FS_ERR_ALIGN = -7,       /* a device pointer is not 16-byte aligned                      */
+  FS_ERR_ALIAS = -8,       /* an output overlaps an input or another output                */
+  FS_ERR_HIP = -9          /* the HIP runtime reported an error at launch                  */
+} fs_status;
+
+/* Problem description. B >= 1, N >= 0 points per sample (N = 0 is allowed: tokens are 0/eps),
+ * H >= 1 heads, D = slice-projection width (dh), V = value width, G = number of slices.     */
+typedef struct {
+  int64_t B, N;
+  int32_t H, D, V, G;
+  int32_t dtype;        /* fs_dtype                                                        */
+  float eps;            /* z = U / (s + eps); must be finite and >= 0 (paper: App. F.1)    */
+  int32_t ws_per_head;  /* 0: W_s (D,G) and bias (G) shared by heads; 1: (H,D,G) and (H,G) */
+} fs_problem;
+
+typedef enum {
+  FS_MIX_IDENTITY = 0, /* zmix = z                                                          */
+  FS_MIX_LINEAR_G = 1, /* zmix[g, :] = sum_k A[g, k] z[k, :]   (constant core of Eq. (1))     */
+  FS_MIX_LINEAR_C = 2, /* zmix = z Wc                          (per-token channel map)        */
+  FS_MIX_ATTN = 3      /* q = z Wq, k = z Wk, v = z Wv; P = softmax_row(scale q k^T); zmix = P v */
+} fs_mix_kind;
+
+/* Token mix parameters (fp32 device pointers; only those of `kind` are read).
+ * A: (G,G), or (H,G,G) when a_per_head = 1. Wc, Wq, Wk, Wv: (V,V), shared by heads.       */
+typedef struct {
+  int32_t kind;         /* fs_mix_kind                                                     */
+  int32_t a_per_head;
+  const float* A;
+  const float* Wc;
+  const float* Wq;
+  const float* Wk;
+  const float* Wv;
+  float scale;          /* attention logit scale, e.g. 1/sqrt(V)                           */
+} fs_mix_desc;
+
+/* Bytes of device workspace needed by fs_slice_fwd (for_backward = 0), or by fs_mix_bwd and
+ * fs_slice_deslice_bwd (for_backward = 1), for this problem. The size never grows with N*G:
+ * it holds per-workgroup partial sums (bounded number of workgroups) and token-sized
+ * buffers. Returns FS_OK and writes *bytes, or a validation error.                          */
+int fs_workspace_bytes(const fs_problem* prob, int for_backward, size_t* bytes);
+
+/* Slice (paper: Sec. 2; App. F.1 single-tile equation): recompute the slice weights per
+ * point tile and reduce them into s (B,H,G) and the normalised tokens z (B,H,G,V).
+ * lse (B,H,N), nullable: receives the base-2 normaliser log2(sum_g 2^(a[n, g] log2 e)) per
+ * point, needed by the deslice and the backward.
+ * ws/ws_bytes: workspace of at least fs_workspace_bytes(prob, 0, .) bytes.                  */
+int fs_slice_fwd(const fs_problem* prob, const void* x, const void* fx, const float* Ws,
+                 const float* bias, const float* tau, float* z, float* s, float* lse,
+                 void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Token mix (paper: Sec. 2; Eq. (1); the attention-free variant). z, zmix: (B,H,G,V).
+ * attn_probs: (B,H,G,G) output, required for FS_MIX_ATTN (saved for the backward),
+ * ignored otherwise.                                                                        */
+int fs_mix(const fs_problem* prob, const fs_mix_desc* mix, const float* z, float* zmix,
+           float* attn_probs, void* hip_stream);
+
+/* Backward of the token mix: dz = Mix^T(dzmix) and the mix-parameter gradient (summed over
+ * samples and heads; per head for a per-head A): dmix_params is dA (G,G)/(H,G,G) for
+ * LINEAR_G, dWc (V,V) for LINEAR_C, [dWq; dWk; dWv] (3,V,V) for ATTN; nullable (skipped).
+ * Needs the backward workspace.                                                             */
+int fs_mix_bwd(const fs_problem* prob, const fs_mix_desc* mix, const float* z,
+               const float* attn_probs, const float* dzmix, float* dz, float* dmix_params,
+               void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Deslice (paper: Sec. 2, u_i = sum_g w_ig z'_g; App. F.1): recompute the weights from x and
+ * lse (required) and write out (B,N,H,V) = w zmix in the storage dtype.                     */
+int fs_deslice_fwd(const fs_problem* prob, const void* x, const float* Ws, const float* bias,
+                   const float* tau, const float* zmix, const float* lse, void* out,
+                   void* hip_stream);
+
+/* Backward of slice -> mix -> deslice for the upstream gradient dout (B,N,H,V).
+ * Inputs are the forward's inputs and saved z, s, zmix, attn_probs (ATTN only), lse.
+ * Outputs: dx (B,N,H,D), dfx (B,N,H,V) in the storage dtype; dWs, dbias shaped like Ws,
+ * bias; dtau (H); dmix_params as in fs_mix_bwd (nullable); dzmix_out (B,H,G,V) = w^T dout
+ * (nullable). The temperature gradient follows App. F.2.                                    */
+int fs_slice_deslice_bwd(const fs_problem* prob, const fs_mix_desc* mix, const void* x,
+                         const void* fx, const float* Ws, const float* bias, const float* tau,
+                         const float* z, const float* s, const float* zmix,
+                         const float* attn_probs, const float* lse, const void* dout,
+                         void* dx, void* dfx, float* dWs, float* dbias, float* dtau,
+                         float* dmix_params, float* dzmix_out, void* ws, size_t ws_bytes,
+                         void* hip_stream);
+
+/* Static text for a status code. */
+const char* fs_status_string(int status);
+
+/* hipError_t recorded by the last FS_ERR_HIP on this thread (0 if none). */
+int fs_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FLASHSLICE_H */

@@ -153,28 +153,35 @@ def logit_backward(da, X, Ws, a, tau):
 # ----------------------------------------------------------------------------------------
 # whole path
 # ----------------------------------------------------------------------------------------
-def _head_params(kind, prm, h):
-    p = {"scale": f64(prm.get("scale") if prm.get("scale") is not None else 1.0)}
+def _head_params(kind, prm, h, ct=f64):
+    p = {"scale": ct(prm.get("scale") if prm.get("scale") is not None else 1.0)}
     if kind == MIX_LINEAR_G:
-        A = np.asarray(prm["A"], dtype=f64)
+        A = np.asarray(prm["A"], dtype=ct)
         p["A"] = A[h] if A.ndim == 3 else A
     elif kind == MIX_LINEAR_C:
-        p["Wc"] = np.asarray(prm["Wc"], dtype=f64)
+        p["Wc"] = np.asarray(prm["Wc"], dtype=ct)
     elif kind == MIX_ATTN:
         for k in ("Wq", "Wk", "Wv"):
-            p[k] = np.asarray(prm[k], dtype=f64)
+            p[k] = np.asarray(prm[k], dtype=ct)
     return p
 
 
-def _ws_b(Ws, b, h):
-    Ws = np.asarray(Ws, dtype=f64)
-    b = np.asarray(b, dtype=f64)
+def _ws_b(Ws, b, h, ct=f64):
+    Ws = np.asarray(Ws, dtype=ct)
+    b = np.asarray(b, dtype=ct)
     return (Ws[h] if Ws.ndim == 3 else Ws), (b[h] if b.ndim == 2 else b)
 
 
+def _pairs(B, H, pairs):
+    return [(bb, h) for bb in range(B) for h in range(H)] if pairs is None else list(pairs)
+
+
 def forward(x, fx, Ws, b, tau, kind, prm: Optional[Dict] = None, eps=1e-5,
-            keep_weights=False) -> Dict[str, np.ndarray]:
-    """Forward of the path over all samples and heads.
+            keep_weights=False, pairs=None, dtype=f64) -> Dict[str, np.ndarray]:
+    """Forward of the path over all samples and heads (or only the (sample, head) pairs
+    listed in ``pairs``; entries of the other pairs are left at zero). ``dtype`` is the
+    arithmetic type (fp64; fp32 only to measure what plain fp32 evaluation of the same
+    definition loses, the yardstick of the acceptance rule in App. F.2).
 
     x (B, N, H, D), fx (B, N, H, V), Ws (D, G) or (H, D, G), b (G) or (H, G), tau (H).
     Returns z, s (B, H, G[, V]), zmix (B, H, G, V), P (B, H, G, G) for attention,
@@ -191,28 +198,29 @@ def forward(x, fx, Ws, b, tau, kind, prm: Optional[Dict] = None, eps=1e-5,
     if keep_weights:
         res["a"] = np.zeros((B, H, N, G))
         res["w"] = np.zeros((B, H, N, G))
-    for bb in range(B):
-        for h in range(H):
-            X = np.asarray(x[bb, :, h, :], dtype=f64)
-            F = np.asarray(fx[bb, :, h, :], dtype=f64)
-            Wsh, bh = _ws_b(Ws, b, h)
-            a = logits(X, Wsh, bh, f64(tau[h]))
-            w, lse = slot_softmax(a)
-            s, U, z = slice_tokens(w, F, eps)
-            zm, P = mix_forward(kind, z, _head_params(kind, prm, h))
-            res["z"][bb, h], res["s"][bb, h], res["zmix"][bb, h] = z, s, zm
-            res["lse"][bb, h] = lse
-            if P is not None:
-                res["P"][bb, h] = P
-            res["out"][bb, :, h, :] = deslice(w, zm)
-            if keep_weights:
-                res["a"][bb, h], res["w"][bb, h] = a, w
+    ct = np.dtype(dtype).type
+    for bb, h in _pairs(B, H, pairs):
+        X = np.asarray(x[bb, :, h, :], dtype=ct)
+        F = np.asarray(fx[bb, :, h, :], dtype=ct)
+        Wsh, bh = _ws_b(Ws, b, h, ct)
+        a = logits(X, Wsh, bh, ct(tau[h]))
+        w, lse = slot_softmax(a)
+        s, U, z = slice_tokens(w, F, ct(eps))
+        zm, P = mix_forward(kind, z, _head_params(kind, prm, h, ct))
+        res["z"][bb, h], res["s"][bb, h], res["zmix"][bb, h] = z, s, zm
+        res["lse"][bb, h] = lse
+        if P is not None:
+            res["P"][bb, h] = P
+        res["out"][bb, :, h, :] = deslice(w, zm)
+        if keep_weights:
+            res["a"][bb, h], res["w"][bb, h] = a, w
     return res
 
 
 def backward(x, fx, Ws, b, tau, kind, prm: Optional[Dict], dout, eps=1e-5,
-             fwd: Optional[Dict] = None) -> Dict[str, np.ndarray]:
-    """Backward of the path for the upstream gradient dout (B, N, H, V).
+             fwd: Optional[Dict] = None, pairs=None, dtype=f64) -> Dict[str, np.ndarray]:
+    """Backward of the path for the upstream gradient dout (B, N, H, V) (over all samples and
+    heads, or only the listed pairs: then parameter gradients sum those pairs only).
 
     Returns dx, dfx (point gradients), dWs, db (shaped like Ws, b), dtau (H), dzmix and dz
     (B, H, G, V), and the mix-parameter gradients (dA, dWc or dWq/dWk/dWv).
@@ -224,54 +232,57 @@ def backward(x, fx, Ws, b, tau, kind, prm: Optional[Dict], dout, eps=1e-5,
     b_arr = np.asarray(b, dtype=f64)
     G = Ws_arr.shape[-1]
     if fwd is None:
-        fwd = forward(x, fx, Ws, b, tau, kind, prm, eps)
+        fwd = forward(x, fx, Ws, b, tau, kind, prm, eps, pairs=pairs, dtype=dtype)
+    ct = np.dtype(dtype).type
     res = dict(dx=np.zeros((B, N, H, D)), dfx=np.zeros((B, N, H, V)),
                dWs=np.zeros_like(Ws_arr), db=np.zeros_like(b_arr), dtau=np.zeros(H),
                dzmix=np.zeros((B, H, G, V)), dz=np.zeros((B, H, G, V)))
-    for bb in range(B):
-        for h in range(H):
-            X = np.asarray(x[bb, :, h, :], dtype=f64)
-            F = np.asarray(fx[bb, :, h, :], dtype=f64)
-            dO = np.asarray(dout[bb, :, h, :], dtype=f64)
-            Wsh, bh = _ws_b(Ws, b, h)
-            t = f64(tau[h])
-            a = logits(X, Wsh, bh, t)
-            w, _ = slot_softmax(a)
-            z, s, zm = fwd["z"][bb, h], fwd["s"][bb, h], fwd["zmix"][bb, h]
-            P = fwd["P"][bb, h] if fwd.get("P") is not None else None
-            dzm = w.T @ dO
-            dz, dprm = mix_backward(kind, z, P, dzm, _head_params(kind, prm, h))
-            dU, ds = token_backward(dz, z, s, eps)
-            dw = weight_grad(dO, zm, F, dU, ds)
-            da = softmax_backward(w, dw)
-            dX, dWs, db, dtau = logit_backward(da, X, Wsh, a, t)
-            res["dx"][bb, :, h, :] = dX
-            res["dfx"][bb, :, h, :] = w @ dU
-            res["dzmix"][bb, h], res["dz"][bb, h] = dzm, dz
-            res["dtau"][h] += dtau
-            if Ws_arr.ndim == 3:
-                res["dWs"][h] += dWs
+    for bb, h in _pairs(B, H, pairs):
+        X = np.asarray(x[bb, :, h, :], dtype=ct)
+        F = np.asarray(fx[bb, :, h, :], dtype=ct)
+        dO = np.asarray(dout[bb, :, h, :], dtype=ct)
+        Wsh, bh = _ws_b(Ws, b, h, ct)
+        t = ct(tau[h])
+        a = logits(X, Wsh, bh, t)
+        w, _ = slot_softmax(a)
+        z, s, zm = (fwd["z"][bb, h].astype(ct), fwd["s"][bb, h].astype(ct),
+                    fwd["zmix"][bb, h].astype(ct))
+        P = fwd["P"][bb, h].astype(ct) if fwd.get("P") is not None else None
+        dzm = w.T @ dO
+        dz, dprm = mix_backward(kind, z, P, dzm, _head_params(kind, prm, h, ct))
+        dU, ds = token_backward(dz, z, s, ct(eps))
+        dw = weight_grad(dO, zm, F, dU, ds)
+        da = softmax_backward(w, dw)
+        dX, dWs, db, dtau = logit_backward(da, X, Wsh, a, t)
+        res["dx"][bb, :, h, :] = dX
+        res["dfx"][bb, :, h, :] = w @ dU
+        res["dzmix"][bb, h], res["dz"][bb, h] = dzm, dz
+        res["dtau"][h] += dtau
+        if Ws_arr.ndim == 3:
+            res["dWs"][h] += dWs
+        else:
+            res["dWs"] += dWs
+        if b_arr.ndim == 2:
+            res["db"][h] += db
+        else:
+            res["db"] += db
+        for k, v in dprm.items():
+            if k == "dA" and np.asarray(prm["A"]).ndim == 3:
+                res.setdefault(k, np.zeros((H, G, G)))[h] += v
             else:
-                res["dWs"] += dWs
-            if b_arr.ndim == 2:
-                res["db"][h] += db
-            else:
-                res["db"] += db
-            for k, v in dprm.items():
-                if k == "dA" and np.asarray(prm["A"]).ndim == 3:
-                    res.setdefault(k, np.zeros((H, G, G)))[h] += v
-                else:
-                    res.setdefault(k, np.zeros_like(v))
-                    res[k] += v
+                res.setdefault(k, np.zeros_like(v))
+                res[k] += v
     return res
 
 
-def run_inputs(inp: Dict, kind: int, eps: float = 1e-5, backward_too: bool = True):
+def run_inputs(inp: Dict, kind: int, eps: float = 1e-5, backward_too: bool = True,
+               pairs=None, dtype=f64):
     """Convenience: forward (+ backward) on a ``workloads.make_inputs`` dictionary."""
     prm = {k: inp.get(k) for k in ("A", "Wc", "Wq", "Wk", "Wv", "scale")}
-    fwd = forward(inp["x"], inp["fx"], inp["Ws"], inp["b"], inp["tau"], kind, prm, eps)
+    fwd = forward(inp["x"], inp["fx"], inp["Ws"], inp["b"], inp["tau"], kind, prm, eps,
+                  pairs=pairs, dtype=dtype)
     if not backward_too:
         return fwd, None
     bwd = backward(inp["x"], inp["fx"], inp["Ws"], inp["b"], inp["tau"], kind, prm,
-                   inp["dout"], eps, fwd=fwd)
+                   inp["dout"], eps, fwd=fwd, pairs=pairs, dtype=dtype)
     return fwd, bwd

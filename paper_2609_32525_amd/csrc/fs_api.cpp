@@ -1,0 +1,429 @@
+// C-ABI entry points of libflashslice: host-side validation, launch-shape selection,
+// workspace carve-up and dispatch to the HIP kernels. Every check runs before anything is
+// enqueued, and no HIP runtime call is made on an error path, so the whole validation layer
+// also works on a machine without a GPU.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <initializer_list>
+
+#include "../../include/flashslice.h"
+#include "fs_internal.h"
+
+namespace fs {
+
+namespace {
+thread_local int g_last_hip_error = 0;
+
+constexpr size_t kAlign = 256;
+size_t up(size_t v, size_t a = kAlign) { return (v + a - 1) / a * a; }
+bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
+
+constexpr int kMaxAttnG = 256;
+constexpr int kMaxAttnGV = 8192;
+}  // namespace
+
+PassCfg pick_cfg(const Geom& g, Pass pass) {
+  PassCfg c{};
+  if (g.G <= 64) {
+    c.GS = g.G;
+    c.NS = 1;
+    c.NP = 4;
+  } else {
+    c.GS = 64;
+    c.NS = g.G / 64;
+    c.NP = c.NS == 2 ? 2 : 1;
+  }
+  // Workgroups along the points per (sample, head): enough to fill 256 CUs several times,
+  // but few enough that the per-workgroup partials stay small next to the streamed data.
+  const bool partials = pass != PASS_DESLICE;
+  int target;
+  if (c.NS >= 8)
+    target = partials ? 256 : 512;
+  else
+    target = partials ? 512 : 2048;
+  const int64_t step = 32LL * c.NP;
+  const int64_t ntiles = std::max<int64_t>(1, (g.N + step - 1) / step);
+  int64_t chunks = std::max<int64_t>(1, (target + g.BH() - 1) / g.BH());
+  // passes that write partials give every chunk at least 4 tiles per point group, so the
+  // partials stay small next to the points they summarise
+  chunks = std::min<int64_t>(chunks, partials ? std::max<int64_t>(1, ntiles / 4) : ntiles);
+  int64_t tiles_per_chunk = (ntiles + chunks - 1) / chunks;
+  c.chunk_pts = tiles_per_chunk * step;
+  c.chunks = (int)std::max<int64_t>(1, (g.N + c.chunk_pts - 1) / c.chunk_pts);
+  return c;
+}
+
+size_t mix_param_count(const Geom& g, int kind, bool a_per_head) {
+  switch (kind) {
+    case FS_MIX_LINEAR_G:
+      return (size_t)(a_per_head ? g.H : 1) * g.G * g.G;
+    case FS_MIX_LINEAR_C:
+      return (size_t)g.V * g.V;
+    case FS_MIX_ATTN:
+      return 3 * (size_t)g.V * g.V;
+    default:
+      return 0;
+  }
+}
+
+FwdWs fwd_ws_layout(const Geom& g) {
+  const PassCfg c = pick_cfg(g, PASS_SLICE);
+  FwdWs L{};
+  size_t off = 0;
+  L.partU = off;
+  off += up(sizeof(float) * (size_t)g.BH() * c.chunks * g.G * g.V);
+  L.partS = off;
+  off += up(sizeof(float) * (size_t)g.BH() * c.chunks * g.G);
+  L.total = off;
+  return L;
+}
+
+BwdWs bwd_ws_layout(const Geom& g, int kind) {
+  const PassCfg ca = pick_cfg(g, PASS_BWD_A);
+  const PassCfg cb = pick_cfg(g, PASS_BWD_B);
+  const size_t tok = sizeof(float) * (size_t)g.BH() * g.G * g.V;
+  BwdWs L{};
+  size_t off = 0;
+  L.partDZ = off;
+  off += up(sizeof(float) * (size_t)g.BH() * ca.chunks * g.G * g.V);
+  L.dzm = off;
+  off += up(tok);
+  L.dz = off;
+  off += up(tok);
+  L.dU = off;
+  off += up(tok);
+  L.ds = off;
+  off += up(sizeof(float) * (size_t)g.BH() * g.G);
+  L.cen = off;
+  off += up(sizeof(float) * (size_t)g.BH() * (2 * (size_t)g.V + 1));
+  L.partP = off;
+  off += up(sizeof(float) * (size_t)g.BH() * cb.chunks * ((size_t)g.D * g.G + g.G + 2));
+  L.partM = off;
+  size_t per_bh = 0;
+  if (kind == FS_MIX_LINEAR_G) per_bh = (size_t)g.G * g.G;
+  if (kind == FS_MIX_LINEAR_C) per_bh = (size_t)g.V * g.V;
+  if (kind == FS_MIX_ATTN) per_bh = 3 * (size_t)g.V * g.V;
+  off += up(sizeof(float) * (size_t)g.BH() * per_bh);
+  L.scr = off;
+  off += up(kind == FS_MIX_ATTN ? 3 * tok : 0);
+  L.total = off;
+  return L;
+}
+
+}  // namespace fs
+
+using fs::Geom;
+
+namespace {
+
+struct Buf {
+  const void* p;
+  size_t bytes;
+  bool required;
+};
+
+int check_problem(const fs_problem* p, Geom* g) {
+  if (p == nullptr) return FS_ERR_NULL;
+  if (p->B < 1 || p->N < 0 || p->H < 1 || p->D < 1 || p->V < 1 || p->G < 1) return FS_ERR_SHAPE;
+  if (p->dtype != FS_F32 && p->dtype != FS_BF16) return FS_ERR_DTYPE;
+  if (!std::isfinite(p->eps) || p->eps < 0.f) return FS_ERR_ARG;
+  if (p->ws_per_head != 0 && p->ws_per_head != 1) return FS_ERR_ARG;
+  // what the kernels implement
+  if (p->D != p->V) return FS_ERR_UNSUPPORTED;
+  if (p->D != 16 && p->D != 32 && p->D != 64) return FS_ERR_UNSUPPORTED;
+  if (!fs::pow2(p->G) || p->G > 1024 || p->G < (p->dtype == FS_BF16 ? 32 : 16))
+    return FS_ERR_UNSUPPORTED;
+  if (p->B * (int64_t)p->H > 65535) return FS_ERR_UNSUPPORTED;
+  if (p->N > ((int64_t)1 << 40)) return FS_ERR_UNSUPPORTED;
+  g->B = p->B;
+  g->N = p->N;
+  g->H = p->H;
+  g->D = p->D;
+  g->V = p->V;
+  g->G = p->G;
+  g->bf16 = p->dtype == FS_BF16;
+  g->eps = p->eps;
+  g->ws_per_head = p->ws_per_head != 0;
+  return FS_OK;
+}
+
+int check_mix(const fs_mix_desc* m, const Geom& g) {
+  if (m == nullptr) return FS_ERR_NULL;
+  if (m->kind < FS_MIX_IDENTITY || m->kind > FS_MIX_ATTN) return FS_ERR_ARG;
+  if (m->a_per_head != 0 && m->a_per_head != 1) return FS_ERR_ARG;
+  if (m->kind == FS_MIX_LINEAR_G && m->A == nullptr) return FS_ERR_NULL;
+  if (m->kind == FS_MIX_LINEAR_C && m->Wc == nullptr) return FS_ERR_NULL;
+  if (m->kind == FS_MIX_ATTN) {
+    if (m->Wq == nullptr || m->Wk == nullptr || m->Wv == nullptr) return FS_ERR_NULL;
+    if (!std::isfinite(m->scale)) return FS_ERR_ARG;
+    if (g.G > fs::kMaxAttnG || (int64_t)g.G * g.V > fs::kMaxAttnGV) return FS_ERR_UNSUPPORTED;
+  }
+  return FS_OK;
+}
+
+fs::MixArgs mix_args(const fs_mix_desc* m) {
+  fs::MixArgs a{};
+  a.kind = m->kind;
+  a.a_per_head = m->a_per_head != 0;
+  a.A = m->A;
+  a.Wc = m->Wc;
+  a.Wq = m->Wq;
+  a.Wk = m->Wk;
+  a.Wv = m->Wv;
+  a.scale = m->scale;
+  return a;
+}
+
+// Mix parameters as buffers (inputs), for the alias check.
+void mix_bufs(const fs_mix_desc* m, const Geom& g, Buf* out, int* n) {
+  const size_t vv = sizeof(float) * (size_t)g.V * g.V;
+  *n = 0;
+  if (m->kind == FS_MIX_LINEAR_G)
+    out[(*n)++] = {m->A, sizeof(float) * (size_t)(m->a_per_head ? g.H : 1) * g.G * g.G, true};
+  if (m->kind == FS_MIX_LINEAR_C) out[(*n)++] = {m->Wc, vv, true};
+  if (m->kind == FS_MIX_ATTN) {
+    out[(*n)++] = {m->Wq, vv, true};
+    out[(*n)++] = {m->Wk, vv, true};
+    out[(*n)++] = {m->Wv, vv, true};
+  }
+}
+
+bool overlap(const Buf& a, const Buf& b) {
+  if (a.p == nullptr || b.p == nullptr || a.bytes == 0 || b.bytes == 0) return false;
+  const uintptr_t a0 = (uintptr_t)a.p, a1 = a0 + a.bytes;
+  const uintptr_t b0 = (uintptr_t)b.p, b1 = b0 + b.bytes;
+  return a0 < b1 && b0 < a1;
+}
+
+// Null, alignment and aliasing checks. Buffers of zero bytes may be anything.
+int check_bufs(const Buf* in, int nin, const Buf* out, int nout) {
+  for (int k = 0; k < nin + nout; ++k) {
+    const Buf& b = k < nin ? in[k] : out[k - nin];
+    if (b.bytes == 0) continue;
+    if (b.p == nullptr) {
+      if (b.required) return FS_ERR_NULL;
+      continue;
+    }
+    if (((uintptr_t)b.p) % 16 != 0) return FS_ERR_ALIGN;
+  }
+  for (int o = 0; o < nout; ++o) {
+    for (int k = 0; k < nin; ++k)
+      if (overlap(out[o], in[k])) return FS_ERR_ALIAS;
+    for (int k = 0; k < o; ++k)
+      if (overlap(out[o], out[k])) return FS_ERR_ALIAS;
+  }
+  return FS_OK;
+}
+
+struct Sizes {
+  size_t x, fx, Ws, b, tau, tok, s, lse, attn;
+};
+Sizes sizes(const Geom& g) {
+  const size_t elt = g.bf16 ? 2 : 4;
+  Sizes z{};
+  z.x = elt * (size_t)g.B * g.N * g.H * g.D;
+  z.fx = elt * (size_t)g.B * g.N * g.H * g.V;
+  z.Ws = sizeof(float) * (size_t)(g.ws_per_head ? g.H : 1) * g.D * g.G;
+  z.b = sizeof(float) * (size_t)(g.ws_per_head ? g.H : 1) * g.G;
+  z.tau = sizeof(float) * (size_t)g.H;
+  z.tok = sizeof(float) * (size_t)g.BH() * g.G * g.V;
+  z.s = sizeof(float) * (size_t)g.BH() * g.G;
+  z.lse = sizeof(float) * (size_t)g.BH() * g.N;
+  z.attn = sizeof(float) * (size_t)g.BH() * g.G * g.G;
+  return z;
+}
+
+// The backward workspace requirement is the one fs_workspace_bytes(prob, 1) documents: the
+// largest over all mix kinds, so one workspace serves every mix.
+size_t bwd_required(const Geom& g) {
+  size_t mx = 0;
+  for (int k = FS_MIX_IDENTITY; k <= FS_MIX_ATTN; ++k) mx = std::max(mx, fs::bwd_ws_layout(g, k).total);
+  return mx;
+}
+
+int hip_status(hipError_t e) {
+  if (e == hipSuccess) return FS_OK;
+  fs::g_last_hip_error = (int)e;
+  return FS_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fs_workspace_bytes(const fs_problem* prob, int for_backward, size_t* bytes) {
+  Geom g;
+  int st = check_problem(prob, &g);
+  if (st != FS_OK) return st;
+  if (bytes == nullptr) return FS_ERR_NULL;
+  if (for_backward) {
+    *bytes = bwd_required(g);
+  } else {
+    *bytes = fs::fwd_ws_layout(g).total;
+  }
+  return FS_OK;
+}
+
+int fs_slice_fwd(const fs_problem* prob, const void* x, const void* fx, const float* Ws,
+                 const float* bias, const float* tau, float* z, float* s, float* lse, void* ws,
+                 size_t ws_bytes, void* hip_stream) {
+  Geom g;
+  int st = check_problem(prob, &g);
+  if (st != FS_OK) return st;
+  const Sizes zs = sizes(g);
+  const fs::FwdWs L = fs::fwd_ws_layout(g);
+  const Buf in[] = {{x, zs.x, true}, {fx, zs.fx, true}, {Ws, zs.Ws, true},
+                    {bias, zs.b, true}, {tau, zs.tau, true}};
+  const Buf out[] = {{z, zs.tok, true}, {s, zs.s, true}, {lse, zs.lse, false},
+                     {ws, ws_bytes, true}};
+  st = check_bufs(in, 5, out, 4);
+  if (st != FS_OK) return st;
+  if (ws == nullptr || ws_bytes < L.total) return FS_ERR_WORKSPACE;
+  char* w = static_cast<char*>(ws);
+  return hip_status(fs::launch_slice(g, x, fx, Ws, bias, tau, z, s, lse,
+                                     reinterpret_cast<float*>(w + L.partU),
+                                     reinterpret_cast<float*>(w + L.partS),
+                                     static_cast<hipStream_t>(hip_stream)));
+}
+
+int fs_mix(const fs_problem* prob, const fs_mix_desc* mix, const float* z, float* zmix,
+           float* attn_probs, void* hip_stream) {
+  Geom g;
+  int st = check_problem(prob, &g);
+  if (st != FS_OK) return st;
+  st = check_mix(mix, g);
+  if (st != FS_OK) return st;
+  const Sizes zs = sizes(g);
+  Buf in[5];
+  int nin = 0;
+  mix_bufs(mix, g, in, &nin);
+  in[nin++] = {z, zs.tok, true};
+  const bool attn = mix->kind == FS_MIX_ATTN;
+  const Buf out[] = {{zmix, zs.tok, true}, {attn ? attn_probs : nullptr, attn ? zs.attn : 0, true}};
+  st = check_bufs(in, nin, out, 2);
+  if (st != FS_OK) return st;
+  return hip_status(fs::launch_mix(g, mix_args(mix), z, zmix, attn_probs,
+                                   static_cast<hipStream_t>(hip_stream)));
+}
+
+int fs_mix_bwd(const fs_problem* prob, const fs_mix_desc* mix, const float* z,
+               const float* attn_probs, const float* dzmix, float* dz, float* dmix_params,
+               void* ws, size_t ws_bytes, void* hip_stream) {
+  Geom g;
+  int st = check_problem(prob, &g);
+  if (st != FS_OK) return st;
+  st = check_mix(mix, g);
+  if (st != FS_OK) return st;
+  const Sizes zs = sizes(g);
+  const fs::BwdWs L = fs::bwd_ws_layout(g, mix->kind);
+  const bool attn = mix->kind == FS_MIX_ATTN;
+  Buf in[7];
+  int nin = 0;
+  mix_bufs(mix, g, in, &nin);
+  in[nin++] = {z, zs.tok, true};
+  in[nin++] = {dzmix, zs.tok, true};
+  in[nin++] = {attn ? attn_probs : nullptr, attn ? zs.attn : 0, true};
+  const size_t np = sizeof(float) * fs::mix_param_count(g, mix->kind, mix->a_per_head != 0);
+  const Buf out[] = {{dz, zs.tok, true}, {dmix_params, np, false}, {ws, ws_bytes, true}};
+  st = check_bufs(in, nin, out, 3);
+  if (st != FS_OK) return st;
+  if (ws == nullptr || ws_bytes < bwd_required(g)) return FS_ERR_WORKSPACE;
+  char* w = static_cast<char*>(ws);
+  return hip_status(fs::launch_mix_bwd(
+      g, mix_args(mix), z, nullptr, attn_probs, dzmix, dz, nullptr, nullptr,
+      reinterpret_cast<float*>(w + L.scr), reinterpret_cast<float*>(w + L.partM),
+      mix->kind == FS_MIX_IDENTITY ? nullptr : dmix_params, static_cast<hipStream_t>(hip_stream)));
+}
+
+int fs_deslice_fwd(const fs_problem* prob, const void* x, const float* Ws, const float* bias,
+                   const float* tau, const float* zmix, const float* lse, void* out,
+                   void* hip_stream) {
+  Geom g;
+  int st = check_problem(prob, &g);
+  if (st != FS_OK) return st;
+  const Sizes zs = sizes(g);
+  const Buf in[] = {{x, zs.x, true},     {Ws, zs.Ws, true},     {bias, zs.b, true},
+                    {tau, zs.tau, true}, {zmix, zs.tok, true},  {lse, zs.lse, true}};
+  const Buf outb[] = {{out, zs.fx, true}};
+  st = check_bufs(in, 6, outb, 1);
+  if (st != FS_OK) return st;
+  return hip_status(fs::launch_deslice(g, x, Ws, bias, tau, zmix, lse, out,
+                                       static_cast<hipStream_t>(hip_stream)));
+}
+
+int fs_slice_deslice_bwd(const fs_problem* prob, const fs_mix_desc* mix, const void* x,
+                         const void* fx, const float* Ws, const float* bias, const float* tau,
+                         const float* z, const float* s, const float* zmix,
+                         const float* attn_probs, const float* lse, const void* dout, void* dx,
+                         void* dfx, float* dWs, float* dbias, float* dtau, float* dmix_params,
+                         float* dzmix_out, void* ws, size_t ws_bytes, void* hip_stream) {
+  Geom g;
+  int st = check_problem(prob, &g);
+  if (st != FS_OK) return st;
+  st = check_mix(mix, g);
+  if (st != FS_OK) return st;
+  const Sizes zs = sizes(g);
+  const fs::BwdWs L = fs::bwd_ws_layout(g, mix->kind);
+  const bool attn = mix->kind == FS_MIX_ATTN;
+  Buf in[16];
+  int nin = 0;
+  mix_bufs(mix, g, in, &nin);
+  in[nin++] = {x, zs.x, true};
+  in[nin++] = {fx, zs.fx, true};
+  in[nin++] = {Ws, zs.Ws, true};
+  in[nin++] = {bias, zs.b, true};
+  in[nin++] = {tau, zs.tau, true};
+  in[nin++] = {z, zs.tok, true};
+  in[nin++] = {s, zs.s, true};
+  in[nin++] = {zmix, zs.tok, true};
+  in[nin++] = {attn ? attn_probs : nullptr, attn ? zs.attn : 0, true};
+  in[nin++] = {lse, zs.lse, true};
+  in[nin++] = {dout, zs.fx, true};
+  const size_t np = sizeof(float) * fs::mix_param_count(g, mix->kind, mix->a_per_head != 0);
+  const Buf out[] = {{dx, zs.x, true},          {dfx, zs.fx, true},       {dWs, zs.Ws, true},
+                     {dbias, zs.b, true},       {dtau, zs.tau, true},     {dmix_params, np, false},
+                     {dzmix_out, zs.tok, false}, {ws, ws_bytes, true}};
+  st = check_bufs(in, nin, out, 8);
+  if (st != FS_OK) return st;
+  if (ws == nullptr || ws_bytes < bwd_required(g)) return FS_ERR_WORKSPACE;
+  return hip_status(fs::launch_bwd(g, mix_args(mix), x, fx, Ws, bias, tau, z, s, zmix,
+                                   attn_probs, lse, dout, dx, dfx, dWs, dbias, dtau,
+                                   mix->kind == FS_MIX_IDENTITY ? nullptr : dmix_params,
+                                   dzmix_out, static_cast<char*>(ws),
+                                   static_cast<hipStream_t>(hip_stream)));
+}
+
+const char* fs_status_string(int status) {
+  switch (status) {
+    case FS_OK:
+      return "ok";
+    case FS_ERR_NULL:
+      return "a required pointer is NULL";
+    case FS_ERR_SHAPE:
+      return "invalid sizes";
+    case FS_ERR_DTYPE:
+      return "unknown storage dtype";
+    case FS_ERR_UNSUPPORTED:
+      return "shape not supported by this library";
+    case FS_ERR_WORKSPACE:
+      return "workspace missing or too small";
+    case FS_ERR_ARG:
+      return "invalid argument";
+    case FS_ERR_ALIGN:
+      return "device pointer not 16-byte aligned";
+    case FS_ERR_ALIAS:
+      return "an output overlaps an input or another output";
+    case FS_ERR_HIP:
+      return "HIP runtime error";
+    default:
+      return "unknown status";
+  }
+}
+
+int fs_last_hip_error(void) { return fs::g_last_hip_error; }
+
+}  // extern "C"

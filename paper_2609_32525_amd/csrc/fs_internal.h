@@ -1,0 +1,77 @@
+// Internal interface between the C-ABI host layer (fs_api.cpp) and the HIP kernels
+// (fs_kernels.hip). Not installed; no torch types anywhere.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace fs {
+
+// Problem geometry after validation.
+struct Geom {
+  int64_t B, N;
+  int H, D, V, G;
+  bool bf16;
+  float eps;
+  bool ws_per_head;
+  int BH() const { return (int)(B * H); }
+};
+
+enum Pass { PASS_SLICE = 0, PASS_DESLICE = 1, PASS_BWD_A = 2, PASS_BWD_B = 3 };
+
+// Launch shape of one streaming pass over the points.
+//   GS: slots owned by one wavefront; NS = G / GS wavefronts share each point tile;
+//   NP: independent point groups per workgroup; a workgroup has NS * NP wavefronts.
+//   chunks: workgroups per (sample, head) along the points, each covering chunk_pts points.
+struct PassCfg {
+  int GS, NS, NP;
+  int chunks;
+  int64_t chunk_pts;
+};
+
+PassCfg pick_cfg(const Geom& g, Pass pass);
+
+// Workspace carve-up (byte offsets, 256-byte aligned).
+struct FwdWs {
+  size_t partU, partS, total;
+};
+struct BwdWs {
+  size_t partDZ, dzm, dz, dU, ds, cen, partP, partM, scr, total;
+};
+FwdWs fwd_ws_layout(const Geom& g);
+BwdWs bwd_ws_layout(const Geom& g, int mix_kind);
+size_t mix_param_count(const Geom& g, int mix_kind, bool a_per_head);
+
+struct MixArgs {
+  int kind;
+  bool a_per_head;
+  const float* A;
+  const float* Wc;
+  const float* Wq;
+  const float* Wk;
+  const float* Wv;
+  float scale;
+};
+
+// Launchers; each returns the hipError_t of its launches.
+hipError_t launch_slice(const Geom& g, const void* x, const void* fx, const float* Ws,
+                        const float* bias, const float* tau, float* z, float* s, float* lse,
+                        float* partU, float* partS, hipStream_t st);
+hipError_t launch_deslice(const Geom& g, const void* x, const float* Ws, const float* bias,
+                          const float* tau, const float* zmix, const float* lse, void* out,
+                          hipStream_t st);
+hipError_t launch_mix(const Geom& g, const MixArgs& m, const float* z, float* zmix,
+                      float* attn, hipStream_t st);
+// dz = Mix^T(dzm); with s given also dU = dz / (s + eps) and ds; per-(b,h) parameter
+// partials into partM, reduced into dmix (nullable). scr: attention scratch [BH][3][G][V].
+hipError_t launch_mix_bwd(const Geom& g, const MixArgs& m, const float* z, const float* s,
+                          const float* attn, const float* dzm, float* dz, float* dU, float* ds,
+                          float* scr, float* partM, float* dmix, hipStream_t st);
+hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void* fx,
+                      const float* Ws, const float* bias, const float* tau, const float* z,
+                      const float* s, const float* zmix, const float* attn, const float* lse,
+                      const void* dout, void* dx, void* dfx, float* dWs, float* dbias,
+                      float* dtau, float* dmix, float* dzm_out, char* ws, hipStream_t st);
+
+}  // namespace fs

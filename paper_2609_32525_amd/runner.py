@@ -1,0 +1,123 @@
+"""Device buffers for one problem and the calls of one forward + backward through the C ABI.
+
+PyTorch supplies device memory and the stream; the binding passes raw pointers. Nothing here
+computes any part of the path.
+"""
+from __future__ import annotations
+
+from typing import Dict, Optional
+
+import numpy as np
+
+from . import (BF16, F32, MIX_ATTN, MIX_IDENTITY, MIX_LINEAR_C, MIX_LINEAR_G, MixDesc, Problem,
+               deslice_fwd, mix, slice_deslice_bwd, slice_fwd, workspace_bytes)
+
+
+class PathBuffers:
+    """Inputs uploaded once, outputs preallocated; forward() / backward() only launch.
+
+    inp: dict of fp32 numpy arrays holding the exact stored values (x, fx, Ws, b, tau, the
+    mix parameters, scale, dout), as produced by the seeded input generators.
+    """
+
+    def __init__(self, inp: Dict, kind: int, dtype: str = "f32", eps: float = 1e-5,
+                 device: str = "cuda:0", with_backward: bool = True):
+        import torch
+        self.torch = torch
+        self.dev = torch.device(device)
+        self.kind = kind
+        sdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+        self.sdt = sdt
+        x = inp["x"]
+        B, N, H, D = x.shape
+        V = inp["fx"].shape[3]
+        Ws = np.asarray(inp["Ws"])
+        G = Ws.shape[-1]
+        self.shape = (B, N, H, D, V, G)
+        self.prob = Problem.make(B, N, H, D, V, G, BF16 if dtype == "bf16" else F32, eps,
+                                 1 if Ws.ndim == 3 else 0)
+
+        def up(a, dt=torch.float32):
+            return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(self.dev).to(dt)
+
+        self.x = up(x, sdt)
+        self.fx = up(inp["fx"], sdt)
+        self.Ws = up(Ws)
+        self.b = up(inp["b"])
+        self.tau = up(inp["tau"])
+        self.params = {}
+        for k in ("A", "Wc", "Wq", "Wk", "Wv"):
+            if inp.get(k) is not None:
+                self.params[k] = up(inp[k])
+        scale = float(inp.get("scale") if inp.get("scale") is not None else 1.0)
+        A = self.params.get("A")
+        self.mixdesc = MixDesc.make(kind, A=A, Wc=self.params.get("Wc"),
+                                    Wq=self.params.get("Wq"), Wk=self.params.get("Wk"),
+                                    Wv=self.params.get("Wv"), scale=scale,
+                                    a_per_head=1 if (A is not None and A.dim() == 3) else 0)
+        f32 = dict(device=self.dev, dtype=torch.float32)
+        self.z = torch.empty((B, H, G, V), **f32)
+        self.s = torch.empty((B, H, G), **f32)
+        self.zmix = torch.empty((B, H, G, V), **f32)
+        self.attn = torch.empty((B, H, G, G), **f32) if kind == MIX_ATTN else None
+        self.lse = torch.empty((B, H, N), **f32)
+        self.out = torch.empty((B, N, H, V), device=self.dev, dtype=sdt)
+        self.ws_f = torch.empty(max(1, workspace_bytes(self.prob, False)), device=self.dev,
+                                dtype=torch.uint8)
+        self.with_backward = with_backward
+        if with_backward:
+            self.dout = up(inp["dout"], sdt)
+            self.dx = torch.empty((B, N, H, D), device=self.dev, dtype=sdt)
+            self.dfx = torch.empty((B, N, H, V), device=self.dev, dtype=sdt)
+            self.dWs = torch.empty_like(self.Ws)
+            self.db = torch.empty_like(self.b)
+            self.dtau = torch.empty_like(self.tau)
+            self.dzmix = torch.empty((B, H, G, V), **f32)
+            nparam = {MIX_IDENTITY: 0, MIX_LINEAR_G: A.numel() if A is not None else 0,
+                      MIX_LINEAR_C: V * V, MIX_ATTN: 3 * V * V}[kind]
+            self.dmix = torch.empty(max(nparam, 1), **f32) if nparam else None
+            self.ws_b = torch.empty(max(1, workspace_bytes(self.prob, True)), device=self.dev,
+                                    dtype=torch.uint8)
+
+    # ---- launches ------------------------------------------------------------------------
+    def forward(self, stream=None) -> None:
+        slice_fwd(self.prob, self.x, self.fx, self.Ws, self.b, self.tau, self.z, self.s,
+                  self.lse, self.ws_f, stream=stream)
+        mix(self.prob, self.mixdesc, self.z, self.zmix, self.attn, stream=stream)
+        deslice_fwd(self.prob, self.x, self.Ws, self.b, self.tau, self.zmix, self.lse,
+                    self.out, stream=stream)
+
+    def backward(self, stream=None) -> None:
+        slice_deslice_bwd(self.prob, self.mixdesc, self.x, self.fx, self.Ws, self.b, self.tau,
+                          self.z, self.s, self.zmix, self.attn, self.lse, self.dout, self.dx,
+                          self.dfx, self.dWs, self.db, self.dtau, self.dmix, self.dzmix,
+                          self.ws_b, stream=stream)
+
+    def step(self, stream=None) -> None:
+        self.forward(stream)
+        if self.with_backward:
+            self.backward(stream)
+
+    # ---- results as fp64 numpy -------------------------------------------------------------
+    def results(self) -> Dict[str, Optional[np.ndarray]]:
+        self.torch.cuda.synchronize(self.dev)
+
+        def h(t):
+            return None if t is None else t.detach().float().cpu().numpy().astype(np.float64)
+
+        r = dict(z=h(self.z), s=h(self.s), zmix=h(self.zmix), P=h(self.attn), lse=h(self.lse),
+                 out=h(self.out))
+        if self.with_backward:
+            r.update(dx=h(self.dx), dfx=h(self.dfx), dWs=h(self.dWs), db=h(self.db),
+                     dtau=h(self.dtau), dzmix=h(self.dzmix))
+            if self.dmix is not None:
+                d = h(self.dmix)
+                if self.kind == MIX_LINEAR_G:
+                    r["dA"] = d.reshape(self.params["A"].shape)
+                elif self.kind == MIX_LINEAR_C:
+                    r["dWc"] = d.reshape(self.params["Wc"].shape)
+                elif self.kind == MIX_ATTN:
+                    V = self.shape[4]
+                    r["dWq"], r["dWk"], r["dWv"] = d[: V * V].reshape(V, V), \
+                        d[V * V: 2 * V * V].reshape(V, V), d[2 * V * V:].reshape(V, V)
+        return r

@@ -1,0 +1,199 @@
+"""Host-side contract of libflashslice (CPU only: no call here reaches a kernel launch).
+
+Every entry point validates its arguments before enqueuing anything, so these tests pass
+fake (never dereferenced) device addresses and check the status codes.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_32525_amd as fs
+from paper_2609_32525_amd import MixDesc, Problem
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "flashslice.h")
+
+OK, NULL, SHAPE, DTYPE, UNSUP, WS, ARG, ALIGN, ALIAS, HIP = 0, -1, -2, -3, -4, -5, -6, -7, -8, -9
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.device_count() > 0   # counts devices without initialising them
+    except Exception:
+        return False
+
+
+# These tests hand fake addresses to the library: they must never run where a kernel could
+# actually be launched on a GPU.
+pytestmark = [
+    pytest.mark.skipif(not os.path.exists(fs.lib_path()), reason="libflashslice.so not built"),
+    pytest.mark.skipif(_gpu_visible(), reason="fake-pointer validation tests run without a GPU"),
+]
+
+
+def declared_symbols():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(fs_[a-z_]+)\s*\(", txt)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_symbols()
+    assert set(names) == set(fs.EXPORTED), names
+    L = fs.lib()
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_status_strings():
+    for code in (OK, NULL, SHAPE, DTYPE, UNSUP, WS, ARG, ALIGN, ALIAS, HIP):
+        s = fs.status_string(code)
+        assert s and s != "unknown status"
+    assert fs.status_string(-100) == "unknown status"
+    assert fs.last_hip_error() == 0
+
+
+class Fake:
+    """Distinct, far-apart, 256-byte aligned fake device addresses."""
+
+    def __init__(self):
+        self.k = 0
+
+    def __call__(self, off=0):
+        self.k += 1
+        return (1 << 44) + self.k * (1 << 36) + off
+
+
+def prob(B=1, N=4096, H=8, D=32, V=32, G=32, dtype=0, eps=1e-5, per_head=0):
+    return Problem.make(B, N, H, D, V, G, dtype, eps, per_head)
+
+
+def ws_bytes(p, bwd):
+    out = ctypes.c_size_t(0)
+    st = fs.lib().fs_workspace_bytes(ctypes.byref(p), bwd, ctypes.byref(out))
+    return st, out.value
+
+
+def call_slice(p, f, **over):
+    a = dict(x=f(), fx=f(), Ws=f(), b=f(), tau=f(), z=f(), s=f(), lse=f(), ws=f())
+    a.update(over)
+    _, need = ws_bytes(p, 0)
+    nb = over.pop("ws_bytes", None)
+    return fs.lib().fs_slice_fwd(ctypes.byref(p), a["x"], a["fx"], a["Ws"], a["b"], a["tau"],
+                                 a["z"], a["s"], a["lse"], a["ws"],
+                                 need if nb is None else nb, None)
+
+
+def test_workspace_formula_bounded():
+    for (N, G, dt) in [(4096, 32, 0), (32768, 32, 0), (1 << 20, 64, 1), (1 << 18, 1024, 1),
+                       (1 << 17, 64, 0)]:
+        p = prob(N=N, G=G, dtype=dt, B=4 if N == (1 << 17) else 1)
+        for bwd in (0, 1):
+            st, n = ws_bytes(p, bwd)
+            assert st == OK and n > 0
+            # never an N x G tensor: far below the slice-weight size
+            elt = 2 if dt else 4
+            frac = 4 if N >= 32768 else 2
+            assert n < p.B * N * p.H * G * elt / frac, (N, G, bwd, n)
+    # does not grow with N once the workgroup count saturates
+    _, a = ws_bytes(prob(N=1 << 20, G=64, dtype=1), 1)
+    _, b = ws_bytes(prob(N=1 << 24, G=64, dtype=1), 1)
+    assert a == b
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(B=0), SHAPE), (dict(N=-1), SHAPE), (dict(H=0), SHAPE), (dict(G=0), SHAPE),
+    (dict(dtype=7), DTYPE), (dict(eps=-1.0), ARG), (dict(eps=float("nan")), ARG),
+    (dict(per_head=3), ARG), (dict(D=24, V=24), UNSUP), (dict(D=32, V=16), UNSUP),
+    (dict(G=48), UNSUP), (dict(G=2048), UNSUP), (dict(G=16, dtype=1), UNSUP),
+    (dict(G=8), UNSUP), (dict(B=70000), UNSUP),
+])
+def test_problem_validation(kw, code):
+    f = Fake()
+    p = prob(**kw)
+    assert call_slice(p, f) == code
+    st, _ = ws_bytes(p, 1)
+    assert st == code
+
+
+def test_null_problem():
+    out = ctypes.c_size_t(0)
+    assert fs.lib().fs_workspace_bytes(None, 0, ctypes.byref(out)) == NULL
+    assert fs.lib().fs_workspace_bytes(ctypes.byref(prob()), 0, None) == NULL
+
+
+def test_buffer_validation_slice():
+    f = Fake()
+    p = prob()
+    assert call_slice(p, f, x=None) == NULL
+    assert call_slice(p, f, tau=None) == NULL
+    assert call_slice(p, f, x=f(4)) == ALIGN
+    x = f()
+    assert call_slice(p, f, x=x, z=x + 64) == ALIAS          # output inside an input
+    z = f()
+    assert call_slice(p, f, z=z, s=z + 256) == ALIAS          # two outputs overlap
+    assert call_slice(p, f, ws_bytes=16) == WS
+    assert call_slice(p, f, ws=None, ws_bytes=0) == WS
+    # lse is optional: NULL lse with a too-small workspace still reaches the workspace check
+    assert call_slice(p, f, lse=None, ws_bytes=16) == WS
+
+
+def test_empty_point_set_buffers_may_be_null():
+    # N = 0: x, fx and lse have zero bytes, so NULL is accepted; the workspace check still runs
+    f = Fake()
+    p = prob(N=0)
+    assert call_slice(p, f, x=None, fx=None, lse=None, ws_bytes=1) == WS
+
+
+def test_mix_validation():
+    f = Fake()
+    L = fs.lib()
+    p = prob()
+    z, zm = f(), f()
+    bad = MixDesc.make(9)
+    assert L.fs_mix(ctypes.byref(p), ctypes.byref(bad), z, zm, None, None) == ARG
+    nullA = MixDesc.make(fs.MIX_LINEAR_G)
+    assert L.fs_mix(ctypes.byref(p), ctypes.byref(nullA), z, zm, None, None) == NULL
+    assert L.fs_mix(ctypes.byref(p), None, z, zm, None, None) == NULL
+    attn = MixDesc.make(fs.MIX_ATTN, Wq=f(), Wk=f(), Wv=f(), scale=0.1)
+    assert L.fs_mix(ctypes.byref(p), ctypes.byref(attn), z, zm, None, None) == NULL  # no P
+    big = prob(G=512)
+    assert L.fs_mix(ctypes.byref(big), ctypes.byref(attn), z, zm, f(), None) == UNSUP
+    A = f()
+    lin = MixDesc.make(fs.MIX_LINEAR_G, A=A)
+    assert L.fs_mix(ctypes.byref(p), ctypes.byref(lin), z, A, None, None) == ALIAS
+    assert L.fs_mix(ctypes.byref(p), ctypes.byref(lin), z, z, None, None) == ALIAS
+    inf_scale = MixDesc.make(fs.MIX_ATTN, Wq=f(), Wk=f(), Wv=f(), scale=float("inf"))
+    assert L.fs_mix(ctypes.byref(p), ctypes.byref(inf_scale), z, zm, f(), None) == ARG
+
+
+def test_backward_validation():
+    f = Fake()
+    L = fs.lib()
+    p = prob()
+    lin = MixDesc.make(fs.MIX_LINEAR_G, A=f())
+    _, need = ws_bytes(p, 1)
+
+    def call(**over):
+        a = {k: f() for k in ("x", "fx", "Ws", "b", "tau", "z", "s", "zmix", "attn", "lse",
+                              "dout", "dx", "dfx", "dWs", "db", "dtau", "dmix", "dzm", "ws")}
+        nb = over.pop("ws_bytes", need)
+        a.update(over)
+        return L.fs_slice_deslice_bwd(
+            ctypes.byref(p), ctypes.byref(lin), a["x"], a["fx"], a["Ws"], a["b"], a["tau"],
+            a["z"], a["s"], a["zmix"], a["attn"], a["lse"], a["dout"], a["dx"], a["dfx"],
+            a["dWs"], a["db"], a["dtau"], a["dmix"], a["dzm"], a["ws"], nb, None)
+
+    assert call(ws_bytes=need - 1) == WS
+    assert call(lse=None) == NULL
+    assert call(dmix=None, dzm=None, ws_bytes=0) == WS       # optional outputs may be NULL
+    assert call(dx=f(8)) == ALIGN
+    x = f()
+    assert call(x=x, dx=x) == ALIAS
+    dfx = f()
+    assert call(dfx=dfx, dtau=dfx + 1024) == ALIAS
+    # the mix backward alone
+    assert L.fs_mix_bwd(ctypes.byref(p), ctypes.byref(lin), f(), None, f(), f(), f(), f(), 0,
+                        None) == WS
