@@ -1,0 +1,235 @@
+#!/usr/bin/env python3
+"""Throughput of the fused slice -> token mix -> deslice path, forward + backward, on one MI355X.
+
+One step = fs_slice_fwd, fs_mix, fs_deslice_fwd and fs_slice_deslice_bwd (which includes the
+mix backward) over one batch of seeded synthetic inputs already resident in device memory.
+The default workload is the car-surface-scale layer (fp32, B=1, N=32768 points, H=8 heads,
+dh=32, G=32 slices, single-head token self-attention). Prints ONE JSON line.
+
+Besides the step time it reports, for the dominant kernel (backward pass B), the roofline
+point from algorithmic bytes or MFMA flops per launch over its average duration measured with
+HIP events recorded around its launch on the stream it runs on, and the fp64 oracle timed on
+the host cores as a CPU baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("points/sec fused slice+deslice fwd+bwd; % HBM BW (small G) / % MFMA (large G)")
+HBM_PEAK = 8.0e12
+MFMA_PEAK = {"f32": 157.3e12, "bf16": 2.5e15}
+PASS_NAMES = ("slice", "deslice", "bwd_a", "bwd_b")
+KERNEL_NAMES = {"slice": "k_slice", "deslice": "k_deslice", "bwd_a": "k_bwd_a", "bwd_b": "k_bwd_b"}
+MIX_NAMES = {0: "identity", 1: "fixed GxG matrix", 2: "per-token channel map",
+             3: "single-head GxG self-attention"}
+
+
+def pass_work(w, pass_name):
+    """Algorithmic HBM bytes and MFMA flops of one streaming pass per (point, head).
+
+    bytes: the pass's point-tensor reads and writes in the storage dtype plus the 4-byte lse;
+    flops: its dense contractions (logits 2DG, each token contraction 2GV or 2DG).
+    """
+    elt = 2 if w.dtype == "bf16" else 4
+    D, V, G = w.D, w.V, w.G
+    if pass_name == "slice":      # read x, fx; write lse; logits + U
+        return (D + V) * elt + 4, 2 * D * G + 2 * G * V
+    if pass_name == "deslice":    # read x, lse; write out; logits + w zmix
+        return (D + V) * elt + 4, 2 * D * G + 2 * G * V
+    if pass_name == "bwd_a":      # read x, dout, lse; logits + w^T dout
+        return (D + V) * elt + 4, 2 * D * G + 2 * G * V
+    # bwd_b: read x, fx, dout, lse; write dx, dfx; logits, dw (2 GV), dfx, dx, dW_s
+    return (2 * D + 3 * V) * elt + 4, 6 * D * G + 6 * G * V
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("fs_kernels.hip", "fs_tokens.hip", "fs_api.cpp", "fs_internal.h"):
+        with open(os.path.join(ROOT, "paper_2609_32525_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was taken on
+    the current kernel sources; otherwise None."""
+    path = os.path.join(ROOT, "profiles", f"pmc_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        d = json.load(fh)
+    if d.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return d.get("traffic_bytes_per_launch")
+
+
+def cpu_baseline(w, budget_s=10.0):
+    """The fp64 oracle (unchanged) on the same workload, timed on the host cores."""
+    try:
+        libc = ctypes.CDLL("libc.so.6")
+        libc.mallopt(-4, 0)
+        libc.mallopt(-1, 2 ** 31 - 1)
+    except OSError:
+        pass
+    threads = int(os.environ.get("ORACLE_BLAS_THREADS", "8"))
+    from threadpoolctl import threadpool_info, threadpool_limits
+    import oracle
+    import workloads
+    with threadpool_limits(threads):
+        used = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        inp = workloads.make_inputs(w)
+        runs, t_total = 0, 0.0
+        while runs == 0 or (t_total < budget_s and runs < 500):
+            t0 = time.perf_counter()
+            oracle.run_inputs(inp, w.mix, w.eps)
+            t_total += time.perf_counter() - t0
+            runs += 1
+    pts = w.B * w.N * runs
+    return {"value": pts / t_total, "unit": "points/s", "cores": used, "kind": "oracle",
+            "sample": f"whole workload (B={w.B}, N={w.N}, all {w.H} heads), forward + "
+                      f"backward in fp64, {runs} run(s), {t_total:.1f} s",
+            "cpu": platform.processor() or platform.machine()}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="surface")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay each step as one captured HIP graph")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the point-sharded "
+              "all-reduce design is described in DESIGN.md); run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import workloads
+    import paper_2609_32525_amd as fs
+    from paper_2609_32525_amd.runner import PathBuffers
+
+    w = workloads.WORKLOADS[args.workload]
+    inp = workloads.make_inputs(w)
+    pb = PathBuffers(inp, w.mix, w.dtype, w.eps)
+    dev = pb.dev
+    stream = torch.cuda.current_stream(dev)
+
+    graph = None
+    if args.graph:
+        s = torch.cuda.Stream(dev)
+        s.wait_stream(stream)
+        with torch.cuda.stream(s):
+            for _ in range(3):
+                pb.step()
+        stream.wait_stream(s)
+        torch.cuda.synchronize(dev)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            pb.step()
+        torch.cuda.synchronize(dev)
+
+    def step():
+        if graph is not None:
+            graph.replay()
+        else:
+            pb.step()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize(dev)
+
+    # timed region: exactly K steps, synchronised on both sides
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize(dev)
+    wall0 = time.perf_counter()
+    t0.record(stream)
+    for _ in range(args.steps):
+        step()
+    t1.record(stream)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - wall0
+    ms_step = t0.elapsed_time(t1) / args.steps
+
+    # per-kernel durations: events recorded around each streaming kernel's launch, on its
+    # stream, over the same number of eager steps
+    ev = {p: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)] for p in range(4)}
+    for p in range(4):      # torch creates the underlying hipEvent_t on first record
+        for a, b in ev[p]:
+            a.record(stream)
+            b.record(stream)
+    torch.cuda.synchronize(dev)
+    for k in range(args.steps):
+        for p in range(4):
+            fs.set_pass_events(p, ev[p][k][0], ev[p][k][1])
+        pb.step()
+    fs.set_pass_events(-1)
+    torch.cuda.synchronize(dev)
+    pass_us = {PASS_NAMES[p]: 1e3 * float(np.mean([a.elapsed_time(b) for a, b in ev[p]]))
+               for p in range(4)}
+
+    units = w.B * w.N * w.H   # (point, head) pairs per launch
+    dom = max(pass_us, key=pass_us.get)
+    byt, flp = pass_work(w, dom)
+    t_dom = pass_us[dom] * 1e-6
+    t_hbm = byt * units / HBM_PEAK
+    t_mfma = flp * units / MFMA_PEAK[w.dtype]
+    if t_hbm >= t_mfma:
+        roof = {"bound": "hbm", "achieved": byt * units / t_dom / 1e9, "peak": HBM_PEAK / 1e9,
+                "unit": "GB/s"}
+    else:
+        roof = {"bound": "mfma", "achieved": flp * units / t_dom / 1e12,
+                "peak": MFMA_PEAK[w.dtype] / 1e12, "unit": "TFLOP/s"}
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = measured_traffic(args.workload, KERNEL_NAMES[dom])
+    roof["kernel"] = KERNEL_NAMES[dom]
+    roof["per_launch"] = {"units": units, "algorithmic_bytes": byt * units,
+                          "algorithmic_flops": flp * units, "avg_duration_us": pass_us[dom]}
+
+    # whole step against the path's own ceilings (4 passes)
+    elt = 2 if w.dtype == "bf16" else 4
+    step_bytes = ((5 * w.D + 6 * w.V) * elt + 12) * units
+    step_flops = 12 * w.G * (w.D + w.V) * units
+    t_step = ms_step * 1e-3
+    step_roof = {"hbm_frac": step_bytes / t_step / HBM_PEAK,
+                 "mfma_frac": step_flops / t_step / MFMA_PEAK[w.dtype],
+                 "t_hbm_us": step_bytes / HBM_PEAK * 1e6,
+                 "t_mfma_us": step_flops / MFMA_PEAK[w.dtype] * 1e6}
+
+    value = w.B * w.N / t_step
+    out = {
+        "metric": METRIC, "value": value, "unit": "points/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "N": w.N, "H": w.H, "dh": w.D, "G": w.G,
+                   "mix": MIX_NAMES[w.mix], "storage": w.dtype, "graph": bool(args.graph)},
+        "roofline": roof,
+        "step_roofline": step_roof,
+        "passes_us": pass_us,
+        "wall_s_timed": wall,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -148,6 +148,14 @@ int fs_slice_deslice_bwd(const fs_problem* prob, const fs_mix_desc* mix, const v
                          float* dmix_params, float* dzmix_out, void* ws, size_t ws_bytes,
                          void* hip_stream);
 
+/* Measurement aid: for calls made later on this thread, record the caller's hipEvent_t
+ * `before` immediately before, and `after` immediately after, the launch of the streaming
+ * kernel of `pass` (0 slice, 1 deslice, 2 backward pass A, 3 backward pass B), on the stream
+ * of that call. Each pass has its own pair; either event may be NULL; pass = -1 clears all
+ * pairs. The events are only recorded (hipEventRecord), never synchronised or destroyed by
+ * the library. Returns FS_ERR_ARG for an unknown pass.                                      */
+int fs_set_pass_events(int pass, void* before, void* after);
+
 /* Static text for a status code. */
 const char* fs_status_string(int status);
 

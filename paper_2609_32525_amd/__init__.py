@@ -17,14 +17,17 @@ __all__ = [
     "F32", "BF16", "MIX_IDENTITY", "MIX_LINEAR_G", "MIX_LINEAR_C", "MIX_ATTN",
     "FsError", "Problem", "MixDesc", "lib", "lib_path", "workspace_bytes", "slice_fwd", "mix",
     "mix_bwd", "deslice_fwd", "slice_deslice_bwd", "status_string", "last_hip_error",
-    "EXPORTED",
+    "set_pass_events", "EXPORTED", "PASS_SLICE", "PASS_DESLICE", "PASS_BWD_A", "PASS_BWD_B",
 ]
 
 F32, BF16 = 0, 1
 MIX_IDENTITY, MIX_LINEAR_G, MIX_LINEAR_C, MIX_ATTN = 0, 1, 2, 3
 
 EXPORTED = ("fs_workspace_bytes", "fs_slice_fwd", "fs_mix", "fs_mix_bwd", "fs_deslice_fwd",
-            "fs_slice_deslice_bwd", "fs_status_string", "fs_last_hip_error")
+            "fs_slice_deslice_bwd", "fs_set_pass_events", "fs_status_string",
+            "fs_last_hip_error")
+
+PASS_SLICE, PASS_DESLICE, PASS_BWD_A, PASS_BWD_B = 0, 1, 2, 3
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 
@@ -90,6 +93,7 @@ def lib() -> ctypes.CDLL:
         L.fs_status_string.argtypes = [ctypes.c_int]
         L.fs_status_string.restype = ctypes.c_char_p
         L.fs_last_hip_error.argtypes = []
+        L.fs_set_pass_events.argtypes = [ctypes.c_int, P, P]
         for name in EXPORTED:
             if name not in ("fs_status_string",):
                 getattr(L, name).restype = ctypes.c_int
@@ -131,6 +135,16 @@ def status_string(status: int) -> str:
 
 def last_hip_error() -> int:
     return lib().fs_last_hip_error()
+
+
+def set_pass_events(pass_id: int, before=None, after=None) -> None:
+    """Record torch.cuda.Event objects (or raw hipEvent_t ints) around one streaming pass of
+    later calls on this thread; pass_id = -1 clears."""
+    def ev(e):
+        if e is None or isinstance(e, int):
+            return e
+        return e.cuda_event
+    _check(lib().fs_set_pass_events(pass_id, ev(before), ev(after)), "fs_set_pass_events")
 
 
 def workspace_bytes(prob: Problem, for_backward: bool) -> int:

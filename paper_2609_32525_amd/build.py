@@ -8,7 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libflashslice.so")
-SOURCES = [os.path.join(HERE, "csrc", "fs_kernels.hip"), os.path.join(HERE, "csrc", "fs_api.cpp")]
+SOURCES = [os.path.join(HERE, "csrc", f) for f in ("fs_kernels.hip", "fs_tokens.hip", "fs_api.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in the generated code.

@@ -26,6 +26,11 @@ constexpr int kMaxAttnG = 256;
 constexpr int kMaxAttnGV = 8192;
 }  // namespace
 
+PassEvents& pass_events() {
+  static thread_local PassEvents ev;
+  return ev;
+}
+
 PassCfg pick_cfg(const Geom& g, Pass pass) {
   PassCfg c{};
   if (g.G <= 64) {
@@ -109,7 +114,7 @@ BwdWs bwd_ws_layout(const Geom& g, int kind) {
   if (kind == FS_MIX_ATTN) per_bh = 3 * (size_t)g.V * g.V;
   off += up(sizeof(float) * (size_t)g.BH() * per_bh);
   L.scr = off;
-  off += up(kind == FS_MIX_ATTN ? 3 * tok : 0);
+  off += up(kind == FS_MIX_ATTN ? 3 * tok + sizeof(float) * (size_t)g.BH() * g.G * g.G : 0);
   L.total = off;
   return L;
 }
@@ -334,7 +339,7 @@ int fs_mix_bwd(const fs_problem* prob, const fs_mix_desc* mix, const float* z,
   if (ws == nullptr || ws_bytes < bwd_required(g)) return FS_ERR_WORKSPACE;
   char* w = static_cast<char*>(ws);
   return hip_status(fs::launch_mix_bwd(
-      g, mix_args(mix), z, nullptr, attn_probs, dzmix, dz, nullptr, nullptr,
+      g, mix_args(mix), z, nullptr, nullptr, attn_probs, dzmix, dz, nullptr, nullptr, nullptr,
       reinterpret_cast<float*>(w + L.scr), reinterpret_cast<float*>(w + L.partM),
       mix->kind == FS_MIX_IDENTITY ? nullptr : dmix_params, static_cast<hipStream_t>(hip_stream)));
 }
@@ -395,6 +400,18 @@ int fs_slice_deslice_bwd(const fs_problem* prob, const fs_mix_desc* mix, const v
                                    mix->kind == FS_MIX_IDENTITY ? nullptr : dmix_params,
                                    dzmix_out, static_cast<char*>(ws),
                                    static_cast<hipStream_t>(hip_stream)));
+}
+
+int fs_set_pass_events(int pass, void* before, void* after) {
+  if (pass < -1 || pass > 3) return FS_ERR_ARG;
+  fs::PassEvents& ev = fs::pass_events();
+  if (pass < 0) {
+    ev = fs::PassEvents{};
+    return FS_OK;
+  }
+  ev.before[pass] = static_cast<hipEvent_t>(before);
+  ev.after[pass] = static_cast<hipEvent_t>(after);
+  return FS_OK;
 }
 
 const char* fs_status_string(int status) {

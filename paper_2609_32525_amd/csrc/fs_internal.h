@@ -32,6 +32,13 @@ struct PassCfg {
 
 PassCfg pick_cfg(const Geom& g, Pass pass);
 
+// Per-thread measurement events recorded around the streaming passes (fs_set_pass_events).
+struct PassEvents {
+  hipEvent_t before[4] = {nullptr, nullptr, nullptr, nullptr};
+  hipEvent_t after[4] = {nullptr, nullptr, nullptr, nullptr};
+};
+PassEvents& pass_events();
+
 // Workspace carve-up (byte offsets, 256-byte aligned).
 struct FwdWs {
   size_t partU, partS, total;
@@ -63,11 +70,20 @@ hipError_t launch_deslice(const Geom& g, const void* x, const float* Ws, const f
                           hipStream_t st);
 hipError_t launch_mix(const Geom& g, const MixArgs& m, const float* z, float* zmix,
                       float* attn, hipStream_t st);
-// dz = Mix^T(dzm); with s given also dU = dz / (s + eps) and ds; per-(b,h) parameter
-// partials into partM, reduced into dmix (nullable). scr: attention scratch [BH][3][G][V].
+// dz = Mix^T(dzm); with s given also dU = dz / (s + eps), ds and the slot-mean shifts cen
+// [BH][2V + 1]; per-(b,h) parameter partials into partM, reduced into dmix (nullable).
+// scr: attention scratch [BH][3 G V + G G].
 hipError_t launch_mix_bwd(const Geom& g, const MixArgs& m, const float* z, const float* s,
-                          const float* attn, const float* dzm, float* dz, float* dU, float* ds,
-                          float* scr, float* partM, float* dmix, hipStream_t st);
+                          const float* zmix, const float* attn, const float* dzm, float* dz,
+                          float* dU, float* ds, float* cen, float* scr, float* partM,
+                          float* dmix, hipStream_t st);
+// Fixed-order reductions of per-workgroup partials (fs_tokens.hip).
+hipError_t launch_reduce_tokens(const Geom& g, const float* partU, const float* partS,
+                                int chunks, float* z, float* s, hipStream_t st);
+hipError_t launch_reduce_rows(const Geom& g, const float* part, float* out, int chunks,
+                              int64_t len, hipStream_t st);
+hipError_t launch_reduce_params(const Geom& g, const float* part, float* dWs, float* dbias,
+                                float* dtau, int chunks, hipStream_t st);
 hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void* fx,
                       const float* Ws, const float* bias, const float* tau, const float* z,
                       const float* s, const float* zmix, const float* attn, const float* lse,

@@ -1124,347 +1124,6 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
 }
 
 // =======================================================================================
-// Token-sized kernels (fp32, plain VALU; their cost is O(B H G V) or O(B H G^2 V))
-// =======================================================================================
-
-// z = (sum_chunks U) / (sum_chunks s + eps), s = sum_chunks s. Fixed chunk order.
-__global__ void k_reduce_tokens(const float* partU, const float* partS, float* z, float* s,
-                                int chunks, int G, int V, float eps) {
-  const int bh = blockIdx.y;
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= G * V) return;
-  const int g = idx / V;
-  const float* pu = partU + (int64_t)bh * chunks * G * V + idx;
-  const float* ps = partS + (int64_t)bh * chunks * G + g;
-  float u = 0.f, sv = 0.f;
-  for (int q = 0; q < chunks; ++q) {
-    u += pu[(int64_t)q * G * V];
-    sv += ps[(int64_t)q * G];
-  }
-  z[(int64_t)bh * G * V + idx] = u / (sv + eps);
-  if (idx % V == 0) s[(int64_t)bh * G + g] = sv;
-}
-
-// out[bh][idx] = sum over chunks of part[bh][chunk][idx], fixed order.
-__global__ void k_reduce_chunks(const float* part, float* out, int chunks, int64_t len) {
-  const int bh = blockIdx.y;
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= len) return;
-  const float* p = part + (int64_t)bh * chunks * len + idx;
-  float acc = 0.f;
-  for (int q = 0; q < chunks; ++q) acc += p[(int64_t)q * len];
-  out[(int64_t)bh * len + idx] = acc;
-}
-
-// Parameter gradients from pass-B partials [BH][chunks][D*G + G + 2] (the last two floats
-// hold one fp64 dtau partial): dWs/dbias summed over (b, h) (shared) or over b (per head);
-// dtau[h] summed over b in fp64.
-__global__ void k_reduce_params(const float* part, float* dWs, float* dbias, float* dtau,
-                                int B, int H, int chunks, int D, int G, int per_head) {
-  const int64_t len = (int64_t)D * G + G + 2;
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int hh = blockIdx.y;  // head for per-head outputs; 0 otherwise
-  if (idx >= len - 1) return;
-  const bool is_tau = idx == len - 2;
-  if (!per_head && !is_tau && hh > 0) return;
-  float acc = 0.f;
-  if (is_tau) {
-    if (hh >= H) return;
-    double t = 0.0;
-    for (int b = 0; b < B; ++b)
-      for (int q = 0; q < chunks; ++q)
-        t += *reinterpret_cast<const double*>(part + ((int64_t)(b * H + hh) * chunks + q) * len + idx);
-    dtau[hh] = (float)t;
-    return;
-  }
-  if (per_head) {
-    for (int b = 0; b < B; ++b)
-      for (int q = 0; q < chunks; ++q)
-        acc += part[((int64_t)(b * H + hh) * chunks + q) * len + idx];
-  } else {
-    for (int bh = 0; bh < B * H; ++bh)
-      for (int q = 0; q < chunks; ++q) acc += part[((int64_t)bh * chunks + q) * len + idx];
-  }
-  if (idx < (int64_t)D * G) {
-    dWs[(per_head ? (int64_t)hh * D * G : 0) + idx] = acc;
-  } else {
-    dbias[(per_head ? (int64_t)hh * G : 0) + (idx - (int64_t)D * G)] = acc;
-  }
-}
-
-// ---- token mix, forward -----------------------------------------------------------------
-__global__ void k_mix_linear(const float* z, float* zmix, const float* A, const float* Wc,
-                             int kind, int a_per_head, int H, int G, int V) {
-  const int bh = blockIdx.y;
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= G * V) return;
-  const int g = idx / V, v = idx % V;
-  const float* zb = z + (int64_t)bh * G * V;
-  float acc = 0.f;
-  if (kind == 0) {
-    acc = zb[idx];
-  } else if (kind == 1) {
-    const float* Ah = A + (a_per_head ? (int64_t)(bh % H) * G * G : 0) + (int64_t)g * G;
-    for (int k = 0; k < G; ++k) acc += Ah[k] * zb[(int64_t)k * V + v];
-  } else {
-    for (int k = 0; k < V; ++k) acc += zb[(int64_t)g * V + k] * Wc[(int64_t)k * V + v];
-  }
-  zmix[(int64_t)bh * G * V + idx] = acc;
-}
-
-// q, k, v = z Wq, z Wk, z Wv into LDS (G * V <= 8192 floats each).
-__device__ void attn_qkv(const float* zb, const float* Wq, const float* Wk, const float* Wv,
-                         float* q, float* k, float* v, int G, int V) {
-  for (int idx = threadIdx.x; idx < G * V; idx += blockDim.x) {
-    const int g = idx / V, c = idx % V;
-    float aq = 0.f, ak = 0.f, av = 0.f;
-    for (int e = 0; e < V; ++e) {
-      const float zz = zb[(int64_t)g * V + e];
-      aq += zz * Wq[e * V + c];
-      ak += zz * Wk[e * V + c];
-      av += zz * Wv[e * V + c];
-    }
-    q[idx] = aq;
-    k[idx] = ak;
-    v[idx] = av;
-  }
-}
-
-constexpr int kAttnMax = 8192;  // G * V limit of the single-workgroup attention mix
-
-// One workgroup per (b, h); thread t handles query rows t, t + blockDim, ...
-__global__ __launch_bounds__(256) void k_mix_attn(const float* z, float* zmix, float* P,
-                                                  const float* Wq, const float* Wk,
-                                                  const float* Wv, float scale, int G, int V) {
-  __shared__ float q[kAttnMax], k[kAttnMax], v[kAttnMax];
-  const int bh = blockIdx.x;
-  const float* zb = z + (int64_t)bh * G * V;
-  attn_qkv(zb, Wq, Wk, Wv, q, k, v, G, V);
-  __syncthreads();
-  float* Pb = P + (int64_t)bh * G * G;
-  for (int g = threadIdx.x; g < G; g += blockDim.x) {
-    float mx = -INFINITY;
-    for (int t = 0; t < G; ++t) {
-      float sdot = 0.f;
-      for (int c = 0; c < V; ++c) sdot += q[g * V + c] * k[t * V + c];
-      sdot *= scale;
-      Pb[(int64_t)g * G + t] = sdot;
-      mx = fmaxf(mx, sdot);
-    }
-    float l = 0.f;
-    for (int t = 0; t < G; ++t) {
-      const float e = expf(Pb[(int64_t)g * G + t] - mx);
-      Pb[(int64_t)g * G + t] = e;
-      l += e;
-    }
-    const float inv = 1.0f / l;
-    for (int t = 0; t < G; ++t) Pb[(int64_t)g * G + t] *= inv;
-    for (int c = 0; c < V; ++c) {
-      float acc = 0.f;
-      for (int t = 0; t < G; ++t) acc += Pb[(int64_t)g * G + t] * v[t * V + c];
-      zmix[(int64_t)bh * G * V + (int64_t)g * V + c] = acc;
-    }
-  }
-}
-
-// ---- token mix, backward ------------------------------------------------------------------
-// Linear kinds: dz = A^T dzm (LINEAR_G) / dzm Wc^T (LINEAR_C) / dzm (IDENTITY), then
-// dU = dz / (s + eps), ds = -sum_v dz z / (s + eps). Parameter partials per (b, h):
-// LINEAR_G: dA_bh[g][k] = sum_v dzm[g][v] z[k][v]; LINEAR_C: dWc_bh[c][v] = sum_g z[g][c] dzm[g][v].
-__global__ void k_mix_bwd_linear(const float* z, const float* s, const float* dzm, float* dz,
-                                 float* dU, float* ds, const float* A, const float* Wc,
-                                 int kind, int a_per_head, int H, int G, int V, float eps) {
-  const int bh = blockIdx.x;
-  const float* zb = z + (int64_t)bh * G * V;
-  const float* db = dzm + (int64_t)bh * G * V;
-  float* dzb = dz + (int64_t)bh * G * V;
-  for (int idx = threadIdx.x; idx < G * V; idx += blockDim.x) {
-    const int g = idx / V, v = idx % V;
-    float acc = 0.f;
-    if (kind == 0) {
-      acc = db[idx];
-    } else if (kind == 1) {
-      const float* Ah = A + (a_per_head ? (int64_t)(bh % H) * G * G : 0);
-      for (int k = 0; k < G; ++k) acc += Ah[(int64_t)k * G + g] * db[(int64_t)k * V + v];
-    } else {
-      for (int k = 0; k < V; ++k) acc += db[(int64_t)g * V + k] * Wc[(int64_t)v * V + k];
-    }
-    dzb[idx] = acc;
-  }
-  if (s == nullptr) return;
-  __syncthreads();
-  for (int g = threadIdx.x; g < G; g += blockDim.x) {
-    const float inv = 1.0f / (s[(int64_t)bh * G + g] + eps);
-    float acc = 0.f;
-    for (int v = 0; v < V; ++v) {
-      const float d = dzb[(int64_t)g * V + v];
-      acc += d * zb[(int64_t)g * V + v];
-      dU[(int64_t)bh * G * V + (int64_t)g * V + v] = d * inv;
-    }
-    ds[(int64_t)bh * G + g] = -acc * inv;
-  }
-}
-
-__global__ void k_mix_param_linear(const float* z, const float* dzm, float* partM, int kind,
-                                   int G, int V) {
-  const int bh = blockIdx.y;
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  const float* zb = z + (int64_t)bh * G * V;
-  const float* db = dzm + (int64_t)bh * G * V;
-  if (kind == 1) {
-    if (idx >= G * G) return;
-    const int g = idx / G, k = idx % G;
-    float acc = 0.f;
-    for (int v = 0; v < V; ++v) acc += db[(int64_t)g * V + v] * zb[(int64_t)k * V + v];
-    partM[(int64_t)bh * G * G + idx] = acc;
-  } else {
-    if (idx >= V * V) return;
-    const int cc = idx / V, v = idx % V;
-    float acc = 0.f;
-    for (int g = 0; g < G; ++g) acc += zb[(int64_t)g * V + cc] * db[(int64_t)g * V + v];
-    partM[(int64_t)bh * V * V + idx] = acc;
-  }
-}
-
-// Attention backward, one workgroup per (b, h). scr holds dq, dk, dv ([3][G][V] per (b, h)).
-// Writes dz, the (dWq, dWk, dWv) partial [3][V][V] of this (b, h), and, when s is given,
-// dU = dz / (s + eps) and ds = -sum_v dz z / (s + eps).
-__global__ __launch_bounds__(256) void k_mix_bwd_attn(const float* z, const float* s,
-                                                      const float* P, const float* dzm,
-                                                      float* dz, float* dU, float* ds,
-                                                      float* scr, float* partM,
-                                                      const float* Wq, const float* Wk,
-                                                      const float* Wv, float scale, int G,
-                                                      int V, float eps) {
-  __shared__ float q[kAttnMax], k[kAttnMax], v[kAttnMax];
-  __shared__ float rsum[256];
-  const int bh = blockIdx.x;
-  const float* zb = z + (int64_t)bh * G * V;
-  const float* Pb = P + (int64_t)bh * G * G;
-  const float* gb = dzm + (int64_t)bh * G * V;
-  float* dq = scr + (int64_t)bh * 3 * G * V;
-  float* dk = dq + (int64_t)G * V;
-  float* dv = dk + (int64_t)G * V;
-  attn_qkv(zb, Wq, Wk, Wv, q, k, v, G, V);
-  __syncthreads();
-  // dP = dzm v^T; rsum[g] = sum_t dP[g][t] P[g][t]; dS = P * (dP - rsum)
-  auto dP = [&](int g, int t) {
-    float acc = 0.f;
-    for (int c = 0; c < V; ++c) acc += gb[(int64_t)g * V + c] * v[t * V + c];
-    return acc;
-  };
-  for (int g = threadIdx.x; g < G; g += blockDim.x) {
-    float acc = 0.f;
-    for (int t = 0; t < G; ++t) acc += dP(g, t) * Pb[(int64_t)g * G + t];
-    rsum[g] = acc;
-  }
-  __syncthreads();
-  // dq[g] = scale sum_t dS[g][t] k[t]
-  for (int g = threadIdx.x; g < G; g += blockDim.x) {
-    for (int c = 0; c < V; ++c) dq[(int64_t)g * V + c] = 0.f;
-    for (int t = 0; t < G; ++t) {
-      const float dS = Pb[(int64_t)g * G + t] * (dP(g, t) - rsum[g]);
-      for (int c = 0; c < V; ++c) dq[(int64_t)g * V + c] += scale * dS * k[t * V + c];
-    }
-  }
-  // dk[t] = scale sum_g dS[g][t] q[g]; dv[t] = sum_g P[g][t] dzm[g]
-  for (int t = threadIdx.x; t < G; t += blockDim.x) {
-    for (int c = 0; c < V; ++c) {
-      dk[(int64_t)t * V + c] = 0.f;
-      dv[(int64_t)t * V + c] = 0.f;
-    }
-    for (int g = 0; g < G; ++g) {
-      const float p = Pb[(int64_t)g * G + t];
-      const float dS = p * (dP(g, t) - rsum[g]);
-      for (int c = 0; c < V; ++c) {
-        dk[(int64_t)t * V + c] += scale * dS * q[g * V + c];
-        dv[(int64_t)t * V + c] += p * gb[(int64_t)g * V + c];
-      }
-    }
-  }
-  __syncthreads();
-  // parameter partials: dWq = z^T dq, dWk = z^T dk, dWv = z^T dv
-  float* pm = partM + (int64_t)bh * 3 * V * V;
-  for (int idx = threadIdx.x; idx < V * V; idx += blockDim.x) {
-    const int e = idx / V, c = idx % V;
-    float aq = 0.f, ak = 0.f, av = 0.f;
-    for (int g = 0; g < G; ++g) {
-      const float zz = zb[(int64_t)g * V + e];
-      aq += zz * dq[(int64_t)g * V + c];
-      ak += zz * dk[(int64_t)g * V + c];
-      av += zz * dv[(int64_t)g * V + c];
-    }
-    pm[idx] = aq;
-    pm[V * V + idx] = ak;
-    pm[2 * V * V + idx] = av;
-  }
-  // dz = dq Wq^T + dk Wk^T + dv Wv^T
-  float* dzb = dz + (int64_t)bh * G * V;
-  for (int idx = threadIdx.x; idx < G * V; idx += blockDim.x) {
-    const int g = idx / V, e = idx % V;
-    float acc = 0.f;
-    for (int c = 0; c < V; ++c)
-      acc += dq[(int64_t)g * V + c] * Wq[e * V + c] + dk[(int64_t)g * V + c] * Wk[e * V + c] +
-             dv[(int64_t)g * V + c] * Wv[e * V + c];
-    dzb[idx] = acc;
-  }
-  if (s == nullptr) return;
-  __syncthreads();
-  for (int g = threadIdx.x; g < G; g += blockDim.x) {
-    const float inv = 1.0f / (s[(int64_t)bh * G + g] + eps);
-    float acc = 0.f;
-    for (int c = 0; c < V; ++c) {
-      const float d = dzb[(int64_t)g * V + c];
-      acc += d * zb[(int64_t)g * V + c];
-      dU[(int64_t)bh * G * V + (int64_t)g * V + c] = d * inv;
-    }
-    ds[(int64_t)bh * G + g] = -acc * inv;
-  }
-}
-
-// Mass-weighted slot means per (b, h): with m_g = s_g / sum_g s_g (the share of all point
-// weight that slot g holds), cen = [sum_g m_g zmix[g][:], sum_g m_g dU[g][:], sum_g m_g ds[g]].
-// Nearly empty slots have huge dU and ds but no weight, so they do not pull the shift away
-// from the values the points actually see. All zero when no slot has weight.
-__global__ void k_token_means(const float* zmix, const float* dU, const float* ds,
-                              const float* s, float* cen, int G, int V) {
-  const int bh = blockIdx.x;
-  const float* sb = s + (int64_t)bh * G;
-  float tot = 0.f;
-  for (int g = 0; g < G; ++g) tot += sb[g];
-  const float inv = tot > 0.f ? 1.0f / tot : 0.f;
-  for (int c = threadIdx.x; c < 2 * V + 1; c += blockDim.x) {
-    float acc = 0.f;
-    if (c < V) {
-      for (int g = 0; g < G; ++g) acc += sb[g] * zmix[((int64_t)bh * G + g) * V + c];
-    } else if (c < 2 * V) {
-      for (int g = 0; g < G; ++g) acc += sb[g] * dU[((int64_t)bh * G + g) * V + (c - V)];
-    } else {
-      for (int g = 0; g < G; ++g) acc += sb[g] * ds[(int64_t)bh * G + g];
-    }
-    cen[(int64_t)bh * (2 * V + 1) + c] = acc * inv;
-  }
-}
-
-// Sum per-(b,h) mix-parameter partials [BH][len] into dmix: over all (b,h), or over b per
-// head (per_head: dmix is (H, len)).
-__global__ void k_reduce_mixparams(const float* partM, float* dmix, int B, int H, int64_t len,
-                                   int per_head) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int hh = blockIdx.y;
-  if (idx >= len) return;
-  float acc = 0.f;
-  if (per_head) {
-    for (int b = 0; b < B; ++b) acc += partM[(int64_t)(b * H + hh) * len + idx];
-    dmix[(int64_t)hh * len + idx] = acc;
-  } else {
-    if (hh > 0) return;
-    for (int bh = 0; bh < B * H; ++bh) acc += partM[(int64_t)bh * len + idx];
-    dmix[idx] = acc;
-  }
-}
-
-// =======================================================================================
 // Dispatch over the compile-time tiling
 // =======================================================================================
 #define FS_DISPATCH_KERNEL(KNAME)                                                           \
@@ -1501,7 +1160,7 @@ hipError_t run_tiled(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t 
 }
 
 template <int PASS>
-hipError_t run_pass(const Geom& g, const PassArgs& a, hipStream_t st) {
+hipError_t run_pass_impl(const Geom& g, const PassArgs& a, hipStream_t st) {
   const PassCfg cfg = pick_cfg(g, (Pass)PASS);
   const int BH = g.BH();
   if (g.bf16) {
@@ -1514,6 +1173,19 @@ hipError_t run_pass(const Geom& g, const PassArgs& a, hipStream_t st) {
     if (g.D == 64) return run_tiled<PASS, false, 64>(cfg, BH, a, st);
   }
   return hipErrorInvalidConfiguration;
+}
+
+// Launch one streaming pass, bracketed by the caller's measurement events if requested.
+template <int PASS>
+hipError_t run_pass(const Geom& g, const PassArgs& a, hipStream_t st) {
+  const PassEvents& ev = pass_events();
+  if (ev.before[PASS] != nullptr) {
+    hipError_t e = hipEventRecord(ev.before[PASS], st);
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = run_pass_impl<PASS>(g, a, st);
+  if (e == hipSuccess && ev.after[PASS] != nullptr) e = hipEventRecord(ev.after[PASS], st);
+  return e;
 }
 
 PassArgs base_args(const Geom& g, Pass p) {
@@ -1549,11 +1221,7 @@ hipError_t launch_slice(const Geom& g, const void* x, const void* fx, const floa
   a.part2 = partS;
   hipError_t e = run_pass<PASS_SLICE>(g, a, st);
   if (e != hipSuccess) return e;
-  const int BH = g.BH();
-  dim3 grid((g.G * g.V + 255) / 256, BH);
-  hipLaunchKernelGGL(k_reduce_tokens, grid, dim3(256), 0, st, partU, partS, z, s, a.chunks,
-                     g.G, g.V, g.eps);
-  return hipGetLastError();
+  return launch_reduce_tokens(g, partU, partS, a.chunks, z, s, st);
 }
 
 hipError_t launch_deslice(const Geom& g, const void* x, const float* Ws, const float* bias,
@@ -1570,51 +1238,6 @@ hipError_t launch_deslice(const Geom& g, const void* x, const float* Ws, const f
   return run_pass<PASS_DESLICE>(g, a, st);
 }
 
-hipError_t launch_mix(const Geom& g, const MixArgs& m, const float* z, float* zmix,
-                      float* attn, hipStream_t st) {
-  const int BH = g.BH();
-  if (m.kind == 3) {
-    hipLaunchKernelGGL(k_mix_attn, dim3(BH), dim3(256), 0, st, z, zmix, attn, m.Wq, m.Wk,
-                       m.Wv, m.scale, g.G, g.V);
-  } else {
-    dim3 grid((g.G * g.V + 255) / 256, BH);
-    hipLaunchKernelGGL(k_mix_linear, grid, dim3(256), 0, st, z, zmix, m.A, m.Wc, m.kind,
-                       m.a_per_head ? 1 : 0, g.H, g.G, g.V);
-  }
-  return hipGetLastError();
-}
-
-hipError_t launch_mix_bwd(const Geom& g, const MixArgs& m, const float* z, const float* s,
-                          const float* attn, const float* dzm, float* dz, float* dU, float* ds,
-                          float* scr, float* partM, float* dmix, hipStream_t st) {
-  const int BH = g.BH();
-  if (m.kind == 3) {
-    hipLaunchKernelGGL(k_mix_bwd_attn, dim3(BH), dim3(256), 0, st, z, s, attn, dzm, dz, dU, ds,
-                       scr, partM, m.Wq, m.Wk, m.Wv, m.scale, g.G, g.V, g.eps);
-  } else {
-    hipLaunchKernelGGL(k_mix_bwd_linear, dim3(BH), dim3(256), 0, st, z, s, dzm, dz, dU, ds,
-                       m.A, m.Wc, m.kind, m.a_per_head ? 1 : 0, g.H, g.G, g.V, g.eps);
-    if (dmix != nullptr && m.kind != 0) {
-      const int len = m.kind == 1 ? g.G * g.G : g.V * g.V;
-      dim3 grid((len + 255) / 256, BH);
-      hipLaunchKernelGGL(k_mix_param_linear, grid, dim3(256), 0, st, z, dzm, partM, m.kind,
-                         g.G, g.V);
-    }
-  }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (dmix != nullptr && m.kind != 0) {
-    const int64_t len =
-        m.kind == 1 ? (int64_t)g.G * g.G : (m.kind == 2 ? (int64_t)g.V * g.V : 3LL * g.V * g.V);
-    const bool per_head = m.kind == 1 && m.a_per_head;
-    dim3 grid((unsigned)((len + 255) / 256), per_head ? g.H : 1);
-    hipLaunchKernelGGL(k_reduce_mixparams, grid, dim3(256), 0, st, partM, dmix, (int)g.B, g.H,
-                       len, per_head ? 1 : 0);
-    e = hipGetLastError();
-  }
-  return e;
-}
-
 hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void* fx,
                       const float* Ws, const float* bias, const float* tau, const float* z,
                       const float* s, const float* zmix, const float* attn, const float* lse,
@@ -1628,8 +1251,6 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
   float* dsv = reinterpret_cast<float*>(ws + L.ds);
   float* partP = reinterpret_cast<float*>(ws + L.partP);
   float* partM = reinterpret_cast<float*>(ws + L.partM);
-  const int BH = g.BH();
-
   // pass A: dzmix = w^T dout
   PassArgs a = base_args(g, PASS_BWD_A);
   a.x = x;
@@ -1641,20 +1262,12 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
   a.part = partDZ;
   hipError_t e = run_pass<PASS_BWD_A>(g, a, st);
   if (e != hipSuccess) return e;
-  {
-    const int64_t len = (int64_t)g.G * g.V;
-    dim3 grid((unsigned)((len + 255) / 256), BH);
-    hipLaunchKernelGGL(k_reduce_chunks, grid, dim3(256), 0, st, partDZ, dzm, a.chunks, len);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  // mix backward: dz, dU, ds (+ parameter gradients)
-  e = launch_mix_bwd(g, m, z, s, attn, dzm, dz, dU, dsv, reinterpret_cast<float*>(ws + L.scr),
-                     partM, dmix, st);
+  e = launch_reduce_rows(g, partDZ, dzm, a.chunks, (int64_t)g.G * g.V, st);
   if (e != hipSuccess) return e;
+  // mix backward: dz, dU, ds, the slot-mean shifts (+ parameter gradients)
   float* cen = reinterpret_cast<float*>(ws + L.cen);
-  hipLaunchKernelGGL(k_token_means, dim3(BH), dim3(128), 0, st, zmix, dU, dsv, s, cen, g.G, g.V);
-  e = hipGetLastError();
+  e = launch_mix_bwd(g, m, z, s, zmix, attn, dzm, dz, dU, dsv, cen,
+                     reinterpret_cast<float*>(ws + L.scr), partM, dmix, st);
   if (e != hipSuccess) return e;
   // pass B
   PassArgs b = base_args(g, PASS_BWD_B);
@@ -1674,13 +1287,7 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
   b.part = partP;
   e = run_pass<PASS_BWD_B>(g, b, st);
   if (e != hipSuccess) return e;
-  {
-    const int64_t len = (int64_t)g.D * g.G + g.G + 2;
-    dim3 grid((unsigned)((len + 255) / 256), g.H);
-    hipLaunchKernelGGL(k_reduce_params, grid, dim3(256), 0, st, partP, dWs, dbias, dtau,
-                       (int)g.B, g.H, b.chunks, g.D, g.G, g.ws_per_head ? 1 : 0);
-    e = hipGetLastError();
-  }
+  e = launch_reduce_params(g, partP, dWs, dbias, dtau, b.chunks, st);
   return e;
 }
 

@@ -47,6 +47,14 @@ def test_exports_every_declared_symbol():
         assert hasattr(L, n), n
 
 
+def test_pass_events_validation():
+    L = fs.lib()
+    assert L.fs_set_pass_events(7, None, None) == ARG
+    assert L.fs_set_pass_events(-2, None, None) == ARG
+    assert L.fs_set_pass_events(3, None, None) == OK
+    assert L.fs_set_pass_events(-1, None, None) == OK
+
+
 def test_status_strings():
     for code in (OK, NULL, SHAPE, DTYPE, UNSUP, WS, ARG, ALIGN, ALIAS, HIP):
         s = fs.status_string(code)

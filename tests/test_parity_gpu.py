@@ -238,7 +238,10 @@ def test_parity_full_size(name):
     # zero over the slots (App. F.2)
     np.testing.assert_allclose(got["s"].sum(-1), w.N, rtol=1e-5)
     assert abs(got["db"].sum()) <= 1e-4 * np.abs(got["db"]).sum()
-    assert np.all(np.abs(got["dWs"].sum(-1)) <= 1e-4 * np.abs(got["dWs"]).sum(-1))
+    # dW_s contracts bf16-rounded logit gradients in bf16 storage, so its slot sums cancel
+    # only to the bf16 rounding level there
+    cancel = 2e-3 if w.dtype == "bf16" else 1e-4
+    assert np.all(np.abs(got["dWs"].sum(-1)) <= cancel * np.abs(got["dWs"]).sum(-1))
     for k in ("out", "dx", "dfx", "dWs", "db", "dtau"):
         assert np.isfinite(got[k]).all(), k
     if pairs is None:
