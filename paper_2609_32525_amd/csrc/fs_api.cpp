@@ -42,6 +42,8 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
     c.NS = g.G / 64;
     c.NP = c.NS == 2 ? 2 : 1;
   }
+  // fp32 backward pass B works on 16-point tiles (its register footprint is the largest)
+  c.PB = (pass == PASS_BWD_B && !g.bf16 && c.NS == 1) ? 1 : 2;
   // Workgroups along the points per (sample, head): enough to fill 256 CUs several times,
   // but few enough that the per-workgroup partials stay small next to the streamed data.
   const bool partials = pass != PASS_DESLICE;
@@ -50,7 +52,7 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
     target = partials ? 256 : 512;
   else
     target = partials ? 512 : 2048;
-  const int64_t step = 32LL * c.NP;
+  const int64_t step = 16LL * c.PB * c.NP;
   const int64_t ntiles = std::max<int64_t>(1, (g.N + step - 1) / step);
   int64_t chunks = std::max<int64_t>(1, (target + g.BH() - 1) / g.BH());
   // passes that write partials give every chunk at least 4 tiles per point group, so the

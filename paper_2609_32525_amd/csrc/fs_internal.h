@@ -26,6 +26,7 @@ enum Pass { PASS_SLICE = 0, PASS_DESLICE = 1, PASS_BWD_A = 2, PASS_BWD_B = 3 };
 //   chunks: workgroups per (sample, head) along the points, each covering chunk_pts points.
 struct PassCfg {
   int GS, NS, NP;
+  int PB;  // 16-point blocks per wavefront tile
   int chunks;
   int64_t chunk_pts;
 };

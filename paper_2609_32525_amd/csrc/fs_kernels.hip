@@ -314,8 +314,8 @@ __device__ __forceinline__ void load_gop(GOp<BF, GB, CB>& o, const float* src, i
 }
 
 // out[cb] (+)= M^T-contraction with a T-layout tile column block pb: rows c, cols points.
-template <bool BF, int GB, int CB>
-__device__ __forceinline__ f4 mm_gop_tile(const GOp<BF, GB, CB>& o, int cb, const f4 (*t)[2],
+template <bool BF, int GB, int CB, int PB = 2>
+__device__ __forceinline__ f4 mm_gop_tile(const GOp<BF, GB, CB>& o, int cb, const f4 (*t)[PB],
                                           int pb, f4 acc) {
   if constexpr (!BF) {
 #pragma unroll
@@ -334,32 +334,35 @@ __device__ __forceinline__ f4 mm_gop_tile(const GOp<BF, GB, CB>& o, int cb, cons
   return acc;
 }
 
-// acc[gb][cb] += (S-layout tile column gb)^T-contraction over the 32 points with rows of a
-// point-major matrix P (row stride rs): out(g, c) += sum_p w(p, g) P(p, 16 cb + i).
-template <bool BF, int GB, int CB>
-__device__ __forceinline__ void mm_points(f4 (*acc)[CB], const f4 (*w)[GB],
-                                          const typename Store<BF>::T* base, int64_t rs,
-                                          int64_t p0, int64_t pend, int i, int j) {
+// Operand rows of a point-major matrix P (row stride rs) for a contraction over the 32 points
+// of a tile: lane (j, i) holds P(p, 16 cb + i) for the points of its k-set.
+//   fp32: point 16 pb + 4 j + r for MFMA (pb, r);  bf16: point 16 (e / 4) + 4 j + (e % 4).
+// Gathered separately from the MFMAs so that the next tile's loads can be issued early.
+template <bool BF, int CB>
+struct PtGather;
+template <int CB>
+struct PtGather<false, CB> {
+  float v[2][4][CB];
+};
+template <int CB>
+struct PtGather<true, CB> {
+  bf8 v[CB];
+};
+
+template <bool BF, int CB>
+__device__ __forceinline__ void gather_points(PtGather<BF, CB>& g,
+                                              const typename Store<BF>::T* base, int64_t rs,
+                                              int64_t p0, int64_t pend, int i, int j) {
   if constexpr (!BF) {
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int64_t p = p0 + 16 * pb + 4 * j + r;
-        const bool ok = p < pend;
 #pragma unroll
-        for (int cb = 0; cb < CB; ++cb) {
-          const float bv = ok ? base[p * rs + 16 * cb + i] : 0.f;
-#pragma unroll
-          for (int gb = 0; gb < GB; ++gb) acc[gb][cb] = mfma_f32(w[pb][gb][r], bv, acc[gb][cb]);
-        }
+        for (int cb = 0; cb < CB; ++cb) g.v[pb][r][cb] = p < pend ? base[p * rs + 16 * cb + i] : 0.f;
       }
   } else {
-    bf8 at[GB];
-#pragma unroll
-    for (int gb = 0; gb < GB; ++gb)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) at[gb][e] = (__bf16)w[e / 4][gb][e % 4];
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
       bf8 bt;
@@ -370,10 +373,56 @@ __device__ __forceinline__ void mm_points(f4 (*acc)[CB], const f4 (*w)[GB],
         if (p < pend) h = base[p * rs + 16 * cb + i];
         bt[e] = __builtin_bit_cast(__bf16, h);
       }
-#pragma unroll
-      for (int gb = 0; gb < GB; ++gb) acc[gb][cb] = mfma_bf16(at[gb], bt, acc[gb][cb]);
+      g.v[cb] = bt;
     }
   }
+}
+
+// acc[gb][cb] += (S-layout tile column gb)^T-contraction over the 32 points with the gathered
+// rows: out(g, c) += sum_p w(p, g) P(p, 16 cb + i).
+template <bool BF, int GB, int CB>
+__device__ __forceinline__ void mm_points(f4 (*acc)[CB], const f4 (*w)[GB],
+                                          const PtGather<BF, CB>& g) {
+  if constexpr (!BF) {
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int gb = 0; gb < GB; ++gb) acc[gb][cb] = mfma_f32(w[pb][gb][r], g.v[pb][r][cb], acc[gb][cb]);
+  } else {
+    bf8 at[GB];
+#pragma unroll
+    for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) at[gb][e] = (__bf16)w[e / 4][gb][e % 4];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb) acc[gb][cb] = mfma_bf16(at[gb], g.v[cb], acc[gb][cb]);
+  }
+}
+
+// Register image of a per-wavefront operand in LDS: 16-byte chunk q of lane l at
+// base[q * 64 + l], so every lane reads its own chunk and no two lanes share a bank group.
+template <class Op>
+__device__ __forceinline__ void lds_put(const Op& o, uint4* base, int lane) {
+  static_assert(sizeof(Op) % 16 == 0, "operand image must be whole 16-byte chunks");
+  const uint4* src = reinterpret_cast<const uint4*>(&o);
+#pragma unroll
+  for (int q = 0; q < (int)(sizeof(Op) / 16); ++q) base[q * 64 + lane] = src[q];
+}
+template <class Op>
+__device__ __forceinline__ void lds_get(Op& o, const uint4* base, int lane) {
+  uint4* dst = reinterpret_cast<uint4*>(&o);
+#pragma unroll
+  for (int q = 0; q < (int)(sizeof(Op) / 16); ++q) dst[q] = base[q * 64 + lane];
+}
+template <class Op>
+constexpr int lds_chunks() {
+  return (int)(sizeof(Op) / 16) * 64;
 }
 
 // ---------------------------------------------------------------------------------------
@@ -462,14 +511,27 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
   const int ntile = pend > pbeg ? (int)((pend - pbeg + 32 * NP - 1) / (32 * NP)) : 0;
 
-  for (int t = 0; t < ntile; ++t) {
-    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+  // software pipeline: the next tile's rows are loaded before the current tile is computed
+  struct Tile {
     RowOp<BF, D> xo[2];
+    PtGather<BF, VB> f;
+  };
+  auto load_tile = [&](Tile& tt, int t) {
+    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) {
       const int64_t p = p0 + 16 * pb + i;
-      load_row<BF, D>(xo[pb], xb + p * rs, p < pend, j);
+      load_row<BF, D>(tt.xo[pb], xb + p * rs, p < pend, j);
     }
+    gather_points<BF, VB>(tt.f, fb, rs, p0, pend, i, j);
+  };
+  Tile cur;
+  if (ntile > 0) load_tile(cur, 0);
+  for (int t = 0; t < ntile; ++t) {
+    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+    Tile nxt;
+    if (t + 1 < ntile) load_tile(nxt, t + 1);
+    const RowOp<BF, D>* xo = cur.xo;
     // S-layout logits: rows = points 16 pb + 4 j + r, cols = slots g0 + 16 gb + i
     f4 w[2][GB];
 #pragma unroll
@@ -555,7 +617,8 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
         for (int r = 0; r < 4; ++r) sum += w[pb][gb][r];
       sacc[gb] += sum;
     }
-    mm_points<BF, GB, VB>(U, w, fb, rs, p0, pend, i, j);
+    mm_points<BF, GB, VB>(U, w, cur.f);
+    cur = nxt;
   }
 
   // ---- combine the NP point groups and write this workgroup's partials --------------------
@@ -630,16 +693,28 @@ __global__ __launch_bounds__(64 * NS * NP) void k_deslice(PassArgs a) {
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
   const int ntile = pend > pbeg ? (int)((pend - pbeg + 32 * NP - 1) / (32 * NP)) : 0;
 
-  for (int t = 0; t < ntile; ++t) {
-    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+  // software pipeline: the next tile's rows are loaded before the current tile is computed
+  struct Tile {
     RowOp<BF, D> xo[2];
     float lse2[2];
+  };
+  auto load_tile = [&](Tile& tt, int t) {
+    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) {
       const int64_t p = p0 + 16 * pb + i;
-      load_row<BF, D>(xo[pb], xb + p * rs, p < pend, j);
-      lse2[pb] = p < pend ? lse[p] : kMasked;
+      load_row<BF, D>(tt.xo[pb], xb + p * rs, p < pend, j);
+      tt.lse2[pb] = p < pend ? lse[p] : kMasked;
     }
+  };
+  Tile cur;
+  if (ntile > 0) load_tile(cur, 0);
+  for (int t = 0; t < ntile; ++t) {
+    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+    Tile nxt;
+    if (t + 1 < ntile) load_tile(nxt, t + 1);
+    const RowOp<BF, D>* xo = cur.xo;
+    const float* lse2 = cur.lse2;
     f4 w[GB][2];
 #pragma unroll
     for (int gb = 0; gb < GB; ++gb)
@@ -694,6 +769,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_deslice(PassArgs a) {
         }
       }
     }
+    cur = nxt;
   }
 }
 
@@ -728,22 +804,33 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_a(PassArgs a) {
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
   const int ntile = pend > pbeg ? (int)((pend - pbeg + 32 * NP - 1) / (32 * NP)) : 0;
 
-  for (int t = 0; t < ntile; ++t) {
-    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+  // software pipeline: the next tile's rows are loaded before the current tile is computed
+  struct Tile {
     RowOp<BF, D> xo[2];
+    float lse2[2][4];
+    PtGather<BF, VB> g;
+  };
+  auto load_tile = [&](Tile& tt, int t) {
+    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) {
       const int64_t p = p0 + 16 * pb + i;
-      load_row<BF, D>(xo[pb], xb + p * rs, p < pend, j);
-    }
-    float lse2[2][4];
-#pragma unroll
-    for (int pb = 0; pb < 2; ++pb)
+      load_row<BF, D>(tt.xo[pb], xb + p * rs, p < pend, j);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t p = p0 + 16 * pb + 4 * j + r;
-        lse2[pb][r] = p < pend ? lse[p] : kMasked;
+        const int64_t q = p0 + 16 * pb + 4 * j + r;
+        tt.lse2[pb][r] = q < pend ? lse[q] : kMasked;
       }
+    }
+    gather_points<BF, VB>(tt.g, db, rs, p0, pend, i, j);
+  };
+  Tile cur;
+  if (ntile > 0) load_tile(cur, 0);
+  for (int t = 0; t < ntile; ++t) {
+    Tile nxt;
+    if (t + 1 < ntile) load_tile(nxt, t + 1);
+    const RowOp<BF, D>* xo = cur.xo;
+    const float(*lse2)[4] = cur.lse2;
     f4 w[2][GB];
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb)
@@ -754,7 +841,8 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_a(PassArgs a) {
         for (int r = 0; r < 4; ++r) acc[r] = __builtin_amdgcn_exp2f(acc[r] - lse2[pb][r]);
         w[pb][gb] = acc;
       }
-    mm_points<BF, GB, VB>(Z, w, db, rs, p0, pend, i, j);
+    mm_points<BF, GB, VB>(Z, w, cur.g);
+    cur = nxt;
   }
 
   float* pZ = a.part + ((int64_t)c.bh * a.chunks + blockIdx.x) * a.G * D;
@@ -788,13 +876,24 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_a(PassArgs a) {
 
 // =======================================================================================
 // Backward pass B: point gradients and parameter partials
-// partial layout per workgroup: [D * G] dW_s (row-major (D, G)), [G] dbias, [1] dtau
+// partial layout per workgroup: [D * G] dW_s (row-major (D, G)), [G] dbias, [2] fp64 dtau
+// PB: 16-point blocks per tile (1 or 2; bf16 needs 2: its contraction over points has K=32).
+// With at most two slot groups, the per-head operands live in LDS as register images shared
+// by the workgroup's wavefronts and are read where they are used, which keeps the register
+// count (and so the number of resident wavefronts) in line with the other passes.
 // =======================================================================================
-template <bool BF, int D, int GS, int NS, int NP>
+template <bool BF, int D, int GS, int NS, int NP, int PB>
 __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
-  constexpr int GB = GS / 16, VB = D / 16, DB = D / 16;
+  static_assert(PB == 2 || !BF, "bf16 contracts over 32 points");
+  constexpr int GB = GS / 16, VB = D / 16, DB = D / 16, TP = 16 * PB;
   constexpr bool SPLIT = BF;
   using T = typename Store<BF>::T;
+  using SOp = SlotOp<BF, D, GB>;
+  using UOp = GOp<BF, GB, VB>;
+  using XOp = GOp<BF, GB, DB>;
+  // operands in LDS when at most two slot groups share a tile and the images fit in 64 KB
+  constexpr bool OPL =
+      NS <= 2 && (size_t)NS * 64 * (3 * sizeof(SOp) + sizeof(UOp) + sizeof(XOp)) <= 65536;
   const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
   const int wave = threadIdx.x >> 6, ws = wave % NS, wp = wave / NS;
   const HeadCtx c = head_ctx<D>(a, ws, GS);
@@ -814,10 +913,6 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
   // one). Subtracting the mass-weighted slot means first keeps the rounding of these
   // operands relative to what actually differs between slots.
   const float* cen = a.cen + (int64_t)c.bh * (2 * D + 1);
-  SlotOp<BF, D, GB> wop, zvop, uvop;
-  load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, c.sc, i, j);
-  load_slotop<BF, D, GB, false, false>(zvop, zm, D, c.g0, 1.0f, i, j, cen);
-  load_slotop<BF, D, GB, false, false>(uvop, dU, D, c.g0, 1.0f, i, j, cen + D);
   float bT[GB][4], dsT[GB][4];
 #pragma unroll
   for (int gb = 0; gb < GB; ++gb)
@@ -826,10 +921,50 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
       bT[gb][r] = c.sc * c.bias[c.g0 + 16 * gb + 4 * j + r];
       dsT[gb][r] = a.ds[(int64_t)c.bh * a.G + c.g0 + 16 * gb + 4 * j + r] - cen[2 * D];
     }
-  GOp<BF, GB, VB> ugop;  // dU(g, v) for dfx = w dU
-  load_gop<BF, GB, VB, false>(ugop, dU, D, c.g0, 1.0f, i, j);
-  GOp<BF, GB, DB> wgop;  // W_s[d][g] / tau for dx = da W_s^T / tau
-  load_gop<BF, GB, DB, true>(wgop, c.W, a.G, c.g0, inv_tau, i, j);
+
+  // operands: W_s (logits), zmix and dU (dw, contraction over v), dU (dfx) and W_s / tau (dx)
+  constexpr int kOpChunks = OPL ? 3 * lds_chunks<SOp>() + lds_chunks<UOp>() + lds_chunks<XOp>() : 1;
+  __shared__ uint4 opl[OPL ? NS : 1][kOpChunks];
+  SOp wop_r, zvop_r, uvop_r;
+  UOp ugop_r;
+  XOp wgop_r;
+  {
+    SOp t0, t1, t2;
+    UOp t3;
+    XOp t4;
+    if (!OPL || wp == 0) {
+      load_slotop<BF, D, GB, true, SPLIT>(t0, c.W, a.G, c.g0, c.sc, i, j);
+      load_slotop<BF, D, GB, false, false>(t1, zm, D, c.g0, 1.0f, i, j, cen);
+      load_slotop<BF, D, GB, false, false>(t2, dU, D, c.g0, 1.0f, i, j, cen + D);
+      load_gop<BF, GB, VB, false>(t3, dU, D, c.g0, 1.0f, i, j);
+      load_gop<BF, GB, DB, true>(t4, c.W, a.G, c.g0, inv_tau, i, j);
+    }
+    if constexpr (OPL) {
+      uint4* b = opl[ws];
+      if (wp == 0) {
+        lds_put(t0, b, lane);
+        lds_put(t1, b + lds_chunks<SOp>(), lane);
+        lds_put(t2, b + 2 * lds_chunks<SOp>(), lane);
+        lds_put(t3, b + 3 * lds_chunks<SOp>(), lane);
+        lds_put(t4, b + 3 * lds_chunks<SOp>() + lds_chunks<UOp>(), lane);
+      }
+      __syncthreads();
+    } else {
+      wop_r = t0;
+      zvop_r = t1;
+      uvop_r = t2;
+      ugop_r = t3;
+      wgop_r = t4;
+    }
+  }
+  const uint4* opb = opl[OPL ? ws : 0];
+  auto get_w = [&](SOp& o) { if constexpr (OPL) lds_get(o, opb, lane); else o = wop_r; };
+  auto get_zv = [&](SOp& o) { if constexpr (OPL) lds_get(o, opb + lds_chunks<SOp>(), lane); else o = zvop_r; };
+  auto get_uv = [&](SOp& o) { if constexpr (OPL) lds_get(o, opb + 2 * lds_chunks<SOp>(), lane); else o = uvop_r; };
+  auto get_ug = [&](UOp& o) { if constexpr (OPL) lds_get(o, opb + 3 * lds_chunks<SOp>(), lane); else o = ugop_r; };
+  auto get_wg = [&](XOp& o) {
+    if constexpr (OPL) lds_get(o, opb + 3 * lds_chunks<SOp>() + lds_chunks<UOp>(), lane); else o = wgop_r;
+  };
 
   f4 dW[DB][GB];
   float dbacc[GB][4];
@@ -842,13 +977,13 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
     for (int d = 0; d < DB; ++d) dW[d][gb] = zero4();
   }
 
-  __shared__ float cx[NS > 1 ? NP : 1][NS > 1 ? NS : 1][2][32];
+  __shared__ float cx[NS > 1 ? NP : 1][NS > 1 ? NS : 1][2][TP];
   // The dfx / dx exchange buffer (NS > 1) and the per-wave da transpose buffer are never live
   // at the same time (a workgroup barrier separates every exchange from the transposes of
   // the previous and the next tile), so they share one LDS allocation.
-  // gx: [NP][NS][VB][2][64] f4; da transpose: fp32 [32 points][GS + 1], bf16 [GS slots][40].
-  constexpr int kDaWords = BF ? (GS * 40 + 1) / 2 : 32 * (GS + 1);
-  constexpr size_t kGxBytes = NS > 1 ? (size_t)NP * NS * VB * 2 * 64 * sizeof(f4) : 0;
+  // gx: [NP][NS][VB][PB][64] f4; da transpose: fp32 [TP points][GS + 1], bf16 [GS slots][40].
+  constexpr int kDaWords = BF ? (GS * 40 + 1) / 2 : TP * (GS + 1);
+  constexpr size_t kGxBytes = NS > 1 ? (size_t)NP * NS * VB * PB * 64 * sizeof(f4) : 0;
   constexpr size_t kDaBytes = (size_t)NS * NP * kDaWords * sizeof(float);
   __shared__ __attribute__((aligned(16))) char smem[kGxBytes > kDaBytes ? kGxBytes : kDaBytes];
   f4* gx = reinterpret_cast<f4*>(smem);
@@ -856,14 +991,14 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
 
   const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
-  const int ntile = pend > pbeg ? (int)((pend - pbeg + 32 * NP - 1) / (32 * NP)) : 0;
+  const int ntile = pend > pbeg ? (int)((pend - pbeg + TP * NP - 1) / (TP * NP)) : 0;
 
   for (int t = 0; t < ntile; ++t) {
-    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
-    RowOp<BF, D> xo[2], go[2], fo[2];
-    float lse2[2];
+    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * TP;
+    RowOp<BF, D> xo[PB], go[PB], fo[PB];
+    float lse2[PB];
 #pragma unroll
-    for (int pb = 0; pb < 2; ++pb) {
+    for (int pb = 0; pb < PB; ++pb) {
       const int64_t p = p0 + 16 * pb + i;
       const bool ok = p < pend;
       load_row<BF, D>(xo[pb], xb + p * rs, ok, j);
@@ -872,31 +1007,45 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
       lse2[pb] = ok ? lse[p] : kMasked;
     }
     // T-layout tiles: rows = slots g0 + 16 gb + 4 j + r, cols = points 16 pb + i
-    f4 tl[GB][2], w[GB][2], dw[GB][2];
+    f4 tl[GB][PB], w[GB][PB], dw[GB][PB];
+    {
+      SOp wop;
+      get_w(wop);
 #pragma unroll
-    for (int gb = 0; gb < GB; ++gb)
+      for (int gb = 0; gb < GB; ++gb)
 #pragma unroll
-      for (int pb = 0; pb < 2; ++pb) {
-        f4 acc = f4{bT[gb][0], bT[gb][1], bT[gb][2], bT[gb][3]};
-        acc = mm_slot_row<BF, D, GB, SPLIT>(wop, gb, xo[pb], acc);
-        f4 tt, ww;
+        for (int pb = 0; pb < PB; ++pb) {
+          f4 acc = f4{bT[gb][0], bT[gb][1], bT[gb][2], bT[gb][3]};
+          acc = mm_slot_row<BF, D, GB, SPLIT>(wop, gb, xo[pb], acc);
+          f4 tt, ww;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          tt[r] = acc[r] - lse2[pb];
-          ww[r] = __builtin_amdgcn_exp2f(tt[r]);
+          for (int r = 0; r < 4; ++r) {
+            tt[r] = acc[r] - lse2[pb];
+            ww[r] = __builtin_amdgcn_exp2f(tt[r]);
+          }
+          tl[gb][pb] = tt;
+          w[gb][pb] = ww;
         }
-        tl[gb][pb] = tt;
-        w[gb][pb] = ww;
-        f4 g = f4{dsT[gb][0], dsT[gb][1], dsT[gb][2], dsT[gb][3]};
-        g = mm_slot_row<BF, D, GB, false>(zvop, gb, go[pb], g);
-        g = mm_slot_row<BF, D, GB, false>(uvop, gb, fo[pb], g);
-        dw[gb][pb] = g;
-      }
+    }
+    {
+      SOp zv, uv;
+      get_zv(zv);
+      get_uv(uv);
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb) {
+          f4 g = f4{dsT[gb][0], dsT[gb][1], dsT[gb][2], dsT[gb][3]};
+          g = mm_slot_row<BF, D, GB, false>(zv, gb, go[pb], g);
+          g = mm_slot_row<BF, D, GB, false>(uv, gb, fo[pb], g);
+          dw[gb][pb] = g;
+        }
+    }
     // per point (column of the tile): c = sum_g w dw, the softmax correction, and
     // tb = sum_g w t, the weighted mean of the shifted base-2 logits t = a2 - lse2
-    float cc[2], tb[2];
+    float cc[PB], tb[PB];
 #pragma unroll
-    for (int pb = 0; pb < 2; ++pb) {
+    for (int pb = 0; pb < PB; ++pb) {
       float sum = 0.f, st = 0.f;
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb)
@@ -911,14 +1060,14 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
     if constexpr (NS > 1) {
       if (j == 0) {
 #pragma unroll
-        for (int pb = 0; pb < 2; ++pb) {
+        for (int pb = 0; pb < PB; ++pb) {
           cx[wp][ws][0][16 * pb + i] = cc[pb];
           cx[wp][ws][1][16 * pb + i] = tb[pb];
         }
       }
       __syncthreads();
 #pragma unroll
-      for (int pb = 0; pb < 2; ++pb) {
+      for (int pb = 0; pb < PB; ++pb) {
         float sum = 0.f, st = 0.f;
         for (int s = 0; s < NS; ++s) {
           sum += cx[wp][s][0][16 * pb + i];
@@ -935,7 +1084,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
 #pragma unroll
     for (int gb = 0; gb < GB; ++gb)
 #pragma unroll
-      for (int pb = 0; pb < 2; ++pb)
+      for (int pb = 0; pb < PB; ++pb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const float da = w[gb][pb][r] * (dw[gb][pb][r] - cc[pb]);
@@ -945,25 +1094,31 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
         }
     dtacc += (double)dts;
     // dfx = w dU, dx = da W_s^T / tau (contractions over this wave's slots)
-    f4 gf[VB][2], gx_[DB][2];
+    f4 gf[VB][PB], gx_[DB][PB];
+    {
+      UOp ug;
+      XOp wg;
+      get_ug(ug);
+      get_wg(wg);
 #pragma unroll
-    for (int pb = 0; pb < 2; ++pb) {
+      for (int pb = 0; pb < PB; ++pb) {
 #pragma unroll
-      for (int vb = 0; vb < VB; ++vb) gf[vb][pb] = mm_gop_tile<BF, GB, VB>(ugop, vb, w, pb, zero4());
+        for (int vb = 0; vb < VB; ++vb) gf[vb][pb] = mm_gop_tile<BF, GB, VB, PB>(ug, vb, w, pb, zero4());
 #pragma unroll
-      for (int d = 0; d < DB; ++d) gx_[d][pb] = mm_gop_tile<BF, GB, DB>(wgop, d, dw, pb, zero4());
+        for (int d = 0; d < DB; ++d) gx_[d][pb] = mm_gop_tile<BF, GB, DB, PB>(wg, d, dw, pb, zero4());
+      }
     }
     if constexpr (NS > 1) {
       __syncthreads();  // every wave has read cx and finished the previous da transposes
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
-        f4(*src)[2] = half == 0 ? gf : gx_;
+        f4(*src)[PB] = half == 0 ? gf : gx_;
         if (ws > 0) {
 #pragma unroll
           for (int cb = 0; cb < VB; ++cb)
 #pragma unroll
-            for (int pb = 0; pb < 2; ++pb)
-              gx[(((size_t)wp * NS + ws) * VB + cb) * 128 + pb * 64 + lane] = src[cb][pb];
+            for (int pb = 0; pb < PB; ++pb)
+              gx[(((size_t)wp * NS + ws) * VB + cb) * (64 * PB) + pb * 64 + lane] = src[cb][pb];
         }
         __syncthreads();
         if (ws == 0) {
@@ -971,15 +1126,15 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
 #pragma unroll
             for (int cb = 0; cb < VB; ++cb)
 #pragma unroll
-              for (int pb = 0; pb < 2; ++pb)
-                src[cb][pb] += gx[(((size_t)wp * NS + s) * VB + cb) * 128 + pb * 64 + lane];
+              for (int pb = 0; pb < PB; ++pb)
+                src[cb][pb] += gx[(((size_t)wp * NS + s) * VB + cb) * (64 * PB) + pb * 64 + lane];
         }
         __syncthreads();
       }
     }
     if (ws == 0) {
 #pragma unroll
-      for (int pb = 0; pb < 2; ++pb) {
+      for (int pb = 0; pb < PB; ++pb) {
         const int64_t p = p0 + 16 * pb + i;
         if (p < pend) {
 #pragma unroll
@@ -1003,18 +1158,18 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
         }
       }
     }
-    // dW_s += X^T da over the 32 points: da goes through LDS to put points on the k index.
+    // dW_s += X^T da over the tile's points: da goes through LDS to put points on the k index.
     if constexpr (!BF) {
       // myda[p * (GS + 1) + gl]
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb)
 #pragma unroll
-        for (int pb = 0; pb < 2; ++pb)
+        for (int pb = 0; pb < PB; ++pb)
 #pragma unroll
           for (int r = 0; r < 4; ++r) myda[(16 * pb + i) * (GS + 1) + 16 * gb + 4 * j + r] = dw[gb][pb][r];
       wave_lds_sync();
 #pragma unroll
-      for (int pb = 0; pb < 2; ++pb)
+      for (int pb = 0; pb < PB; ++pb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int pl = 16 * pb + 4 * j + r;
@@ -1035,7 +1190,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb)
 #pragma unroll
-        for (int pb = 0; pb < 2; ++pb)
+        for (int pb = 0; pb < PB; ++pb)
 #pragma unroll
           for (int r = 0; r < 4; ++r) t16[(16 * gb + 4 * j + r) * 40 + 16 * pb + i] = f_to_bf(dw[gb][pb][r]);
       wave_lds_sync();
@@ -1126,33 +1281,35 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
 // =======================================================================================
 // Dispatch over the compile-time tiling
 // =======================================================================================
-#define FS_DISPATCH_KERNEL(KNAME)                                                           \
-  template <bool BF, int D, int GS, int NS, int NP>                                        \
+#define FS_DISPATCH_KERNEL(KNAME, ...)                                                      \
+  template <bool BF, int D, int GS, int NS, int NP, int PB>                                \
   hipError_t run_##KNAME(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {  \
     dim3 grid(cfg.chunks, BH);                                                             \
-    hipLaunchKernelGGL((KNAME<BF, D, GS, NS, NP>), grid, dim3(64 * NS * NP), 0, st, a);    \
+    hipLaunchKernelGGL((KNAME<__VA_ARGS__>), grid, dim3(64 * NS * NP), 0, st, a);          \
     return hipGetLastError();                                                              \
   }
-FS_DISPATCH_KERNEL(k_slice)
-FS_DISPATCH_KERNEL(k_deslice)
-FS_DISPATCH_KERNEL(k_bwd_a)
-FS_DISPATCH_KERNEL(k_bwd_b)
+FS_DISPATCH_KERNEL(k_slice, BF, D, GS, NS, NP)
+FS_DISPATCH_KERNEL(k_deslice, BF, D, GS, NS, NP)
+FS_DISPATCH_KERNEL(k_bwd_a, BF, D, GS, NS, NP)
+FS_DISPATCH_KERNEL(k_bwd_b, BF, D, GS, NS, NP, PB)
 
-// Supported (GS, NS, NP) tilings; pick_cfg in fs_api.cpp chooses among exactly these.
-#define FS_TILINGS(X, BF, D)                                                    \
-  X(BF, D, 16, 1, 4) X(BF, D, 32, 1, 4) X(BF, D, 64, 1, 4) X(BF, D, 64, 2, 2) \
-  X(BF, D, 64, 4, 1) X(BF, D, 64, 8, 1) X(BF, D, 64, 16, 1)
+// Supported (GS, NS, NP, PB) tilings; pick_cfg in fs_api.cpp chooses among exactly these.
+// PB = 1 (16-point tiles) exists for the fp32 backward pass B only.
+#define FS_TILINGS(X, BF, D)                                                              \
+  X(BF, D, 16, 1, 4, 2) X(BF, D, 32, 1, 4, 2) X(BF, D, 64, 1, 4, 2) X(BF, D, 64, 2, 2, 2) \
+  X(BF, D, 64, 4, 1, 2) X(BF, D, 64, 8, 1, 2) X(BF, D, 64, 16, 1, 2)                     \
+  X(BF, D, 16, 1, 4, 1) X(BF, D, 32, 1, 4, 1) X(BF, D, 64, 1, 4, 1)
 
 template <int PASS, bool BF, int D>
 hipError_t run_tiled(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
-#define FS_CASE(BF_, D_, GS_, NS_, NP_)                                              \
-  if (cfg.GS == GS_ && cfg.NS == NS_ && cfg.NP == NP_) {                             \
-    if constexpr (!(BF_ && GS_ < 32)) {                                              \
-      if constexpr (PASS == PASS_SLICE) return run_k_slice<BF_, D_, GS_, NS_, NP_>(cfg, BH, a, st);     \
-      if constexpr (PASS == PASS_DESLICE) return run_k_deslice<BF_, D_, GS_, NS_, NP_>(cfg, BH, a, st); \
-      if constexpr (PASS == PASS_BWD_A) return run_k_bwd_a<BF_, D_, GS_, NS_, NP_>(cfg, BH, a, st);     \
-      if constexpr (PASS == PASS_BWD_B) return run_k_bwd_b<BF_, D_, GS_, NS_, NP_>(cfg, BH, a, st);     \
-    }                                                                                \
+#define FS_CASE(BF_, D_, GS_, NS_, NP_, PB_)                                                   \
+  if (cfg.GS == GS_ && cfg.NS == NS_ && cfg.NP == NP_ && cfg.PB == PB_) {                      \
+    if constexpr (!(BF_ && GS_ < 32) && (PB_ == 2 || (!BF_ && PASS == PASS_BWD_B))) {          \
+      if constexpr (PASS == PASS_SLICE) return run_k_slice<BF_, D_, GS_, NS_, NP_, PB_>(cfg, BH, a, st);     \
+      if constexpr (PASS == PASS_DESLICE) return run_k_deslice<BF_, D_, GS_, NS_, NP_, PB_>(cfg, BH, a, st); \
+      if constexpr (PASS == PASS_BWD_A) return run_k_bwd_a<BF_, D_, GS_, NS_, NP_, PB_>(cfg, BH, a, st);     \
+      if constexpr (PASS == PASS_BWD_B) return run_k_bwd_b<BF_, D_, GS_, NS_, NP_, PB_>(cfg, BH, a, st);     \
+    }                                                                                          \
   }
   FS_TILINGS(FS_CASE, BF, D)
 #undef FS_CASE
