@@ -1,0 +1,193 @@
+"""Summaries of rocprofv3 output for the library's kernels (host-side post-processing only).
+
+Two summaries, both written as short text (markdown) plus, for traffic, a JSON record:
+
+* ``stats``: per-kernel call count and average / min / max duration from the
+  ``kernel_stats.csv`` that ``rocprofv3 --kernel-trace --stats -f csv`` writes.
+* ``traffic``: HBM bytes per launch of each kernel from two counter runs
+  (``--pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE``, ``-f csv``). Each counter is calibrated by
+  what it reads for a plain device-to-device copy of known size that the profiled program
+  issues first (``bench.py --copy-calibration-mib M``): the copy reads and writes exactly M MiB,
+  so the factor is M MiB over the counter's reading for that dispatch.
+
+The JSON record carries a hash of the kernel sources; ``bench.py`` reports the traffic only
+while the hash matches the sources it runs.
+
+Usage::
+
+    python -m paper_2609_32525_amd.profiling stats DIR/kernel_stats.csv --command "..." --out F.md
+    python -m paper_2609_32525_amd.profiling traffic FETCH_DIR WRITE_DIR --copy-mib 256 \
+        --workload surface --command "..." --out profiles/pmc_<kernel>_<workload>
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import csv
+import glob
+import hashlib
+import json
+import os
+import re
+import subprocess
+from typing import Dict, List, Tuple
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCES = ("fs_kernels.hip", "fs_tokens.hip", "fs_api.cpp", "fs_internal.h")
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+
+
+def kernel_source_hash() -> str:
+    """First 16 hex digits of the SHA-256 of the kernel and launcher sources."""
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(_HERE, "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def short_name(name: str) -> str:
+    """Demangled kernel name without namespaces, argument list and return type."""
+    if name.startswith("_Z"):
+        try:
+            name = subprocess.run(["c++filt", name], capture_output=True, text=True,
+                                  check=True).stdout.strip()
+        except (OSError, subprocess.CalledProcessError):
+            pass
+    name = re.sub(r"fs::\(anonymous namespace\)::|fs::", "", name)
+    name = re.sub(r"^void ", "", name)
+    depth, cut = 0, len(name)
+    for i, c in enumerate(name):      # drop the argument list: first '(' outside <...>
+        if c == "<":
+            depth += 1
+        elif c == ">":
+            depth -= 1
+        elif c == "(" and depth == 0:
+            cut = i
+            break
+    return name[:cut].strip()
+
+
+def _find(path: str, pattern: str) -> str:
+    if os.path.isfile(path):
+        return path
+    hits = sorted(glob.glob(os.path.join(path, "**", pattern), recursive=True))
+    if not hits:
+        raise FileNotFoundError(f"no {pattern} under {path}")
+    return hits[0]
+
+
+def kernel_stats(path: str) -> List[Tuple[str, int, float, float, float, float]]:
+    """(kernel, calls, total_us, avg_us, min_us, max_us) sorted by total time."""
+    rows = []
+    with open(_find(path, "*kernel_stats.csv")) as fh:
+        for r in csv.DictReader(fh):
+            ns = 1e-3
+            rows.append((short_name(r["Name"]), int(r["Calls"]), float(r["TotalDurationNs"]) * ns,
+                         float(r["AverageNs"]) * ns, float(r["MinNs"]) * ns,
+                         float(r["MaxNs"]) * ns))
+    rows.sort(key=lambda t: -t[2])
+    return rows
+
+
+def counter_values(path: str, counter: str) -> Dict[str, List[float]]:
+    """Per-dispatch values (KiB for FETCH_SIZE / WRITE_SIZE) of one counter, by kernel."""
+    per_dispatch: Dict[Tuple[str, str], float] = collections.defaultdict(float)
+    with open(_find(path, "*counter_collection.csv")) as fh:
+        for r in csv.DictReader(fh):
+            if r["Counter_Name"] != counter:
+                continue
+            per_dispatch[(r["Dispatch_Id"], r["Kernel_Name"])] += float(r["Counter_Value"])
+    out: Dict[str, List[float]] = collections.defaultdict(list)
+    for (_, k), v in sorted(per_dispatch.items(), key=lambda kv: int(kv[0][0])):
+        out[k].append(v)
+    return out
+
+
+def calibrated_traffic(fetch_dir: str, write_dir: str, copy_mib: float):
+    """Per-kernel average (fetch, write) bytes per launch, each counter scaled by its reading
+    for the copy of ``copy_mib`` MiB (only copy dispatches of at least half that size count)."""
+    f = counter_values(fetch_dir, "FETCH_SIZE")
+    w = counter_values(write_dir, "WRITE_SIZE")
+    kib = copy_mib * 1024.0
+
+    def scale(vals, what):
+        big = [v for v in vals if v > 0.5 * kib]
+        if not big:
+            raise RuntimeError(f"no calibration copy of {copy_mib} MiB in the {what} run")
+        return kib / (sum(big) / len(big))
+
+    cf = scale([v for k, vs in f.items() if short_name(k) == COPY_KERNEL for v in vs], "fetch")
+    cw = scale([v for k, vs in w.items() if short_name(k) == COPY_KERNEL for v in vs], "write")
+    res = {}
+    for k in f:
+        if short_name(k).startswith(("__amd", "at::")) or k not in w:
+            continue
+        fb = sum(f[k]) / len(f[k]) * cf * 1024.0
+        wb = sum(w[k]) / len(w[k]) * cw * 1024.0
+        res[short_name(k)] = {"fetch_bytes": fb, "write_bytes": wb, "dispatches": len(f[k])}
+    return cf, cw, res
+
+
+def _main():
+    ap = argparse.ArgumentParser(description=__doc__,
+                                 formatter_class=argparse.RawDescriptionHelpFormatter)
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("path")
+    s.add_argument("--command", required=True, help="the rocprofv3 command that made it")
+    s.add_argument("--title", default="Kernel durations")
+    s.add_argument("--out", required=True)
+    t = sub.add_parser("traffic")
+    t.add_argument("fetch")
+    t.add_argument("write")
+    t.add_argument("--copy-mib", type=float, required=True)
+    t.add_argument("--workload", required=True)
+    t.add_argument("--kernel", default="k_bwd_b", help="kernel whose JSON record bench reads")
+    t.add_argument("--command", action="append", required=True)
+    t.add_argument("--out", required=True, help="output path without extension")
+    a = ap.parse_args()
+
+    if a.cmd == "stats":
+        rows = kernel_stats(a.path)
+        tot = sum(r[2] for r in rows) or 1.0
+        lines = [f"# {a.title}", "", "Command:", "", "```", a.command, "```", "",
+                 f"Kernel sources sha256[:16] = `{kernel_source_hash()}`", "",
+                 "| kernel | calls | avg us | min us | max us | % time |",
+                 "|---|---:|---:|---:|---:|---:|"]
+        for n, c, tt, av, mn, mx in rows:
+            lines.append(f"| `{n}` | {c} | {av:.2f} | {mn:.2f} | {mx:.2f} | {100 * tt / tot:.1f} |")
+        with open(a.out, "w") as fh:
+            fh.write("\n".join(lines) + "\n")
+        print("\n".join(lines))
+        return
+
+    cf, cw, res = calibrated_traffic(a.fetch, a.write, a.copy_mib)
+    lines = [f"# HBM traffic per launch, workload {a.workload}", "",
+             "Commands (one counter per run):", "", "```"] + a.command + ["```", "",
+             f"Calibration: a {a.copy_mib:g} MiB device copy; FETCH_SIZE x{cf:.3f}, "
+             f"WRITE_SIZE x{cw:.3f}.", "",
+             f"Kernel sources sha256[:16] = `{kernel_source_hash()}`", "",
+             "| kernel | dispatches | fetch MiB | write MiB |", "|---|---:|---:|---:|"]
+    for n, r in res.items():
+        lines.append(f"| `{n}` | {r['dispatches']} | {r['fetch_bytes'] / 2**20:.2f} | "
+                     f"{r['write_bytes'] / 2**20:.2f} |")
+    with open(a.out + ".md", "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+    mine = [n for n in res if n.startswith(a.kernel + "<") or n == a.kernel]
+    if mine:
+        r = res[mine[0]]
+        rec = {"workload": a.workload, "kernel": mine[0],
+               "kernel_source_sha256": kernel_source_hash(),
+               "fetch_scale": cf, "write_scale": cw, "copy_mib": a.copy_mib,
+               "fetch_bytes_per_launch": r["fetch_bytes"],
+               "write_bytes_per_launch": r["write_bytes"],
+               "traffic_bytes_per_launch": r["fetch_bytes"] + r["write_bytes"],
+               "commands": a.command}
+        with open(a.out + ".json", "w") as fh:
+            json.dump(rec, fh, indent=1)
+
+
+if __name__ == "__main__":
+    _main()
