@@ -108,8 +108,8 @@ def main():
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (the point-sharded "
-              "all-reduce design is described in DESIGN.md); run with --gpus 1.",
+        print("bench.py measures one GPU: the library has no multi-GPU path (sharding the points "
+              "would add one all-reduce of the token partials per pass); run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
 

@@ -35,8 +35,9 @@ Parity: every function here is pinned by the CPU tests (partition of unity, the 
 the zero-logit / averaging-operator reduction of App. A.2, hard-assignment limit against a
 group-by mean, brute-force loops on tiny inputs, invariances, the per-point cancellation of
 App. F.2, and central finite differences of the backward). The value of eps, the sharing of
-W_s across heads and the attention details are readings of under-specified text (listed in
-the design doc); within those readings no function is unpinned.
+W_s across heads and the attention details are readings of under-specified text (eps is an
+argument, W_s may be shared or per head, the attention is one head over the V channels with
+scale 1/sqrt(V)); within those readings no function is unpinned.
 """
 from __future__ import annotations
 

@@ -9,7 +9,7 @@
 // (paper: Sec. 2 "The Transolver layer"; App. F.1 "Kernel design"; App. F.2 "Temperature
 // gradients"; the backward is the exact derivative of the forward.)
 //
-// Design (see DESIGN.md): a wavefront owns GS consecutive slots and a 32-point tile (two
+// Design: a wavefront owns GS consecutive slots and a 32-point tile (two
 // 16-point MFMA blocks); NS = G / GS wavefronts share one point tile and exchange per-point
 // softmax statistics through LDS, so the slice weights never leave registers and no N x G
 // tensor is ever written. The logits are an MFMA contraction over the head width; the

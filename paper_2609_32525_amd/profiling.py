@@ -38,11 +38,15 @@ COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
 
 def kernel_source_hash() -> str:
-    """First 16 hex digits of the SHA-256 of the kernel and launcher sources."""
+    """First 16 hex digits of the SHA-256 of the kernel and launcher sources, with line
+    comments and blank lines removed (editing a comment does not change a kernel)."""
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
-        with open(os.path.join(_HERE, "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(_HERE, "csrc", f)) as fh:
+            for line in fh:
+                code = re.sub(r"//.*$", "", line).rstrip()
+                if code:
+                    h.update(code.encode() + b"\n")
     return h.hexdigest()[:16]
 
 
@@ -156,6 +160,8 @@ def _main():
                  "| kernel | calls | avg us | min us | max us | % time |",
                  "|---|---:|---:|---:|---:|---:|"]
         for n, c, tt, av, mn, mx in rows:
+            if n.startswith("at::"):
+                continue
             lines.append(f"| `{n}` | {c} | {av:.2f} | {mn:.2f} | {mx:.2f} | {100 * tt / tot:.1f} |")
         with open(a.out, "w") as fh:
             fh.write("\n".join(lines) + "\n")

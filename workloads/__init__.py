@@ -8,7 +8,8 @@ Every tensor comes from its own sub-stream ``numpy.random.default_rng([SEED, cfg
 so that adding a tensor never shifts another one. Values are drawn in fp32 and, for bf16
 storage, rounded to the nearest bf16 (ties to even) and kept as exactly representable fp32.
 
-Workloads (the readings of under-specified choices are listed in the design doc):
+Workloads (shapes and value distributions of the paper's 3D-flow layers; the temperature and
+W_s choices open in the text are the ``tau_mode`` / ``ws_mode`` fields below):
 
 =========  ======  =====  =========  ==  ==  ====  =====================================
 name       dtype   B      N          H   D   G     mix / special structure
