@@ -4,11 +4,15 @@ from __future__ import annotations
 import os
 import subprocess
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libflashslice.so")
-SOURCES = [os.path.join(HERE, "csrc", f) for f in ("fs_kernels.hip", "fs_tokens.hip", "fs_api.cpp")]
+OBJDIR = os.path.join(HERE, "_build")
+SOURCES = [os.path.join(HERE, "csrc", f) for f in (
+    "fs_pass_bwd_b.hip", "fs_pass_slice.hip", "fs_pass_deslice.hip", "fs_pass_bwd_a.hip",
+    "fs_kernels.hip", "fs_tokens.hip", "fs_tokmix.hip", "fs_api.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in the generated code.
@@ -17,18 +21,34 @@ FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
          "-I", os.path.join(ROOT, "include"), "-Wno-unused-result"]
 
 
-def build(verbose: bool = False, extra=None) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC] + FLAGS + (extra or []) + SOURCES + ["-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
+def _run(cmd):
     res = subprocess.run(cmd, capture_output=True, text=True)
     noise = "is not a recognized feature for this target"
     err = "\n".join(l for l in res.stderr.splitlines() if noise not in l)
     if res.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
-    if verbose and err.strip():
-        print(err, file=sys.stderr)
+        raise RuntimeError(f"hipcc failed ({res.returncode}): {' '.join(cmd)}\n{err}")
+    return err
+
+
+def build(verbose: bool = False, extra=None) -> str:
+    """Compiles every source to an object (in parallel), then links the shared library."""
+    os.makedirs(OBJDIR, exist_ok=True)
+    cflags = [f for f in FLAGS if f != "-shared"] + (extra or [])
+    objs, cmds = [], []
+    for src in SOURCES:
+        obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
+        objs.append(obj)
+        cmds.append([HIPCC] + cflags + ["-c", src, "-o", obj])
+    with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 1)) as ex:
+        errs = list(ex.map(_run, cmds))
+    tmp = LIB + ".tmp"
+    errs.append(_run([HIPCC] + FLAGS + (extra or []) + objs + ["-o", tmp]))
+    if verbose:
+        for c in cmds:
+            print(" ".join(c), flush=True)
+        for e in errs:
+            if e.strip():
+                print(e, file=sys.stderr)
     os.replace(tmp, LIB)
     return LIB
 

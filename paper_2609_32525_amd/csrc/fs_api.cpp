@@ -343,7 +343,8 @@ int fs_mix_bwd(const fs_problem* prob, const fs_mix_desc* mix, const float* z,
   return hip_status(fs::launch_mix_bwd(
       g, mix_args(mix), z, nullptr, nullptr, attn_probs, dzmix, dz, nullptr, nullptr, nullptr,
       reinterpret_cast<float*>(w + L.scr), reinterpret_cast<float*>(w + L.partM),
-      mix->kind == FS_MIX_IDENTITY ? nullptr : dmix_params, static_cast<hipStream_t>(hip_stream)));
+      mix->kind == FS_MIX_IDENTITY ? nullptr : dmix_params, true,
+      static_cast<hipStream_t>(hip_stream)));
 }
 
 int fs_deslice_fwd(const fs_problem* prob, const void* x, const float* Ws, const float* bias,

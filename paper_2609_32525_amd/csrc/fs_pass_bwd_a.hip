@@ -1,0 +1,125 @@
+// Streaming pass: backward pass A (dzmix partials = w^T dout).
+// Kernel design and MFMA lane layouts are described at the top of fs_stream.h.
+
+#include "fs_stream.h"
+
+namespace fs {
+namespace {
+
+// =======================================================================================
+// Backward pass A: dzmix = w^T dout (partials per workgroup)
+// =======================================================================================
+template <bool BF, int D, int GS, int NS, int NP>
+__global__ __launch_bounds__(64 * NS * NP) void k_bwd_a(PassArgs a) {
+  constexpr int GB = GS / 16, VB = D / 16;
+  constexpr bool SPLIT = BF;
+  using T = typename Store<BF>::T;
+  const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
+  const int wave = threadIdx.x >> 6, ws = wave % NS, wp = wave / NS;
+  const HeadCtx c = head_ctx<D>(a, ws, GS);
+  const int64_t rs = (int64_t)a.H * D;
+  const T* xb = (const T*)a.x + c.off;
+  const T* db = (const T*)a.dout + c.off;
+  const float* lse = a.lse_in + (int64_t)c.bh * a.N;
+
+  SlotOp<BF, D, GB> wop;
+  load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, c.sc, i, j);
+  float bS[GB];
+#pragma unroll
+  for (int gb = 0; gb < GB; ++gb) bS[gb] = c.sc * c.bias[c.g0 + 16 * gb + i];
+  f4 Z[GB][VB];
+#pragma unroll
+  for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb) Z[gb][vb] = zero4();
+
+  const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
+  const int64_t pend = min(a.N, pbeg + a.chunk_pts);
+  const int ntile = pend > pbeg ? (int)((pend - pbeg + 32 * NP - 1) / (32 * NP)) : 0;
+
+  // software pipeline: the next tile's rows are loaded before the current tile is computed
+  struct Tile {
+    RowOp<BF, D> xo[2];
+    float lse2[2][4];
+    PtGather<BF, VB> g;
+  };
+  auto load_tile = [&](Tile& tt, int t) {
+    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      const int64_t p = p0 + 16 * pb + i;
+      load_row<BF, D>(tt.xo[pb], xb + p * rs, p < pend, j);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t q = p0 + 16 * pb + 4 * j + r;
+        tt.lse2[pb][r] = q < pend ? lse[q] : kMasked;
+      }
+    }
+    gather_points<BF, VB>(tt.g, db, rs, p0, pend, i, j);
+  };
+  Tile cur;
+  if (ntile > 0) load_tile(cur, 0);
+  for (int t = 0; t < ntile; ++t) {
+    Tile nxt;
+    if (t + 1 < ntile) load_tile(nxt, t + 1);
+    const RowOp<BF, D>* xo = cur.xo;
+    const float(*lse2)[4] = cur.lse2;
+    f4 w[2][GB];
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb) {
+        f4 acc = mm_row_slot<BF, D, GB, SPLIT>(xo[pb], wop, gb, splat4(bS[gb]));
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r] = __builtin_amdgcn_exp2f(acc[r] - lse2[pb][r]);
+        w[pb][gb] = acc;
+      }
+    mm_points<BF, GB, VB>(Z, w, cur.g);
+    cur = nxt;
+  }
+
+  float* pZ = a.part + ((int64_t)c.bh * a.chunks + blockIdx.x) * a.G * D;
+  if constexpr (NP > 1) {
+    __shared__ f4 red[NP - 1][NS][GB][VB][64];
+    if (wp > 0) {
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+        for (int vb = 0; vb < VB; ++vb) red[wp - 1][ws][gb][vb][lane] = Z[gb][vb];
+    }
+    __syncthreads();
+    if (wp == 0) {
+      for (int q = 0; q < NP - 1; ++q)
+#pragma unroll
+        for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+          for (int vb = 0; vb < VB; ++vb) Z[gb][vb] += red[q][ws][gb][vb][lane];
+    }
+  }
+  if (wp == 0) {
+#pragma unroll
+    for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+      for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          pZ[(int64_t)(c.g0 + 16 * gb + 4 * j + r) * D + 16 * vb + i] = Z[gb][vb][r];
+  }
+}
+
+template <bool BF, int D, int GS, int NS, int NP, int PB>
+struct Run_k_bwd_a {
+  static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
+    dim3 grid(cfg.chunks, BH);
+    hipLaunchKernelGGL((k_bwd_a<BF, D, GS, NS, NP>), grid, dim3(64 * NS * NP), 0, st, a);
+    return hipGetLastError();
+  }
+};
+
+}  // namespace
+
+hipError_t run_pass_bwd_a(const Geom& g, const PassArgs& a, hipStream_t st) {
+  return run_pass_tilings<PASS_BWD_A, Run_k_bwd_a>(g, a, st);
+}
+
+}  // namespace fs

@@ -1,0 +1,428 @@
+// Streaming pass: backward pass B (point gradients and parameter partials).
+// Kernel design and MFMA lane layouts are described at the top of fs_stream.h.
+
+#include "fs_stream.h"
+
+namespace fs {
+namespace {
+
+// =======================================================================================
+// Backward pass B: point gradients and parameter partials
+// partial layout per workgroup: [D * G] dW_s (row-major (D, G)), [G] dbias, [2] fp64 dtau
+// PB: 16-point blocks per tile (1 or 2; bf16 needs 2: its contraction over points has K=32).
+// With at most two slot groups, the per-head operands live in LDS as register images shared
+// by the workgroup's wavefronts and are read where they are used, which keeps the register
+// count (and so the number of resident wavefronts) in line with the other passes.
+// =======================================================================================
+template <bool BF, int D, int GS, int NS, int NP, int PB>
+__global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
+  static_assert(PB == 2 || !BF, "bf16 contracts over 32 points");
+  constexpr int GB = GS / 16, VB = D / 16, DB = D / 16, TP = 16 * PB;
+  constexpr bool SPLIT = BF;
+  using T = typename Store<BF>::T;
+  using SOp = SlotOp<BF, D, GB>;
+  using UOp = GOp<BF, GB, VB>;
+  using XOp = GOp<BF, GB, DB>;
+  // operands in LDS when at most two slot groups share a tile and the images fit in 64 KB
+  constexpr bool OPL =
+      NS <= 2 && (size_t)NS * 64 * (3 * sizeof(SOp) + sizeof(UOp) + sizeof(XOp)) <= 65536;
+  const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
+  const int wave = threadIdx.x >> 6, ws = wave % NS, wp = wave / NS;
+  const HeadCtx c = head_ctx<D>(a, ws, GS);
+  const int64_t rs = (int64_t)a.H * D;
+  const T* xb = (const T*)a.x + c.off;
+  const T* fb = (const T*)a.fx + c.off;
+  const T* gb_ = (const T*)a.dout + c.off;
+  T* dxb = (T*)a.out + c.off;
+  T* dfb = (T*)a.out2 + c.off;
+  const float* lse = a.lse_in + (int64_t)c.bh * a.N;
+  const float inv_tau = 1.0f / a.tau[c.h];
+  const float* zm = a.zmix + (int64_t)c.bh * a.G * D;
+  const float* dU = a.dU + (int64_t)c.bh * a.G * D;
+
+  // dw enters only through da = w (dw - sum_g w dw), which is unchanged when one vector is
+  // added to every token of zmix or dU, or one constant to every ds_g (the weights sum to
+  // one). Subtracting the mass-weighted slot means first keeps the rounding of these
+  // operands relative to what actually differs between slots.
+  const float* cen = a.cen + (int64_t)c.bh * (2 * D + 1);
+  float bT[GB][4], dsT[GB][4];
+#pragma unroll
+  for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      bT[gb][r] = c.sc * c.bias[c.g0 + 16 * gb + 4 * j + r];
+      dsT[gb][r] = a.ds[(int64_t)c.bh * a.G + c.g0 + 16 * gb + 4 * j + r] - cen[2 * D];
+    }
+
+  // operands: W_s (logits), zmix and dU (dw, contraction over v), dU (dfx) and W_s / tau (dx)
+  constexpr int kOpChunks = OPL ? 3 * lds_chunks<SOp>() + lds_chunks<UOp>() + lds_chunks<XOp>() : 1;
+  __shared__ uint4 opl[OPL ? NS : 1][kOpChunks];
+  SOp wop_r, zvop_r, uvop_r;
+  UOp ugop_r;
+  XOp wgop_r;
+  {
+    SOp t0, t1, t2;
+    UOp t3;
+    XOp t4;
+    if (!OPL || wp == 0) {
+      load_slotop<BF, D, GB, true, SPLIT>(t0, c.W, a.G, c.g0, c.sc, i, j);
+      load_slotop<BF, D, GB, false, false>(t1, zm, D, c.g0, 1.0f, i, j, cen);
+      load_slotop<BF, D, GB, false, false>(t2, dU, D, c.g0, 1.0f, i, j, cen + D);
+      load_gop<BF, GB, VB, false>(t3, dU, D, c.g0, 1.0f, i, j);
+      load_gop<BF, GB, DB, true>(t4, c.W, a.G, c.g0, inv_tau, i, j);
+    }
+    if constexpr (OPL) {
+      uint4* b = opl[ws];
+      if (wp == 0) {
+        lds_put(t0, b, lane);
+        lds_put(t1, b + lds_chunks<SOp>(), lane);
+        lds_put(t2, b + 2 * lds_chunks<SOp>(), lane);
+        lds_put(t3, b + 3 * lds_chunks<SOp>(), lane);
+        lds_put(t4, b + 3 * lds_chunks<SOp>() + lds_chunks<UOp>(), lane);
+      }
+      __syncthreads();
+    } else {
+      wop_r = t0;
+      zvop_r = t1;
+      uvop_r = t2;
+      ugop_r = t3;
+      wgop_r = t4;
+    }
+  }
+  const uint4* opb = opl[OPL ? ws : 0];
+  auto get_w = [&](SOp& o) { if constexpr (OPL) lds_get(o, opb, lane); else o = wop_r; };
+  auto get_zv = [&](SOp& o) { if constexpr (OPL) lds_get(o, opb + lds_chunks<SOp>(), lane); else o = zvop_r; };
+  auto get_uv = [&](SOp& o) { if constexpr (OPL) lds_get(o, opb + 2 * lds_chunks<SOp>(), lane); else o = uvop_r; };
+  auto get_ug = [&](UOp& o) { if constexpr (OPL) lds_get(o, opb + 3 * lds_chunks<SOp>(), lane); else o = ugop_r; };
+  auto get_wg = [&](XOp& o) {
+    if constexpr (OPL) lds_get(o, opb + 3 * lds_chunks<SOp>() + lds_chunks<UOp>(), lane); else o = wgop_r;
+  };
+
+  f4 dW[DB][GB];
+  float dbacc[GB][4];
+  double dtacc = 0.0;
+#pragma unroll
+  for (int gb = 0; gb < GB; ++gb) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dbacc[gb][r] = 0.f;
+#pragma unroll
+    for (int d = 0; d < DB; ++d) dW[d][gb] = zero4();
+  }
+
+  __shared__ float cx[NS > 1 ? NP : 1][NS > 1 ? NS : 1][2][TP];
+  // The dfx / dx exchange buffer (NS > 1) and the per-wave da transpose buffer are never live
+  // at the same time (a workgroup barrier separates every exchange from the transposes of
+  // the previous and the next tile), so they share one LDS allocation.
+  // gx: [NP][NS][VB][PB][64] f4; da transpose: fp32 [TP points][GS + 1], bf16 [GS slots][40].
+  constexpr int kDaWords = BF ? (GS * 40 + 1) / 2 : TP * (GS + 1);
+  constexpr size_t kGxBytes = NS > 1 ? (size_t)NP * NS * VB * PB * 64 * sizeof(f4) : 0;
+  constexpr size_t kDaBytes = (size_t)NS * NP * kDaWords * sizeof(float);
+  __shared__ __attribute__((aligned(16))) char smem[kGxBytes > kDaBytes ? kGxBytes : kDaBytes];
+  f4* gx = reinterpret_cast<f4*>(smem);
+  float* myda = reinterpret_cast<float*>(smem) + (size_t)wave * kDaWords;
+
+  const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
+  const int64_t pend = min(a.N, pbeg + a.chunk_pts);
+  const int ntile = pend > pbeg ? (int)((pend - pbeg + TP * NP - 1) / (TP * NP)) : 0;
+
+  for (int t = 0; t < ntile; ++t) {
+    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * TP;
+    RowOp<BF, D> xo[PB], go[PB], fo[PB];
+    float lse2[PB];
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      const int64_t p = p0 + 16 * pb + i;
+      const bool ok = p < pend;
+      load_row<BF, D>(xo[pb], xb + p * rs, ok, j);
+      load_row<BF, D>(go[pb], gb_ + p * rs, ok, j);
+      load_row<BF, D>(fo[pb], fb + p * rs, ok, j);
+      lse2[pb] = ok ? lse[p] : kMasked;
+    }
+    // T-layout tiles: rows = slots g0 + 16 gb + 4 j + r, cols = points 16 pb + i
+    f4 tl[GB][PB], w[GB][PB], dw[GB][PB];
+    {
+      SOp wop;
+      get_w(wop);
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb) {
+          f4 acc = f4{bT[gb][0], bT[gb][1], bT[gb][2], bT[gb][3]};
+          acc = mm_slot_row<BF, D, GB, SPLIT>(wop, gb, xo[pb], acc);
+          f4 tt, ww;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            tt[r] = acc[r] - lse2[pb];
+            ww[r] = __builtin_amdgcn_exp2f(tt[r]);
+          }
+          tl[gb][pb] = tt;
+          w[gb][pb] = ww;
+        }
+    }
+    {
+      SOp zv, uv;
+      get_zv(zv);
+      get_uv(uv);
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb) {
+          f4 g = f4{dsT[gb][0], dsT[gb][1], dsT[gb][2], dsT[gb][3]};
+          g = mm_slot_row<BF, D, GB, false>(zv, gb, go[pb], g);
+          g = mm_slot_row<BF, D, GB, false>(uv, gb, fo[pb], g);
+          dw[gb][pb] = g;
+        }
+    }
+    // per point (column of the tile): c = sum_g w dw, the softmax correction, and
+    // tb = sum_g w t, the weighted mean of the shifted base-2 logits t = a2 - lse2
+    float cc[PB], tb[PB];
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb) {
+      float sum = 0.f, st = 0.f;
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          sum += w[gb][pb][r] * dw[gb][pb][r];
+          st += w[gb][pb][r] * tl[gb][pb][r];
+        }
+      cc[pb] = col4_sum(sum);
+      tb[pb] = col4_sum(st);
+    }
+    if constexpr (NS > 1) {
+      if (j == 0) {
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb) {
+          cx[wp][ws][0][16 * pb + i] = cc[pb];
+          cx[wp][ws][1][16 * pb + i] = tb[pb];
+        }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        float sum = 0.f, st = 0.f;
+        for (int s = 0; s < NS; ++s) {
+          sum += cx[wp][s][0][16 * pb + i];
+          st += cx[wp][s][1][16 * pb + i];
+        }
+        cc[pb] = sum;
+        tb[pb] = st;
+      }
+    }
+    // da = w (dw - c); dbias partials; dtau partial (App. F.2): sum_g da a = sum_g da (a - k)
+    // for any per-point k because sum_g da = 0; with k = lse + tb the first-order effect of
+    // the rounding of c on the sum cancels (sum_g w (t - tb) = 0).
+    float dts = 0.f;
+#pragma unroll
+    for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float da = w[gb][pb][r] * (dw[gb][pb][r] - cc[pb]);
+          dw[gb][pb][r] = da;
+          dts += da * (tl[gb][pb][r] - tb[pb]);
+          dbacc[gb][r] += da;
+        }
+    dtacc += (double)dts;
+    // dfx = w dU, dx = da W_s^T / tau (contractions over this wave's slots)
+    f4 gf[VB][PB], gx_[DB][PB];
+    {
+      UOp ug;
+      XOp wg;
+      get_ug(ug);
+      get_wg(wg);
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+#pragma unroll
+        for (int vb = 0; vb < VB; ++vb) gf[vb][pb] = mm_gop_tile<BF, GB, VB, PB>(ug, vb, w, pb, zero4());
+#pragma unroll
+        for (int d = 0; d < DB; ++d) gx_[d][pb] = mm_gop_tile<BF, GB, DB, PB>(wg, d, dw, pb, zero4());
+      }
+    }
+    if constexpr (NS > 1) {
+      __syncthreads();  // every wave has read cx and finished the previous da transposes
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        f4(*src)[PB] = half == 0 ? gf : gx_;
+        if (ws > 0) {
+#pragma unroll
+          for (int cb = 0; cb < VB; ++cb)
+#pragma unroll
+            for (int pb = 0; pb < PB; ++pb)
+              gx[(((size_t)wp * NS + ws) * VB + cb) * (64 * PB) + pb * 64 + lane] = src[cb][pb];
+        }
+        __syncthreads();
+        if (ws == 0) {
+          for (int s = 1; s < NS; ++s)
+#pragma unroll
+            for (int cb = 0; cb < VB; ++cb)
+#pragma unroll
+              for (int pb = 0; pb < PB; ++pb)
+                src[cb][pb] += gx[(((size_t)wp * NS + s) * VB + cb) * (64 * PB) + pb * 64 + lane];
+        }
+        __syncthreads();
+      }
+    }
+    if (ws == 0) {
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        const int64_t p = p0 + 16 * pb + i;
+        if (p < pend) {
+#pragma unroll
+          for (int cb = 0; cb < VB; ++cb) {
+            T* d1 = dfb + p * rs + 16 * cb + 4 * j;
+            T* d2 = dxb + p * rs + 16 * cb + 4 * j;
+            if constexpr (!BF) {
+              *reinterpret_cast<float4*>(d1) =
+                  float4{gf[cb][pb][0], gf[cb][pb][1], gf[cb][pb][2], gf[cb][pb][3]};
+              *reinterpret_cast<float4*>(d2) =
+                  float4{gx_[cb][pb][0], gx_[cb][pb][1], gx_[cb][pb][2], gx_[cb][pb][3]};
+            } else {
+              *reinterpret_cast<uint2*>(d1) =
+                  uint2{f_to_bf(gf[cb][pb][0]) | ((unsigned)f_to_bf(gf[cb][pb][1]) << 16),
+                        f_to_bf(gf[cb][pb][2]) | ((unsigned)f_to_bf(gf[cb][pb][3]) << 16)};
+              *reinterpret_cast<uint2*>(d2) =
+                  uint2{f_to_bf(gx_[cb][pb][0]) | ((unsigned)f_to_bf(gx_[cb][pb][1]) << 16),
+                        f_to_bf(gx_[cb][pb][2]) | ((unsigned)f_to_bf(gx_[cb][pb][3]) << 16)};
+            }
+          }
+        }
+      }
+    }
+    // dW_s += X^T da over the tile's points: da goes through LDS to put points on the k index.
+    if constexpr (!BF) {
+      // myda[p * (GS + 1) + gl]
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) myda[(16 * pb + i) * (GS + 1) + 16 * gb + 4 * j + r] = dw[gb][pb][r];
+      wave_lds_sync();
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int pl = 16 * pb + 4 * j + r;
+          const int64_t p = p0 + pl;
+          float xv[DB];
+#pragma unroll
+          for (int d = 0; d < DB; ++d) xv[d] = p < pend ? xb[p * rs + 16 * d + i] : 0.f;
+#pragma unroll
+          for (int gb = 0; gb < GB; ++gb) {
+            const float bv = myda[pl * (GS + 1) + 16 * gb + i];
+#pragma unroll
+            for (int d = 0; d < DB; ++d) dW[d][gb] = mfma_f32(xv[d], bv, dW[d][gb]);
+          }
+        }
+      wave_lds_sync();
+    } else {
+      unsigned short* t16 = reinterpret_cast<unsigned short*>(myda);  // [GS][40]
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) t16[(16 * gb + 4 * j + r) * 40 + 16 * pb + i] = f_to_bf(dw[gb][pb][r]);
+      wave_lds_sync();
+      bf8 xa[DB];
+#pragma unroll
+      for (int d = 0; d < DB; ++d)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int64_t p = p0 + 16 * (e / 4) + 4 * j + (e % 4);
+          unsigned short h = 0;
+          if (p < pend) h = xb[p * rs + 16 * d + i];
+          xa[d][e] = __builtin_bit_cast(__bf16, h);
+        }
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb) {
+        const uint2 lo = *reinterpret_cast<const uint2*>(t16 + (16 * gb + i) * 40 + 4 * j);
+        const uint2 hi = *reinterpret_cast<const uint2*>(t16 + (16 * gb + i) * 40 + 16 + 4 * j);
+        const bf8 bt = __builtin_bit_cast(bf8, uint4{lo.x, lo.y, hi.x, hi.y});
+#pragma unroll
+        for (int d = 0; d < DB; ++d) dW[d][gb] = mfma_bf16(xa[d], bt, dW[d][gb]);
+      }
+      wave_lds_sync();
+    }
+  }
+
+  // ---- finish: reduce over lanes / waves and write the partial ---------------------------
+  float dbv[GB][4];
+#pragma unroll
+  for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) dbv[gb][r] = row16_sum(dbacc[gb][r]);
+  // dtau: fp64 sum over the wave, then over all waves of the workgroup in a fixed order
+  double dt = dtacc;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) dt += __shfl_xor(dt, off);
+  __shared__ double dtw[NS * NP];
+  if (lane == 0) dtw[wave] = dt;
+
+  float* pp = a.part + ((int64_t)c.bh * a.chunks + blockIdx.x) * ((int64_t)D * a.G + a.G + 2);
+  if constexpr (NP > 1) {
+    __shared__ f4 red[NP - 1][NS][DB][GB][64];
+    __shared__ float redb[NP - 1][NS][GB][4][16];
+    if (wp > 0) {
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb) {
+#pragma unroll
+        for (int d = 0; d < DB; ++d) red[wp - 1][ws][d][gb][lane] = dW[d][gb];
+        if (i == 0)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) redb[wp - 1][ws][gb][r][j] = dbv[gb][r];
+      }
+    }
+    __syncthreads();
+    if (wp == 0) {
+      for (int q = 0; q < NP - 1; ++q)
+#pragma unroll
+        for (int gb = 0; gb < GB; ++gb) {
+#pragma unroll
+          for (int d = 0; d < DB; ++d) dW[d][gb] += red[q][ws][d][gb][lane];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) dbv[gb][r] += redb[q][ws][gb][r][j];
+        }
+    }
+  } else {
+    __syncthreads();
+  }
+  if (wp == 0) {
+#pragma unroll
+    for (int gb = 0; gb < GB; ++gb) {
+#pragma unroll
+      for (int d = 0; d < DB; ++d)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          pp[(int64_t)(16 * d + 4 * j + r) * a.G + c.g0 + 16 * gb + i] = dW[d][gb][r] * inv_tau;
+      if (i == 0)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) pp[(int64_t)D * a.G + c.g0 + 16 * gb + 4 * j + r] = dbv[gb][r] * inv_tau;
+    }
+  }
+  if (threadIdx.x == 0) {
+    double s = 0.0;
+    for (int q = 0; q < NS * NP; ++q) s += dtw[q];
+    // (D * G + G) is even, so this slot is 8-byte aligned
+    *reinterpret_cast<double*>(pp + (int64_t)D * a.G + a.G) = -s * (double)kLn2 * (double)inv_tau;
+  }
+}
+
+template <bool BF, int D, int GS, int NS, int NP, int PB>
+struct Run_k_bwd_b {
+  static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
+    dim3 grid(cfg.chunks, BH);
+    hipLaunchKernelGGL((k_bwd_b<BF, D, GS, NS, NP, PB>), grid, dim3(64 * NS * NP), 0, st, a);
+    return hipGetLastError();
+  }
+};
+
+}  // namespace
+
+hipError_t run_pass_bwd_b(const Geom& g, const PassArgs& a, hipStream_t st) {
+  return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b>(g, a, st);
+}
+
+}  // namespace fs

@@ -1,0 +1,136 @@
+// Streaming pass: deslice (logits, w = exp2(a - lse), out = w zmix).
+// Kernel design and MFMA lane layouts are described at the top of fs_stream.h.
+
+#include "fs_stream.h"
+
+namespace fs {
+namespace {
+
+// =======================================================================================
+// Deslice pass
+// =======================================================================================
+template <bool BF, int D, int GS, int NS, int NP>
+__global__ __launch_bounds__(64 * NS * NP) void k_deslice(PassArgs a) {
+  constexpr int GB = GS / 16, VB = D / 16;
+  constexpr bool SPLIT = BF;
+  using T = typename Store<BF>::T;
+  const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
+  const int wave = threadIdx.x >> 6, ws = wave % NS, wp = wave / NS;
+  const HeadCtx c = head_ctx<D>(a, ws, GS);
+  const int64_t rs = (int64_t)a.H * D;
+  const T* xb = (const T*)a.x + c.off;
+  T* ob = (T*)a.out + c.off;
+  const float* lse = a.lse_in + (int64_t)c.bh * a.N;
+
+  SlotOp<BF, D, GB> wop;
+  load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, c.sc, i, j);
+  float bT[GB][4];
+#pragma unroll
+  for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) bT[gb][r] = c.sc * c.bias[c.g0 + 16 * gb + 4 * j + r];
+  GOp<BF, GB, VB> zop;
+  load_gop<BF, GB, VB, false>(zop, a.zmix + (int64_t)c.bh * a.G * D, D, c.g0, 1.0f, i, j);
+
+  __shared__ f4 ox[NS > 1 ? NP : 1][NS > 1 ? NS : 1][VB][2][64];
+
+  const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
+  const int64_t pend = min(a.N, pbeg + a.chunk_pts);
+  const int ntile = pend > pbeg ? (int)((pend - pbeg + 32 * NP - 1) / (32 * NP)) : 0;
+
+  // software pipeline: the next tile's rows are loaded before the current tile is computed
+  struct Tile {
+    RowOp<BF, D> xo[2];
+    float lse2[2];
+  };
+  auto load_tile = [&](Tile& tt, int t) {
+    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      const int64_t p = p0 + 16 * pb + i;
+      load_row<BF, D>(tt.xo[pb], xb + p * rs, p < pend, j);
+      tt.lse2[pb] = p < pend ? lse[p] : kMasked;
+    }
+  };
+  Tile cur;
+  if (ntile > 0) load_tile(cur, 0);
+  for (int t = 0; t < ntile; ++t) {
+    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+    Tile nxt;
+    if (t + 1 < ntile) load_tile(nxt, t + 1);
+    const RowOp<BF, D>* xo = cur.xo;
+    const float* lse2 = cur.lse2;
+    f4 w[GB][2];
+#pragma unroll
+    for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb) {
+        f4 acc = f4{bT[gb][0], bT[gb][1], bT[gb][2], bT[gb][3]};
+        acc = mm_slot_row<BF, D, GB, SPLIT>(wop, gb, xo[pb], acc);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[r] = __builtin_amdgcn_exp2f(acc[r] - lse2[pb]);
+        w[gb][pb] = acc;
+      }
+    f4 o[VB][2];
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb) o[vb][pb] = mm_gop_tile<BF, GB, VB>(zop, vb, w, pb, zero4());
+
+    if constexpr (NS > 1) {
+      if (ws > 0) {
+#pragma unroll
+        for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+          for (int pb = 0; pb < 2; ++pb) ox[wp][ws][vb][pb][lane] = o[vb][pb];
+      }
+      __syncthreads();
+      if (ws == 0) {
+        for (int s = 1; s < NS; ++s)
+#pragma unroll
+          for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+            for (int pb = 0; pb < 2; ++pb) o[vb][pb] += ox[wp][s][vb][pb][lane];
+      }
+      __syncthreads();
+    }
+    if (ws == 0) {
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb) {
+        const int64_t p = p0 + 16 * pb + i;
+        if (p < pend) {
+#pragma unroll
+          for (int vb = 0; vb < VB; ++vb) {
+            T* dst = ob + p * rs + 16 * vb + 4 * j;
+            if constexpr (!BF) {
+              *reinterpret_cast<float4*>(dst) =
+                  float4{o[vb][pb][0], o[vb][pb][1], o[vb][pb][2], o[vb][pb][3]};
+            } else {
+              const unsigned lo = f_to_bf(o[vb][pb][0]) | ((unsigned)f_to_bf(o[vb][pb][1]) << 16);
+              const unsigned hi = f_to_bf(o[vb][pb][2]) | ((unsigned)f_to_bf(o[vb][pb][3]) << 16);
+              *reinterpret_cast<uint2*>(dst) = uint2{lo, hi};
+            }
+          }
+        }
+      }
+    }
+    cur = nxt;
+  }
+}
+
+template <bool BF, int D, int GS, int NS, int NP, int PB>
+struct Run_k_deslice {
+  static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
+    dim3 grid(cfg.chunks, BH);
+    hipLaunchKernelGGL((k_deslice<BF, D, GS, NS, NP>), grid, dim3(64 * NS * NP), 0, st, a);
+    return hipGetLastError();
+  }
+};
+
+}  // namespace
+
+hipError_t run_pass_deslice(const Geom& g, const PassArgs& a, hipStream_t st) {
+  return run_pass_tilings<PASS_DESLICE, Run_k_deslice>(g, a, st);
+}
+
+}  // namespace fs

@@ -1,0 +1,211 @@
+// Streaming pass: slice (logits, per-point softmax, U += w^T F, s += sum w, lse).
+// Kernel design and MFMA lane layouts are described at the top of fs_stream.h.
+
+#include "fs_stream.h"
+
+namespace fs {
+namespace {
+
+// =======================================================================================
+// Slice pass
+// =======================================================================================
+template <bool BF, int D, int GS, int NS, int NP>
+__global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
+  constexpr int GB = GS / 16, VB = D / 16;
+  constexpr bool SPLIT = BF;
+  using T = typename Store<BF>::T;
+  const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
+  const int wave = threadIdx.x >> 6, ws = wave % NS, wp = wave / NS;
+  const HeadCtx c = head_ctx<D>(a, ws, GS);
+  const int64_t rs = (int64_t)a.H * D;
+  const T* xb = (const T*)a.x + c.off;
+  const T* fb = (const T*)a.fx + c.off;
+
+  SlotOp<BF, D, GB> wop;
+  load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, c.sc, i, j);
+  float bS[GB];
+#pragma unroll
+  for (int gb = 0; gb < GB; ++gb) bS[gb] = c.sc * c.bias[c.g0 + 16 * gb + i];
+
+  f4 U[GB][VB];
+  float sacc[GB];
+#pragma unroll
+  for (int gb = 0; gb < GB; ++gb) {
+    sacc[gb] = 0.f;
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb) U[gb][vb] = zero4();
+  }
+
+  __shared__ float st_m[NS > 1 ? 2 : 1][NP][NS][32];
+  __shared__ float st_l[NS > 1 ? 2 : 1][NP][NS][32];
+
+  const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
+  const int64_t pend = min(a.N, pbeg + a.chunk_pts);
+  const int ntile = pend > pbeg ? (int)((pend - pbeg + 32 * NP - 1) / (32 * NP)) : 0;
+
+  // software pipeline: the next tile's rows are loaded before the current tile is computed
+  struct Tile {
+    RowOp<BF, D> xo[2];
+    PtGather<BF, VB> f;
+  };
+  auto load_tile = [&](Tile& tt, int t) {
+    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      const int64_t p = p0 + 16 * pb + i;
+      load_row<BF, D>(tt.xo[pb], xb + p * rs, p < pend, j);
+    }
+    gather_points<BF, VB>(tt.f, fb, rs, p0, pend, i, j);
+  };
+  Tile cur;
+  if (ntile > 0) load_tile(cur, 0);
+  for (int t = 0; t < ntile; ++t) {
+    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+    Tile nxt;
+    if (t + 1 < ntile) load_tile(nxt, t + 1);
+    const RowOp<BF, D>* xo = cur.xo;
+    // S-layout logits: rows = points 16 pb + 4 j + r, cols = slots g0 + 16 gb + i
+    f4 w[2][GB];
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb)
+        w[pb][gb] = mm_row_slot<BF, D, GB, SPLIT>(xo[pb], wop, gb, splat4(bS[gb]));
+
+    float m[2][4], l[2][4];
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float mx = w[pb][0][r];
+#pragma unroll
+        for (int gb = 1; gb < GB; ++gb) mx = fmaxf(mx, w[pb][gb][r]);
+        m[pb][r] = row16_max(mx);
+        float sum = 0.f;
+#pragma unroll
+        for (int gb = 0; gb < GB; ++gb) {
+          const float e = __builtin_amdgcn_exp2f(w[pb][gb][r] - m[pb][r]);
+          w[pb][gb][r] = e;
+          sum += e;
+        }
+        l[pb][r] = row16_sum(sum);
+      }
+
+    float f[2][4], lse2[2][4];
+    if constexpr (NS == 1) {
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          f[pb][r] = 1.0f / l[pb][r];
+          lse2[pb][r] = m[pb][r] + __log2f(l[pb][r]);
+        }
+    } else {
+      const int par = t & 1;
+      if (i == 0) {
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            st_m[par][wp][ws][16 * pb + 4 * j + r] = m[pb][r];
+            st_l[par][wp][ws][16 * pb + 4 * j + r] = l[pb][r];
+          }
+      }
+      __syncthreads();
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int q = 16 * pb + 4 * j + r;
+          float M = st_m[par][wp][0][q];
+#pragma unroll
+          for (int s = 1; s < NS; ++s) M = fmaxf(M, st_m[par][wp][s][q]);
+          float L = 0.f;
+#pragma unroll
+          for (int s = 0; s < NS; ++s)
+            L += st_l[par][wp][s][q] * __builtin_amdgcn_exp2f(st_m[par][wp][s][q] - M);
+          f[pb][r] = __builtin_amdgcn_exp2f(m[pb][r] - M) / L;
+          lse2[pb][r] = M + __log2f(L);
+        }
+    }
+
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t p = p0 + 16 * pb + 4 * j + r;
+        const float fr = p < pend ? f[pb][r] : 0.f;
+#pragma unroll
+        for (int gb = 0; gb < GB; ++gb) w[pb][gb][r] *= fr;
+        if (a.lse_out != nullptr && ws == 0 && i == 0 && p < pend)
+          a.lse_out[(int64_t)c.bh * a.N + p] = lse2[pb][r];
+      }
+#pragma unroll
+    for (int gb = 0; gb < GB; ++gb) {
+      float sum = 0.f;
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sum += w[pb][gb][r];
+      sacc[gb] += sum;
+    }
+    mm_points<BF, GB, VB>(U, w, cur.f);
+    cur = nxt;
+  }
+
+  // ---- combine the NP point groups and write this workgroup's partials --------------------
+#pragma unroll
+  for (int gb = 0; gb < GB; ++gb) sacc[gb] = col4_sum(sacc[gb]);
+  float* pU = a.part + ((int64_t)c.bh * a.chunks + blockIdx.x) * a.G * D;
+  float* pS = a.part2 + ((int64_t)c.bh * a.chunks + blockIdx.x) * a.G;
+  if constexpr (NP > 1) {
+    __shared__ f4 red[NP - 1][NS][GB][VB][64];
+    __shared__ float reds[NP - 1][NS][GB][16];
+    if (wp > 0) {
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb) {
+#pragma unroll
+        for (int vb = 0; vb < VB; ++vb) red[wp - 1][ws][gb][vb][lane] = U[gb][vb];
+        if (j == 0) reds[wp - 1][ws][gb][i] = sacc[gb];
+      }
+    }
+    __syncthreads();
+    if (wp == 0) {
+      for (int q = 0; q < NP - 1; ++q)
+#pragma unroll
+        for (int gb = 0; gb < GB; ++gb) {
+#pragma unroll
+          for (int vb = 0; vb < VB; ++vb) U[gb][vb] += red[q][ws][gb][vb][lane];
+          sacc[gb] += reds[q][ws][gb][i];
+        }
+    }
+  }
+  if (wp == 0) {
+#pragma unroll
+    for (int gb = 0; gb < GB; ++gb) {
+#pragma unroll
+      for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          pU[(int64_t)(c.g0 + 16 * gb + 4 * j + r) * D + 16 * vb + i] = U[gb][vb][r];
+      if (j == 0) pS[c.g0 + 16 * gb + i] = sacc[gb];
+    }
+  }
+}
+
+template <bool BF, int D, int GS, int NS, int NP, int PB>
+struct Run_k_slice {
+  static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
+    dim3 grid(cfg.chunks, BH);
+    hipLaunchKernelGGL((k_slice<BF, D, GS, NS, NP>), grid, dim3(64 * NS * NP), 0, st, a);
+    return hipGetLastError();
+  }
+};
+
+}  // namespace
+
+hipError_t run_pass_slice(const Geom& g, const PassArgs& a, hipStream_t st) {
+  return run_pass_tilings<PASS_SLICE, Run_k_slice>(g, a, st);
+}
+
+}  // namespace fs

@@ -1,0 +1,493 @@
+// HIP kernels of the fused slice -> token mix -> deslice path for gfx950 (CDNA4).
+//
+// Streaming passes over the points (the hot path):
+//   k_slice    logits -> per-point softmax over the slices -> U += w^T F, s += sum w, lse
+//   k_deslice  logits -> w = exp(a - lse) -> out = w zmix
+//   k_bwd_a    logits -> w -> dzmix += w^T dout
+//   k_bwd_b    logits -> w -> dw = dout zmix^T + F dU^T + ds -> da = w (dw - sum_g w dw)
+//              -> dx = da W_s^T / tau, dfx = w dU, and partials of dW_s, dbias, dtau
+// (paper: Sec. 2 "The Transolver layer"; App. F.1 "Kernel design"; App. F.2 "Temperature
+// gradients"; the backward is the exact derivative of the forward.)
+//
+// Design: a wavefront owns GS consecutive slots and a 32-point tile (two
+// 16-point MFMA blocks); NS = G / GS wavefronts share one point tile and exchange per-point
+// softmax statistics through LDS, so the slice weights never leave registers and no N x G
+// tensor is ever written. The logits are an MFMA contraction over the head width; the
+// token contractions are MFMAs over slots (deslice, dx, dfx) or over points (slice, dzmix,
+// dW_s). fp32 storage uses v_mfma_f32_16x16x4_f32; bf16 storage uses
+// v_mfma_f32_16x16x32_bf16 with the slice projection split into a high and a low bf16 part
+// so the logits keep about 16 mantissa bits. The softmax works in base 2: each workgroup
+// folds log2(e)/tau_h into W_s and the bias as it loads them.
+//
+// MFMA lane layouts used throughout (lane = 16 * j + i, 0 <= i < 16, 0 <= j < 4):
+//   A operand A[m][k]: lane supplies m = i and a k-set that depends on j only;
+//   B operand B[k][n]: lane supplies n = i and the same k-set;
+//   C/D tile C[m][n]: lane holds rows m = 4 j + r (r = 0..3) of column n = i.
+// The k-set is the same function of j for A and B, so any consistent assignment of the
+// contraction index to (j, register) is a valid product; the code picks assignments that
+// make global loads contiguous per lane.
+//
+// This header holds what the four passes share (one translation unit per pass includes it):
+// MFMA wrappers and operand layouts, cross-lane reductions, the per-(sample, head) context,
+// and the dispatch over the compile-time tilings.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include "fs_internal.h"
+
+namespace fs {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kMasked = 1.0e30f;  // base-2 lse of padding points: exp2(a - kMasked) == 0
+
+__device__ __forceinline__ f4 mfma_f32(float a, float b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f4 mfma_bf16(bf8 a, bf8 b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float bf_to_f(unsigned short h) {
+  return __uint_as_float(((unsigned)h) << 16);
+}
+__device__ __forceinline__ unsigned short f_to_bf(float f) {
+  return __builtin_bit_cast(unsigned short, (__bf16)f);  // round to nearest even
+}
+__device__ __forceinline__ f4 zero4() { return f4{0.f, 0.f, 0.f, 0.f}; }
+__device__ __forceinline__ f4 splat4(float v) { return f4{v, v, v, v}; }
+
+// Cross-lane reductions over the 16 lanes of a row (DPP: xor 1, xor 2, half-mirror, mirror).
+// Every lane of the row ends with the same bitwise result (each step adds commuted pairs).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));
+  v = fmaxf(v, dpp<0x4E>(v));
+  v = fmaxf(v, dpp<0x141>(v));
+  v = fmaxf(v, dpp<0x140>(v));
+  return v;
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v = v + dpp<0xB1>(v);
+  v = v + dpp<0x4E>(v);
+  v = v + dpp<0x141>(v);
+  v = v + dpp<0x140>(v);
+  return v;
+}
+// Sum over the four 16-lane rows (lanes i, i+16, i+32, i+48): identical result in all four.
+__device__ __forceinline__ float col4_sum(float v) {
+  v = v + __shfl_xor(v, 16);
+  v = v + __shfl_xor(v, 32);
+  return v;
+}
+
+// Orders LDS traffic between lanes of one wavefront (no s_barrier needed within a wave).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+template <bool BF>
+struct Store;
+template <>
+struct Store<false> {
+  using T = float;
+};
+template <>
+struct Store<true> {
+  using T = unsigned short;
+};
+
+template <bool BF>
+__device__ __forceinline__ float ld1(const typename Store<BF>::T* p) {
+  if constexpr (BF)
+    return bf_to_f(*p);
+  else
+    return *p;
+}
+
+// ---------------------------------------------------------------------------------------
+// Row operand of a 16-point block: lane (j, i) holds a contiguous segment of the row of
+// point i. fp32: K = D/4 values, MFMA step kk uses column j*K + kk. bf16: one bf8 per K=32
+// step; step kk holds columns kbase(j, kk) .. +7 (D = 16 pads rows j >= 2 with zeros).
+// ---------------------------------------------------------------------------------------
+template <bool BF, int D>
+struct RowOp;
+template <int D>
+struct RowOp<false, D> {
+  static constexpr int K = D / 4;
+  float v[K];
+};
+template <int D>
+struct RowOp<true, D> {
+  static constexpr int K = (D + 31) / 32;
+  bf8 v[K];
+};
+
+template <int D>
+__device__ __forceinline__ int kbase_bf(int j, int kk) {
+  return D == 64 ? 16 * j + 8 * kk : 8 * j;
+}
+// Column of K-slot (j, kk, e) of a bf16 row operand; -1 if it is padding.
+template <int D>
+__device__ __forceinline__ int kcol_bf(int j, int kk, int e) {
+  if (D == 16 && j >= 2) return -1;
+  return kbase_bf<D>(j, kk) + e;
+}
+// Column of K-slot (j, kk) of an fp32 row operand.
+template <int D>
+__device__ __forceinline__ int kcol_f(int j, int kk) {
+  return j * (D / 4) + kk;
+}
+
+template <bool BF, int D>
+__device__ __forceinline__ void load_row(RowOp<BF, D>& o, const typename Store<BF>::T* row,
+                                         bool valid, int j) {
+  if constexpr (!BF) {
+    constexpr int K = D / 4;
+    if (valid) {
+      const float4* src = reinterpret_cast<const float4*>(row + j * K);
+#pragma unroll
+      for (int q = 0; q < K / 4; ++q) {
+        float4 t = src[q];
+        o.v[4 * q + 0] = t.x;
+        o.v[4 * q + 1] = t.y;
+        o.v[4 * q + 2] = t.z;
+        o.v[4 * q + 3] = t.w;
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < K; ++q) o.v[q] = 0.f;
+    }
+  } else {
+    constexpr int K = (D + 31) / 32;
+#pragma unroll
+    for (int kk = 0; kk < K; ++kk) {
+      if (valid && !(D == 16 && j >= 2)) {
+        uint4 t = *reinterpret_cast<const uint4*>(row + kbase_bf<D>(j, kk));
+        o.v[kk] = __builtin_bit_cast(bf8, t);
+      } else {
+        o.v[kk] = __builtin_bit_cast(bf8, uint4{0u, 0u, 0u, 0u});
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+// Slot-range operand of a [rows = slots][cols = k] matrix for a contraction over k with the
+// slot on the MFMA M (or N) index: lane (j, i) holds M(g0 + 16 gb + i, kcol(j, kk)).
+// Used for the scaled slice projection (M(g, d) = W_s[d][g] * sc, W stored (D, G)) and for
+// zmix / dU in dw (M(g, v) = Z[g][v], stored (G, V)). bf16 keeps a high and a low part.
+// ---------------------------------------------------------------------------------------
+template <bool BF, int D, int GB>
+struct SlotOp;
+template <int D, int GB>
+struct SlotOp<false, D, GB> {
+  float v[GB][D / 4];
+};
+template <int D, int GB>
+struct SlotOp<true, D, GB> {
+  static constexpr int K = (D + 31) / 32;
+  bf8 hi[GB][K];
+  bf8 lo[GB][K];
+};
+
+// TRANSPOSED = true: element (g, k) read from src[k * ld + g] (W_s (D,G)); else
+// src[g * ld + k] - cen[k] (cen nullable: a per-column shift removed before rounding).
+template <bool BF, int D, int GB, bool TRANSPOSED, bool SPLIT>
+__device__ __forceinline__ void load_slotop(SlotOp<BF, D, GB>& o, const float* src, int ld,
+                                            int g0, float sc, int i, int j,
+                                            const float* cen = nullptr) {
+  auto M = [&](int g, int k) -> float {
+    if (TRANSPOSED) return sc * src[(int64_t)k * ld + g];
+    return sc * (src[(int64_t)g * ld + k] - (cen != nullptr ? cen[k] : 0.f));
+  };
+#pragma unroll
+  for (int gb = 0; gb < GB; ++gb) {
+    const int g = g0 + 16 * gb + i;
+    if constexpr (!BF) {
+#pragma unroll
+      for (int kk = 0; kk < D / 4; ++kk) o.v[gb][kk] = M(g, kcol_f<D>(j, kk));
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < SlotOp<true, D, GB>::K; ++kk) {
+        bf8 hi, lo;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int k = kcol_bf<D>(j, kk, e);
+          float val = 0.f;
+          if (k >= 0) val = M(g, k);
+          const __bf16 h = (__bf16)val;
+          hi[e] = h;
+          lo[e] = SPLIT ? (__bf16)(val - (float)h) : (__bf16)0.f;
+        }
+        o.hi[gb][kk] = hi;
+        o.lo[gb][kk] = lo;
+      }
+    }
+  }
+}
+
+// acc += (slot operand) x (row operand)^T : T-layout tile (rows = slots, cols = points).
+template <bool BF, int D, int GB, bool SPLIT>
+__device__ __forceinline__ f4 mm_slot_row(const SlotOp<BF, D, GB>& s, int gb,
+                                          const RowOp<BF, D>& r, f4 acc) {
+  if constexpr (!BF) {
+#pragma unroll
+    for (int kk = 0; kk < D / 4; ++kk) acc = mfma_f32(s.v[gb][kk], r.v[kk], acc);
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < RowOp<true, D>::K; ++kk) {
+      acc = mfma_bf16(s.hi[gb][kk], r.v[kk], acc);
+      if constexpr (SPLIT) acc = mfma_bf16(s.lo[gb][kk], r.v[kk], acc);
+    }
+  }
+  return acc;
+}
+// acc += (row operand) x (slot operand)^T : S-layout tile (rows = points, cols = slots).
+template <bool BF, int D, int GB, bool SPLIT>
+__device__ __forceinline__ f4 mm_row_slot(const RowOp<BF, D>& r, const SlotOp<BF, D, GB>& s,
+                                          int gb, f4 acc) {
+  if constexpr (!BF) {
+#pragma unroll
+    for (int kk = 0; kk < D / 4; ++kk) acc = mfma_f32(r.v[kk], s.v[gb][kk], acc);
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < RowOp<true, D>::K; ++kk) {
+      acc = mfma_bf16(r.v[kk], s.hi[gb][kk], acc);
+      if constexpr (SPLIT) acc = mfma_bf16(r.v[kk], s.lo[gb][kk], acc);
+    }
+  }
+  return acc;
+}
+
+// ---------------------------------------------------------------------------------------
+// Operand for a contraction over slots whose output rows are columns c of a slot-major
+// matrix M(g, c): lane (j, i) supplies M(g, 16 cb + i) for g in its k-set.
+//   fp32: k-set of (gb, r) is g0 + 16 gb + 4 j + r (one MFMA per (gb, r)).
+//   bf16: k-set of pair q, element e: g0 + 32 q + 16 (e / 4) + 4 j + (e % 4).
+// These k-sets coincide with the rows a T-layout tile holds, so the tile is the B operand.
+// ---------------------------------------------------------------------------------------
+template <bool BF, int GB, int CB>
+struct GOp;
+template <int GB, int CB>
+struct GOp<false, GB, CB> {
+  float v[GB][4][CB];
+};
+template <int GB, int CB>
+struct GOp<true, GB, CB> {
+  bf8 v[GB / 2][CB];
+};
+
+// TRANSPOSED = true: M(g, c) = src[c * ld + g] * sc, else src[g * ld + c] * sc.
+template <bool BF, int GB, int CB, bool TRANSPOSED>
+__device__ __forceinline__ void load_gop(GOp<BF, GB, CB>& o, const float* src, int ld, int g0,
+                                         float sc, int i, int j) {
+  auto M = [&](int g, int c) -> float {
+    return sc * (TRANSPOSED ? src[(int64_t)c * ld + g] : src[(int64_t)g * ld + c]);
+  };
+  if constexpr (!BF) {
+#pragma unroll
+    for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) o.v[gb][r][cb] = M(g0 + 16 * gb + 4 * j + r, 16 * cb + i);
+  } else {
+#pragma unroll
+    for (int q = 0; q < GB / 2; ++q)
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        bf8 t;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          t[e] = (__bf16)M(g0 + 32 * q + 16 * (e / 4) + 4 * j + (e % 4), 16 * cb + i);
+        o.v[q][cb] = t;
+      }
+  }
+}
+
+// out[cb] (+)= M^T-contraction with a T-layout tile column block pb: rows c, cols points.
+template <bool BF, int GB, int CB, int PB = 2>
+__device__ __forceinline__ f4 mm_gop_tile(const GOp<BF, GB, CB>& o, int cb, const f4 (*t)[PB],
+                                          int pb, f4 acc) {
+  if constexpr (!BF) {
+#pragma unroll
+    for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc = mfma_f32(o.v[gb][r][cb], t[gb][pb][r], acc);
+  } else {
+#pragma unroll
+    for (int q = 0; q < GB / 2; ++q) {
+      bf8 bt;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) bt[e] = (__bf16)t[2 * q + e / 4][pb][e % 4];
+      acc = mfma_bf16(o.v[q][cb], bt, acc);
+    }
+  }
+  return acc;
+}
+
+// Operand rows of a point-major matrix P (row stride rs) for a contraction over the 32 points
+// of a tile: lane (j, i) holds P(p, 16 cb + i) for the points of its k-set.
+//   fp32: point 16 pb + 4 j + r for MFMA (pb, r);  bf16: point 16 (e / 4) + 4 j + (e % 4).
+// Gathered separately from the MFMAs so that the next tile's loads can be issued early.
+template <bool BF, int CB>
+struct PtGather;
+template <int CB>
+struct PtGather<false, CB> {
+  float v[2][4][CB];
+};
+template <int CB>
+struct PtGather<true, CB> {
+  bf8 v[CB];
+};
+
+template <bool BF, int CB>
+__device__ __forceinline__ void gather_points(PtGather<BF, CB>& g,
+                                              const typename Store<BF>::T* base, int64_t rs,
+                                              int64_t p0, int64_t pend, int i, int j) {
+  if constexpr (!BF) {
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t p = p0 + 16 * pb + 4 * j + r;
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) g.v[pb][r][cb] = p < pend ? base[p * rs + 16 * cb + i] : 0.f;
+      }
+  } else {
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      bf8 bt;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int64_t p = p0 + 16 * (e / 4) + 4 * j + (e % 4);
+        unsigned short h = 0;
+        if (p < pend) h = base[p * rs + 16 * cb + i];
+        bt[e] = __builtin_bit_cast(__bf16, h);
+      }
+      g.v[cb] = bt;
+    }
+  }
+}
+
+// acc[gb][cb] += (S-layout tile column gb)^T-contraction over the 32 points with the gathered
+// rows: out(g, c) += sum_p w(p, g) P(p, 16 cb + i).
+template <bool BF, int GB, int CB>
+__device__ __forceinline__ void mm_points(f4 (*acc)[CB], const f4 (*w)[GB],
+                                          const PtGather<BF, CB>& g) {
+  if constexpr (!BF) {
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+          for (int gb = 0; gb < GB; ++gb) acc[gb][cb] = mfma_f32(w[pb][gb][r], g.v[pb][r][cb], acc[gb][cb]);
+  } else {
+    bf8 at[GB];
+#pragma unroll
+    for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) at[gb][e] = (__bf16)w[e / 4][gb][e % 4];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb)
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb) acc[gb][cb] = mfma_bf16(at[gb], g.v[cb], acc[gb][cb]);
+  }
+}
+
+// Register image of a per-wavefront operand in LDS: 16-byte chunk q of lane l at
+// base[q * 64 + l], so every lane reads its own chunk and no two lanes share a bank group.
+template <class Op>
+__device__ __forceinline__ void lds_put(const Op& o, uint4* base, int lane) {
+  static_assert(sizeof(Op) % 16 == 0, "operand image must be whole 16-byte chunks");
+  const uint4* src = reinterpret_cast<const uint4*>(&o);
+#pragma unroll
+  for (int q = 0; q < (int)(sizeof(Op) / 16); ++q) base[q * 64 + lane] = src[q];
+}
+template <class Op>
+__device__ __forceinline__ void lds_get(Op& o, const uint4* base, int lane) {
+  uint4* dst = reinterpret_cast<uint4*>(&o);
+#pragma unroll
+  for (int q = 0; q < (int)(sizeof(Op) / 16); ++q) dst[q] = base[q * 64 + lane];
+}
+template <class Op>
+constexpr int lds_chunks() {
+  return (int)(sizeof(Op) / 16) * 64;
+}
+
+struct HeadCtx {
+  int bh, b, h, g0;
+  float sc;  // log2(e) / tau_h
+  const float* W;
+  const float* bias;
+  int64_t off;  // element offset of point 0 of this (b, h) in the (B, N, H, D) layout
+};
+
+template <int D>
+__device__ __forceinline__ HeadCtx head_ctx(const PassArgs& a, int ws, int GS) {
+  HeadCtx c;
+  c.bh = blockIdx.y;
+  c.b = c.bh / a.H;
+  c.h = c.bh % a.H;
+  c.g0 = ws * GS;
+  c.sc = kLog2e / a.tau[c.h];
+  c.W = a.Ws + (a.ws_per_head ? (int64_t)c.h * D * a.G : 0);
+  c.bias = a.bias + (a.ws_per_head ? (int64_t)c.h * a.G : 0);
+  c.off = ((int64_t)c.b * a.N * a.H + c.h) * D;
+  return c;
+}
+
+// =======================================================================================
+// Dispatch over the compile-time tiling
+// =======================================================================================
+// Supported (GS, NS, NP, PB) tilings; pick_cfg in fs_api.cpp chooses among exactly these.
+// PB = 1 (16-point tiles) exists for the fp32 backward pass B only.
+#define FS_TILINGS(X, BF, D)                                                              \
+  X(BF, D, 16, 1, 4, 2) X(BF, D, 32, 1, 4, 2) X(BF, D, 64, 1, 4, 2) X(BF, D, 64, 2, 2, 2) \
+  X(BF, D, 64, 4, 1, 2) X(BF, D, 64, 8, 1, 2) X(BF, D, 64, 16, 1, 2)                     \
+  X(BF, D, 16, 1, 4, 1) X(BF, D, 32, 1, 4, 1) X(BF, D, 64, 1, 4, 1)
+
+// Runner<BF, D, GS, NS, NP, PB>::run launches one pass's kernel for one tiling.
+template <int PASS, template <bool, int, int, int, int, int> class Runner, bool BF, int D>
+hipError_t run_tiled(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
+#define FS_CASE(BF_, D_, GS_, NS_, NP_, PB_)                                             \
+  if (cfg.GS == GS_ && cfg.NS == NS_ && cfg.NP == NP_ && cfg.PB == PB_) {                \
+    if constexpr (!(BF_ && GS_ < 32) && (PB_ == 2 || (!BF_ && PASS == PASS_BWD_B)))      \
+      return Runner<BF_, D_, GS_, NS_, NP_, PB_>::run(cfg, BH, a, st);                   \
+  }
+  FS_TILINGS(FS_CASE, BF, D)
+#undef FS_CASE
+  return hipErrorInvalidConfiguration;
+}
+
+template <int PASS, template <bool, int, int, int, int, int> class Runner>
+hipError_t run_pass_tilings(const Geom& g, const PassArgs& a, hipStream_t st) {
+  const PassCfg cfg = pick_cfg(g, (Pass)PASS);
+  const int BH = g.BH();
+  if (g.bf16) {
+    if (g.D == 16) return run_tiled<PASS, Runner, true, 16>(cfg, BH, a, st);
+    if (g.D == 32) return run_tiled<PASS, Runner, true, 32>(cfg, BH, a, st);
+    if (g.D == 64) return run_tiled<PASS, Runner, true, 64>(cfg, BH, a, st);
+  } else {
+    if (g.D == 16) return run_tiled<PASS, Runner, false, 16>(cfg, BH, a, st);
+    if (g.D == 32) return run_tiled<PASS, Runner, false, 32>(cfg, BH, a, st);
+    if (g.D == 64) return run_tiled<PASS, Runner, false, 64>(cfg, BH, a, st);
+  }
+  return hipErrorInvalidConfiguration;
+}
+
+}  // namespace
+}  // namespace fs

@@ -6,6 +6,8 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "fs_internal.h"
 
 namespace fs {
@@ -131,20 +133,52 @@ __global__ __launch_bounds__(kRedThreads) void k_reduce_rows(const float* part, 
   if (rg == 0 && c < len) out[(int64_t)bh * len + c] = tot;
 }
 
+// Mix-parameter gradient from per-(b, h) partials [BH][len]: summed over (b, h), or over b
+// per head (per_head); column block cb of output head hh.
+__device__ __forceinline__ void reduce_mixparams_block(const float* partM, float* dmix, int B,
+                                                       int H, int64_t len, int per_head, int cb,
+                                                       int hh, float (*red)[kColsWide]) {
+  const int cg = threadIdx.x % kColsWide, rg = threadIdx.x / kColsWide;
+  const int64_t c = (int64_t)cb * kColsWide + cg;
+  RowMap m;
+  if (per_head)
+    m = RowMap{hh, B, 1, H};
+  else
+    m = RowMap{0, B * H, B * H, 0};
+  const float v = c < len ? colsum<kRowGroupsWide>(partM, len, m, c, rg) : 0.f;
+  const float tot = combine_groups<kRowGroupsWide, kColsWide>(v, red, rg, cg);
+  if (rg == 0 && c < len) dmix[(per_head ? (int64_t)hh * len : 0) + c] = tot;
+}
+
+__global__ __launch_bounds__(kRedThreads) void k_reduce_mixparams(const float* partM, float* dmix,
+                                                               int B, int H, int64_t len,
+                                                               int per_head) {
+  __shared__ float red[kRowGroupsWide][kColsWide];
+  reduce_mixparams_block(partM, dmix, B, H, len, per_head, blockIdx.x, blockIdx.y, red);
+}
+
 // Parameter gradients from the backward-pass-B partials [BH][chunks][D G + G + 2] (the last
-// two floats of each partial hold one fp64 dtau partial).
-// grid (ceil((D G + G) / 64) + 1, heads_out): blockIdx.y is the head for per-head W_s and
-// bias (rows: b = 0..B-1, chunk), or 0 with rows over every (b, h, chunk) when shared.
-// The extra last column block sums dtau for every head in fp64.
-__global__ __launch_bounds__(kRedThreads) void k_reduce_params(const float* part, float* dWs,
-                                                            float* dbias, float* dtau, int B,
-                                                            int H, int chunks, int D, int G,
-                                                            int per_head) {
+// two floats of each partial hold one fp64 dtau partial), and optionally the mix-parameter
+// gradient from its per-(b, h) partials, in one launch.
+// grid.x = [column blocks of dW_s and dbias] [one dtau block] [column blocks of dmix];
+// blockIdx.y is the head for per-head outputs (rows: b = 0..B-1, chunk), else 0 with rows
+// over every (b, h, chunk); blocks whose segment has fewer heads return at once.
+__global__ __launch_bounds__(kRedThreads) void k_reduce_params(
+    const float* part, float* dWs, float* dbias, float* dtau, int B, int H, int chunks, int D,
+    int G, int per_head, const float* partM, float* dmix, int64_t mix_len, int mix_per_head) {
   __shared__ float red[kRowGroupsWide][kColsWide];
   const int64_t len = (int64_t)D * G + G + 2;
   const int64_t ncol = (int64_t)D * G + G;
+  const int nbp = (int)((ncol + kColsWide - 1) / kColsWide);
   const int hh = blockIdx.y;
-  if ((int64_t)blockIdx.x * kColsWide >= ncol) {
+  if ((int)blockIdx.x > nbp) {
+    if (dmix != nullptr && (mix_per_head || hh == 0))
+      reduce_mixparams_block(partM, dmix, B, H, mix_len, mix_per_head, blockIdx.x - nbp - 1, hh,
+                             red);
+    return;
+  }
+  if (!per_head && hh > 0) return;
+  if ((int)blockIdx.x == nbp) {
     // dtau: one wavefront per head; lane l sums the fp64 partials l, l + 64, ... of the
     // head's (b, chunk) rows in order, then a butterfly over the 64 lanes (fixed pairing)
     if (hh == 0) {
@@ -178,25 +212,6 @@ __global__ __launch_bounds__(kRedThreads) void k_reduce_params(const float* part
     else
       dbias[(per_head ? (int64_t)hh * G : 0) + (c - (int64_t)D * G)] = tot;
   }
-}
-
-// Mix-parameter gradient from per-(b, h) partials [BH][len]: summed over (b, h), or over b
-// per head (per_head). grid (ceil(len / 64), per_head ? H : 1).
-__global__ __launch_bounds__(kRedThreads) void k_reduce_mixparams(const float* partM, float* dmix,
-                                                               int B, int H, int64_t len,
-                                                               int per_head) {
-  __shared__ float red[kRowGroupsWide][kColsWide];
-  const int hh = blockIdx.y;
-  const int cg = threadIdx.x % kColsWide, rg = threadIdx.x / kColsWide;
-  const int64_t c = (int64_t)blockIdx.x * kColsWide + cg;
-  RowMap m;
-  if (per_head)
-    m = RowMap{hh, B, 1, H};
-  else
-    m = RowMap{0, B * H, B * H, 0};
-  const float v = c < len ? colsum<kRowGroupsWide>(partM, len, m, c, rg) : 0.f;
-  const float tot = combine_groups<kRowGroupsWide, kColsWide>(v, red, rg, cg);
-  if (rg == 0 && c < len) dmix[(per_head ? (int64_t)hh * len : 0) + c] = tot;
 }
 
 // ---------------------------------------------------------------------------------------
@@ -720,6 +735,10 @@ __global__ __launch_bounds__(kThreads) void k_attn_bwd(
 }
 
 inline unsigned blocks(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+// Floats of one (b, h) mix-parameter partial.
+inline int64_t mix_partial_len(const Geom& g, int kind) {
+  return kind == 1 ? (int64_t)g.G * g.G : (kind == 2 ? (int64_t)g.V * g.V : 3LL * g.V * g.V);
+}
 inline bool attn_small(const Geom& g) {
   return g.G * g.V <= kAttnSmallGV && g.G <= 64 && g.V <= 64;
 }
@@ -749,19 +768,25 @@ hipError_t launch_reduce_rows(const Geom& g, const float* part, float* out, int 
 }
 
 hipError_t launch_reduce_params(const Geom& g, const float* part, float* dWs, float* dbias,
-                                float* dtau, int chunks, hipStream_t st) {
+                                float* dtau, int chunks, const MixArgs* m, const float* partM,
+                                float* dmix, hipStream_t st) {
   const int64_t ncol = (int64_t)g.D * g.G + g.G;
-  dim3 grid(blocks(ncol, kColsWide) + 1, g.ws_per_head ? g.H : 1);
-  hipLaunchKernelGGL(k_reduce_params, grid, dim3(kRedThreads), 0, st, part, dWs, dbias, dtau,
-                     (int)g.B, g.H, chunks, g.D, g.G, g.ws_per_head ? 1 : 0);
+  const bool with_mix = m != nullptr && dmix != nullptr && m->kind != 0;
+  const int64_t mix_len = with_mix ? mix_partial_len(g, m->kind) : 0;
+  const bool mix_per_head = with_mix && m->kind == 1 && m->a_per_head;
+  const unsigned nb = blocks(ncol, kColsWide) + 1 + (with_mix ? blocks(mix_len, kColsWide) : 0);
+  const int heads = std::max(g.ws_per_head ? g.H : 1, mix_per_head ? g.H : 1);
+  hipLaunchKernelGGL(k_reduce_params, dim3(nb, heads), dim3(kRedThreads), 0, st, part, dWs,
+                     dbias, dtau, (int)g.B, g.H, chunks, g.D, g.G, g.ws_per_head ? 1 : 0, partM,
+                     with_mix ? dmix : nullptr, mix_len, mix_per_head ? 1 : 0);
   return hipGetLastError();
 }
 
 hipError_t launch_mix(const Geom& g, const MixArgs& m, const float* z, float* zmix,
                       float* attn, hipStream_t st) {
   const int BH = g.BH();
+  if (tok_fused(g, m.kind)) return launch_tok_fwd(g, m, z, zmix, attn, st);
   if (m.kind == 3) {
-    const int GV = g.G * g.V, VV = g.V * g.V;
     if (attn_small(g)) {
       const size_t lds = sizeof(float) * (size_t)attn_small_fwd_floats(g.G, g.V);
       hipError_t e = allow_lds(k_attn_fwd_small, lds);
@@ -783,11 +808,13 @@ hipError_t launch_mix(const Geom& g, const MixArgs& m, const float* z, float* zm
 hipError_t launch_mix_bwd(const Geom& g, const MixArgs& m, const float* z, const float* s,
                           const float* zmix, const float* attn, const float* dzm, float* dz,
                           float* dU, float* ds, float* cen, float* scr, float* partM,
-                          float* dmix, hipStream_t st) {
+                          float* dmix, bool reduce_params, hipStream_t st) {
   const int BH = g.BH();
-  if (m.kind == 3) {
+  hipError_t e;
+  if (tok_fused(g, m.kind)) {
+    e = launch_tok_bwd(g, m, z, s, zmix, attn, dzm, dz, dU, ds, cen, partM, st);
+  } else if (m.kind == 3) {
     if (attn_small(g)) {
-      const int GV = g.G * g.V, VV = g.V * g.V;
       const size_t lds = sizeof(float) * (size_t)attn_small_bwd_floats(g.G, g.V);
       hipError_t e = allow_lds(k_attn_bwd_small, lds);
       if (e != hipSuccess) return e;
@@ -811,11 +838,10 @@ hipError_t launch_mix_bwd(const Geom& g, const MixArgs& m, const float* z, const
       hipLaunchKernelGGL(k_token_grads, dim3(BH), dim3(kThreads), 0, st, z, s, zmix, dz, dU, ds,
                          cen, g.G, g.V, g.eps);
   }
-  hipError_t e = hipGetLastError();
+  if (!tok_fused(g, m.kind)) e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (dmix != nullptr && m.kind != 0) {
-    const int64_t len =
-        m.kind == 1 ? (int64_t)g.G * g.G : (m.kind == 2 ? (int64_t)g.V * g.V : 3LL * g.V * g.V);
+  if (reduce_params && dmix != nullptr && m.kind != 0) {
+    const int64_t len = mix_partial_len(g, m.kind);
     const bool per_head = m.kind == 1 && m.a_per_head;
     dim3 grid(blocks(len, kColsWide), per_head ? g.H : 1);
     hipLaunchKernelGGL(k_reduce_mixparams, grid, dim3(kRedThreads), 0, st, partM, dmix, (int)g.B,
