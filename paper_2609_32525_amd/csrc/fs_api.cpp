@@ -58,6 +58,10 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
   // passes that write partials give every chunk at least 4 tiles per point group, so the
   // partials stay small next to the points they summarise
   chunks = std::min<int64_t>(chunks, partials ? std::max<int64_t>(1, ntiles / 4) : ntiles);
+  // the kernels address a chunk's rows with 32-bit byte offsets (raw buffer loads)
+  const int64_t row_bytes = (int64_t)g.H * g.D * (g.bf16 ? 2 : 4);
+  const int64_t max_tiles = std::max<int64_t>(1, (((int64_t)1 << 31) - 1) / (row_bytes * step) - 1);
+  chunks = std::max<int64_t>(chunks, (ntiles + max_tiles - 1) / max_tiles);
   int64_t tiles_per_chunk = (ntiles + chunks - 1) / chunks;
   c.chunk_pts = tiles_per_chunk * step;
   c.chunks = (int)std::max<int64_t>(1, (g.N + c.chunk_pts - 1) / c.chunk_pts);

@@ -35,33 +35,33 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_a(PassArgs a) {
 
   const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
-  const int ntile = pend > pbeg ? (int)((pend - pbeg + 32 * NP - 1) / (32 * NP)) : 0;
+  const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
+  const int ntile = (npts + 32 * NP - 1) / (32 * NP);
+  const int rsb = (int)(rs * sizeof(T));
+  const auto rx = rows_rsrc(xb + pbeg * rs, npts, (int)rs, D);
+  const auto rg = rows_rsrc(db + pbeg * rs, npts, (int)rs, D);
+  const auto rl = rows_rsrc(lse + pbeg, npts, 1, 1);
+  const int wpu = __builtin_amdgcn_readfirstlane(wp);
 
-  // software pipeline: the next tile's rows are loaded before the current tile is computed
   struct Tile {
     RowOp<BF, D> xo[2];
     float lse2[2][4];
     PtGather<BF, VB> g;
   };
   auto load_tile = [&](Tile& tt, int t) {
-    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+    const int tb = (t * NP + wpu) * 32;
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) {
-      const int64_t p = p0 + 16 * pb + i;
-      load_row<BF, D>(tt.xo[pb], xb + p * rs, p < pend, j);
+      load_row_buf<BF, D>(tt.xo[pb], rx, i * rsb, (tb + 16 * pb) * rsb, j);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t q = p0 + 16 * pb + 4 * j + r;
-        tt.lse2[pb][r] = q < pend ? lse[q] : kMasked;
+        const float l = bld32(rl, 4 * (4 * j + r), 4 * (tb + 16 * pb));
+        tt.lse2[pb][r] = tb + 16 * pb + 4 * j + r < npts ? l : kMasked;
       }
     }
-    gather_points<BF, VB>(tt.g, db, rs, p0, pend, i, j);
+    gather_points_buf<BF, VB>(tt.g, rg, rsb, tb * rsb, i, j);
   };
-  Tile cur;
-  if (ntile > 0) load_tile(cur, 0);
-  for (int t = 0; t < ntile; ++t) {
-    Tile nxt;
-    if (t + 1 < ntile) load_tile(nxt, t + 1);
+  pipeline<FS_PF_BWD_A, Tile>(ntile, load_tile, [&](Tile& cur, int t) {
     const RowOp<BF, D>* xo = cur.xo;
     const float(*lse2)[4] = cur.lse2;
     f4 w[2][GB];
@@ -75,8 +75,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_a(PassArgs a) {
         w[pb][gb] = acc;
       }
     mm_points<BF, GB, VB>(Z, w, cur.g);
-    cur = nxt;
-  }
+  });
 
   float* pZ = a.part + ((int64_t)c.bh * a.chunks + blockIdx.x) * a.G * D;
   if constexpr (NP > 1) {

@@ -123,21 +123,39 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
 
   const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
-  const int ntile = pend > pbeg ? (int)((pend - pbeg + TP * NP - 1) / (TP * NP)) : 0;
+  const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
+  const int ntile = (npts + TP * NP - 1) / (TP * NP);
+  const int rsb = (int)(rs * sizeof(T));
+  const auto rx = rows_rsrc(xb + pbeg * rs, npts, (int)rs, D);
+  const auto rf = rows_rsrc(fb + pbeg * rs, npts, (int)rs, D);
+  const auto rg = rows_rsrc(gb_ + pbeg * rs, npts, (int)rs, D);
+  const auto rdx = rows_rsrc(dxb + pbeg * rs, npts, (int)rs, D);
+  const auto rdf = rows_rsrc(dfb + pbeg * rs, npts, (int)rs, D);
+  const auto rl = rows_rsrc(lse + pbeg, npts, 1, 1);
+  const int wpu = __builtin_amdgcn_readfirstlane(wp);
 
-  for (int t = 0; t < ntile; ++t) {
-    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * TP;
+  struct Tile {
     RowOp<BF, D> xo[PB], go[PB], fo[PB];
     float lse2[PB];
+  };
+  auto load_tile = [&](Tile& tt, int t) {
+    const int tb = (t * NP + wpu) * TP;
 #pragma unroll
     for (int pb = 0; pb < PB; ++pb) {
-      const int64_t p = p0 + 16 * pb + i;
-      const bool ok = p < pend;
-      load_row<BF, D>(xo[pb], xb + p * rs, ok, j);
-      load_row<BF, D>(go[pb], gb_ + p * rs, ok, j);
-      load_row<BF, D>(fo[pb], fb + p * rs, ok, j);
-      lse2[pb] = ok ? lse[p] : kMasked;
+      const int so = (tb + 16 * pb) * rsb;
+      load_row_buf<BF, D>(tt.xo[pb], rx, i * rsb, so, j);
+      load_row_buf<BF, D>(tt.go[pb], rg, i * rsb, so, j);
+      load_row_buf<BF, D>(tt.fo[pb], rf, i * rsb, so, j);
+      const float l = bld32(rl, 4 * i, 4 * (tb + 16 * pb));
+      tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
     }
+  };
+  pipeline<FS_PF_BWD_B, Tile>(ntile, load_tile, [&](Tile& cur, int t) {
+    const int tp0 = (t * NP + wpu) * TP;
+    const RowOp<BF, D>(&xo)[PB] = cur.xo;
+    const RowOp<BF, D>(&go)[PB] = cur.go;
+    const RowOp<BF, D>(&fo)[PB] = cur.fo;
+    const float(&lse2)[PB] = cur.lse2;
     // T-layout tiles: rows = slots g0 + 16 gb + 4 j + r, cols = points 16 pb + i
     f4 tl[GB][PB], w[GB][PB], dw[GB][PB];
     {
@@ -266,29 +284,13 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
     }
     if (ws == 0) {
 #pragma unroll
-      for (int pb = 0; pb < PB; ++pb) {
-        const int64_t p = p0 + 16 * pb + i;
-        if (p < pend) {
+      for (int pb = 0; pb < PB; ++pb)
 #pragma unroll
-          for (int cb = 0; cb < VB; ++cb) {
-            T* d1 = dfb + p * rs + 16 * cb + 4 * j;
-            T* d2 = dxb + p * rs + 16 * cb + 4 * j;
-            if constexpr (!BF) {
-              *reinterpret_cast<float4*>(d1) =
-                  float4{gf[cb][pb][0], gf[cb][pb][1], gf[cb][pb][2], gf[cb][pb][3]};
-              *reinterpret_cast<float4*>(d2) =
-                  float4{gx_[cb][pb][0], gx_[cb][pb][1], gx_[cb][pb][2], gx_[cb][pb][3]};
-            } else {
-              *reinterpret_cast<uint2*>(d1) =
-                  uint2{f_to_bf(gf[cb][pb][0]) | ((unsigned)f_to_bf(gf[cb][pb][1]) << 16),
-                        f_to_bf(gf[cb][pb][2]) | ((unsigned)f_to_bf(gf[cb][pb][3]) << 16)};
-              *reinterpret_cast<uint2*>(d2) =
-                  uint2{f_to_bf(gx_[cb][pb][0]) | ((unsigned)f_to_bf(gx_[cb][pb][1]) << 16),
-                        f_to_bf(gx_[cb][pb][2]) | ((unsigned)f_to_bf(gx_[cb][pb][3]) << 16)};
-            }
-          }
+        for (int cb = 0; cb < VB; ++cb) {
+          const int vo = i * rsb + (16 * cb + 4 * j) * (int)sizeof(T), so = (tp0 + 16 * pb) * rsb;
+          bst_row4<BF>(rdf, gf[cb][pb], vo, so);
+          bst_row4<BF>(rdx, gx_[cb][pb], vo, so);
         }
-      }
     }
     // dW_s += X^T da over the tile's points: da goes through LDS to put points on the k index.
     if constexpr (!BF) {
@@ -305,10 +307,9 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int pl = 16 * pb + 4 * j + r;
-          const int64_t p = p0 + pl;
           float xv[DB];
 #pragma unroll
-          for (int d = 0; d < DB; ++d) xv[d] = p < pend ? xb[p * rs + 16 * d + i] : 0.f;
+          for (int d = 0; d < DB; ++d) xv[d] = bld32(rx, 4 * j * rsb + (16 * d + i) * 4, (tp0 + 16 * pb + r) * rsb);
 #pragma unroll
           for (int gb = 0; gb < GB; ++gb) {
             const float bv = myda[pl * (GS + 1) + 16 * gb + i];
@@ -331,9 +332,8 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
       for (int d = 0; d < DB; ++d)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const int64_t p = p0 + 16 * (e / 4) + 4 * j + (e % 4);
-          unsigned short h = 0;
-          if (p < pend) h = xb[p * rs + 16 * d + i];
+          const unsigned short h =
+              bld16(rx, 4 * j * rsb + (16 * d + i) * 2, (tp0 + 16 * (e / 4) + (e % 4)) * rsb);
           xa[d][e] = __builtin_bit_cast(__bf16, h);
         }
 #pragma unroll
@@ -346,7 +346,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
       }
       wave_lds_sync();
     }
-  }
+  });
 
   // ---- finish: reduce over lanes / waves and write the partial ---------------------------
   float dbv[GB][4];

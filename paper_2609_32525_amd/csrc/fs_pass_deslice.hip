@@ -36,28 +36,29 @@ __global__ __launch_bounds__(64 * NS * NP) void k_deslice(PassArgs a) {
 
   const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
-  const int ntile = pend > pbeg ? (int)((pend - pbeg + 32 * NP - 1) / (32 * NP)) : 0;
+  const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
+  const int ntile = (npts + 32 * NP - 1) / (32 * NP);
+  const int rsb = (int)(rs * sizeof(T));
+  const auto rx = rows_rsrc(xb + pbeg * rs, npts, (int)rs, D);
+  const auto ro = rows_rsrc(ob + pbeg * rs, npts, (int)rs, D);
+  const auto rl = rows_rsrc(lse + pbeg, npts, 1, 1);
+  const int wpu = __builtin_amdgcn_readfirstlane(wp);
 
-  // software pipeline: the next tile's rows are loaded before the current tile is computed
   struct Tile {
     RowOp<BF, D> xo[2];
     float lse2[2];
   };
   auto load_tile = [&](Tile& tt, int t) {
-    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+    const int tb = (t * NP + wpu) * 32;
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) {
-      const int64_t p = p0 + 16 * pb + i;
-      load_row<BF, D>(tt.xo[pb], xb + p * rs, p < pend, j);
-      tt.lse2[pb] = p < pend ? lse[p] : kMasked;
+      load_row_buf<BF, D>(tt.xo[pb], rx, i * rsb, (tb + 16 * pb) * rsb, j);
+      const float l = bld32(rl, 4 * i, 4 * (tb + 16 * pb));
+      tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
     }
   };
-  Tile cur;
-  if (ntile > 0) load_tile(cur, 0);
-  for (int t = 0; t < ntile; ++t) {
-    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
-    Tile nxt;
-    if (t + 1 < ntile) load_tile(nxt, t + 1);
+  pipeline<FS_PF_DESLICE, Tile>(ntile, load_tile, [&](Tile& cur, int t) {
+    const int tb = (t * NP + wpu) * 32;
     const RowOp<BF, D>* xo = cur.xo;
     const float* lse2 = cur.lse2;
     f4 w[GB][2];
@@ -96,26 +97,12 @@ __global__ __launch_bounds__(64 * NS * NP) void k_deslice(PassArgs a) {
     }
     if (ws == 0) {
 #pragma unroll
-      for (int pb = 0; pb < 2; ++pb) {
-        const int64_t p = p0 + 16 * pb + i;
-        if (p < pend) {
+      for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
-          for (int vb = 0; vb < VB; ++vb) {
-            T* dst = ob + p * rs + 16 * vb + 4 * j;
-            if constexpr (!BF) {
-              *reinterpret_cast<float4*>(dst) =
-                  float4{o[vb][pb][0], o[vb][pb][1], o[vb][pb][2], o[vb][pb][3]};
-            } else {
-              const unsigned lo = f_to_bf(o[vb][pb][0]) | ((unsigned)f_to_bf(o[vb][pb][1]) << 16);
-              const unsigned hi = f_to_bf(o[vb][pb][2]) | ((unsigned)f_to_bf(o[vb][pb][3]) << 16);
-              *reinterpret_cast<uint2*>(dst) = uint2{lo, hi};
-            }
-          }
-        }
-      }
+        for (int vb = 0; vb < VB; ++vb)
+          bst_row4<BF>(ro, o[vb][pb], i * rsb + (16 * vb + 4 * j) * (int)sizeof(T), (tb + 16 * pb) * rsb);
     }
-    cur = nxt;
-  }
+  });
 }
 
 template <bool BF, int D, int GS, int NS, int NP, int PB>

@@ -41,28 +41,27 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
 
   const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
-  const int ntile = pend > pbeg ? (int)((pend - pbeg + 32 * NP - 1) / (32 * NP)) : 0;
+  const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
+  const int ntile = (npts + 32 * NP - 1) / (32 * NP);
+  const int rsb = (int)(rs * sizeof(T));
+  const auto rx = rows_rsrc(xb + pbeg * rs, npts, (int)rs, D);
+  const auto rf = rows_rsrc(fb + pbeg * rs, npts, (int)rs, D);
+  const bool want_lse = a.lse_out != nullptr;
+  const auto rl = rows_rsrc(want_lse ? a.lse_out + (int64_t)c.bh * a.N + pbeg : a.Ws, npts, 1, 1);
+  const int wpu = __builtin_amdgcn_readfirstlane(wp);
 
-  // software pipeline: the next tile's rows are loaded before the current tile is computed
   struct Tile {
     RowOp<BF, D> xo[2];
     PtGather<BF, VB> f;
   };
   auto load_tile = [&](Tile& tt, int t) {
-    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
+    const int tbo = (t * NP + wpu) * 32 * rsb;
 #pragma unroll
-    for (int pb = 0; pb < 2; ++pb) {
-      const int64_t p = p0 + 16 * pb + i;
-      load_row<BF, D>(tt.xo[pb], xb + p * rs, p < pend, j);
-    }
-    gather_points<BF, VB>(tt.f, fb, rs, p0, pend, i, j);
+    for (int pb = 0; pb < 2; ++pb) load_row_buf<BF, D>(tt.xo[pb], rx, i * rsb, tbo + 16 * pb * rsb, j);
+    gather_points_buf<BF, VB>(tt.f, rf, rsb, tbo, i, j);
   };
-  Tile cur;
-  if (ntile > 0) load_tile(cur, 0);
-  for (int t = 0; t < ntile; ++t) {
-    const int64_t p0 = pbeg + (int64_t)(t * NP + wp) * 32;
-    Tile nxt;
-    if (t + 1 < ntile) load_tile(nxt, t + 1);
+  pipeline<FS_PF_SLICE, Tile>(ntile, load_tile, [&](Tile& cur, int t) {
+    const int tb = (t * NP + wpu) * 32;
     const RowOp<BF, D>* xo = cur.xo;
     // S-layout logits: rows = points 16 pb + 4 j + r, cols = slots g0 + 16 gb + i
     f4 w[2][GB];
@@ -97,7 +96,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
       for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          f[pb][r] = 1.0f / l[pb][r];
+          f[pb][r] = __builtin_amdgcn_rcpf(l[pb][r]);
           lse2[pb][r] = m[pb][r] + __log2f(l[pb][r]);
         }
     } else {
@@ -124,7 +123,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
 #pragma unroll
           for (int s = 0; s < NS; ++s)
             L += st_l[par][wp][s][q] * __builtin_amdgcn_exp2f(st_m[par][wp][s][q] - M);
-          f[pb][r] = __builtin_amdgcn_exp2f(m[pb][r] - M) / L;
+          f[pb][r] = __builtin_amdgcn_exp2f(m[pb][r] - M) * __builtin_amdgcn_rcpf(L);
           lse2[pb][r] = M + __log2f(L);
         }
     }
@@ -133,12 +132,11 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
     for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t p = p0 + 16 * pb + 4 * j + r;
-        const float fr = p < pend ? f[pb][r] : 0.f;
+        const int q = 16 * pb + 4 * j + r;
+        const float fr = tb + q < npts ? f[pb][r] : 0.f;
 #pragma unroll
         for (int gb = 0; gb < GB; ++gb) w[pb][gb][r] *= fr;
-        if (a.lse_out != nullptr && ws == 0 && i == 0 && p < pend)
-          a.lse_out[(int64_t)c.bh * a.N + p] = lse2[pb][r];
+        if (want_lse && ws == 0 && i == 0) bst32(rl, lse2[pb][r], 4 * q, 4 * tb);
       }
 #pragma unroll
     for (int gb = 0; gb < GB; ++gb) {
@@ -150,8 +148,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
       sacc[gb] += sum;
     }
     mm_points<BF, GB, VB>(U, w, cur.f);
-    cur = nxt;
-  }
+  });
 
   // ---- combine the NP point groups and write this workgroup's partials --------------------
 #pragma unroll

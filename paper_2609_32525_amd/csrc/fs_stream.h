@@ -149,6 +149,80 @@ __device__ __forceinline__ int kcol_f(int j, int kk) {
   return j * (D / 4) + kk;
 }
 
+// ---------------------------------------------------------------------------------------
+// Raw buffer access to the point rows of one workgroup's (b, h, chunk): byte offsets are
+// 32-bit and relative to the chunk's first point; a tile's base goes in the scalar offset,
+// the lane's part in the vector offset. The record count ends at the last valid point's
+// final column of this head, so the hardware returns zero for loads past the chunk and
+// drops stores there: ragged tails need no branches or exec-mask juggling.
+// ---------------------------------------------------------------------------------------
+constexpr int kRsrcWord3 = 0x00020000;  // gfx9 raw buffer descriptor, dword data format
+
+template <class T>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rows_rsrc(const T* first_row, int npts,
+                                                            int rs, int cols) {
+  const int bytes = npts > 0 ? (int)(((int64_t)(npts - 1) * rs + cols) * (int64_t)sizeof(T)) : 0;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(first_row), (short)0, bytes, kRsrcWord3);
+}
+__device__ __forceinline__ f4 bld128(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ uint4 bld128u(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ float bld32(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+__device__ __forceinline__ unsigned short bld16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(unsigned short, __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0));
+}
+__device__ __forceinline__ void bst128(__amdgpu_buffer_rsrc_t r, f4 v, int voff, int soff) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(r, 0, 0, 0)), v), r, voff, soff, 0);
+}
+__device__ __forceinline__ void bst64(__amdgpu_buffer_rsrc_t r, uint2 v, int voff, int soff) {
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(r, 0, 0, 0)), v), r, voff, soff, 0);
+}
+__device__ __forceinline__ void bst32(__amdgpu_buffer_rsrc_t r, float v, int voff, int soff) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, voff, soff, 0);
+}
+// Four values of one row in the storage dtype, at byte offset voff + soff.
+template <bool BF>
+__device__ __forceinline__ void bst_row4(__amdgpu_buffer_rsrc_t r, f4 v, int voff, int soff) {
+  if constexpr (!BF) {
+    bst128(r, v, voff, soff);
+  } else {
+    const unsigned lo = f_to_bf(v[0]) | ((unsigned)f_to_bf(v[1]) << 16);
+    const unsigned hi = f_to_bf(v[2]) | ((unsigned)f_to_bf(v[3]) << 16);
+    bst64(r, uint2{lo, hi}, voff, soff);
+  }
+}
+
+// Row operand from a buffer: rowoff = byte offset of the lane's row (point 16 pb + i of the
+// tile, scalar part in soff). Same register layout as load_row.
+template <bool BF, int D>
+__device__ __forceinline__ void load_row_buf(RowOp<BF, D>& o, __amdgpu_buffer_rsrc_t r,
+                                             int rowoff, int soff, int j) {
+  if constexpr (!BF) {
+    constexpr int K = D / 4;
+#pragma unroll
+    for (int q = 0; q < K / 4; ++q) {
+      const f4 t = bld128(r, rowoff + (j * K + 4 * q) * 4, soff);
+      o.v[4 * q + 0] = t[0];
+      o.v[4 * q + 1] = t[1];
+      o.v[4 * q + 2] = t[2];
+      o.v[4 * q + 3] = t[3];
+    }
+  } else {
+    constexpr int K = (D + 31) / 32;
+#pragma unroll
+    for (int kk = 0; kk < K; ++kk) {
+      uint4 t = bld128u(r, rowoff + kbase_bf<D>(j, kk) * 2, soff);
+      if (D == 16 && j >= 2) t = uint4{0u, 0u, 0u, 0u};
+      o.v[kk] = __builtin_bit_cast(bf8, t);
+    }
+  }
+}
+
 template <bool BF, int D>
 __device__ __forceinline__ void load_row(RowOp<BF, D>& o, const typename Store<BF>::T* row,
                                          bool valid, int j) {
@@ -381,6 +455,34 @@ __device__ __forceinline__ void gather_points(PtGather<BF, CB>& g,
   }
 }
 
+// gather_points from a buffer: lane (j, i) reads column 16 cb + i of points
+// tb + 16 pb + 4 j + r (fp32) or tb + 16 (e / 4) + 4 j + (e % 4) (bf16); rsb = row stride in
+// bytes, tbo = tb * rsb (wave-uniform).
+template <bool BF, int CB>
+__device__ __forceinline__ void gather_points_buf(PtGather<BF, CB>& g, __amdgpu_buffer_rsrc_t r,
+                                                  int rsb, int tbo, int i, int j) {
+  if constexpr (!BF) {
+    const int lo = 4 * j * rsb + 4 * i;
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr)
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb)
+          g.v[pb][rr][cb] = bld32(r, lo + 64 * cb, tbo + (16 * pb + rr) * rsb);
+  } else {
+    const int lo = 4 * j * rsb + 2 * i;
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      bf8 bt;
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        bt[e] = __builtin_bit_cast(__bf16, bld16(r, lo + 32 * cb, tbo + (16 * (e / 4) + (e % 4)) * rsb));
+      g.v[cb] = bt;
+    }
+  }
+}
+
 // acc[gb][cb] += (S-layout tile column gb)^T-contraction over the 32 points with the gathered
 // rows: out(g, c) += sum_p w(p, g) P(p, 16 cb + i).
 template <bool BF, int GB, int CB>
@@ -427,6 +529,46 @@ template <class Op>
 constexpr int lds_chunks() {
   return (int)(sizeof(Op) / 16) * 64;
 }
+
+// ---------------------------------------------------------------------------------------
+// Software pipeline over a wavefront's point tiles: the loads of tile t + PF are issued
+// before tile t is computed, so PF tiles of global loads are in flight behind the compute.
+// The PF + 1 buffers form a ring indexed with compile-time constants (the loop over the
+// ring is unrolled), so they stay in registers. Prefetches are unconditional: load() must be
+// safe for tiles past the end (the buffer loads return zeros there). A conditional prefetch
+// would make the compiler's wait counts cover the path without it, i.e. wait for every load
+// in flight before each tile.
+// ---------------------------------------------------------------------------------------
+template <int PF, class Tile, class Load, class Body>
+__device__ __forceinline__ void pipeline(int ntile, Load&& load, Body&& body) {
+  constexpr int DEPTH = PF + 1;
+  Tile buf[DEPTH];
+#pragma unroll
+  for (int s = 0; s < PF; ++s) load(buf[s], s);
+  for (int t0 = 0; t0 < ntile; t0 += DEPTH) {
+#pragma unroll
+    for (int u = 0; u < DEPTH; ++u) {
+      const int t = t0 + u;
+      if (t >= ntile) break;
+      load(buf[(u + PF) % DEPTH], t + PF);
+      body(buf[u], t);
+    }
+  }
+}
+
+// Prefetch distance (in tiles) of each streaming pass.
+#ifndef FS_PF_SLICE
+#define FS_PF_SLICE 2
+#endif
+#ifndef FS_PF_DESLICE
+#define FS_PF_DESLICE 2
+#endif
+#ifndef FS_PF_BWD_A
+#define FS_PF_BWD_A 2
+#endif
+#ifndef FS_PF_BWD_B
+#define FS_PF_BWD_B 1
+#endif
 
 struct HeadCtx {
   int bh, b, h, g0;
