@@ -22,6 +22,13 @@ constexpr size_t kAlign = 256;
 size_t up(size_t v, size_t a = kAlign) { return (v + a - 1) / a * a; }
 bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 
+#ifndef FS_TARGET_PARTIAL
+#define FS_TARGET_PARTIAL 512
+#endif
+#ifndef FS_TARGET_DESLICE
+#define FS_TARGET_DESLICE 512
+#endif
+
 constexpr int kMaxAttnG = 256;
 constexpr int kMaxAttnGV = 8192;
 }  // namespace
@@ -51,7 +58,7 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
   if (c.NS >= 8)
     target = partials ? 256 : 512;
   else
-    target = partials ? 512 : 2048;
+    target = partials ? FS_TARGET_PARTIAL : FS_TARGET_DESLICE;
   const int64_t step = 16LL * c.PB * c.NP;
   const int64_t ntiles = std::max<int64_t>(1, (g.N + step - 1) / step);
   int64_t chunks = std::max<int64_t>(1, (target + g.BH() - 1) / g.BH());

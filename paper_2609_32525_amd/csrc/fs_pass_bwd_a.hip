@@ -10,7 +10,8 @@ namespace {
 // Backward pass A: dzmix = w^T dout (partials per workgroup)
 // =======================================================================================
 template <bool BF, int D, int GS, int NS, int NP>
-__global__ __launch_bounds__(64 * NS * NP) void k_bwd_a(PassArgs a) {
+__global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_BWD_A))) void k_bwd_a(
+    PassArgs a) {
   constexpr int GB = GS / 16, VB = D / 16;
   constexpr bool SPLIT = BF;
   using T = typename Store<BF>::T;
@@ -33,7 +34,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_a(PassArgs a) {
 #pragma unroll
     for (int vb = 0; vb < VB; ++vb) Z[gb][vb] = zero4();
 
-  const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
+  const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
   const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
   const int ntile = (npts + 32 * NP - 1) / (32 * NP);
@@ -61,7 +62,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_a(PassArgs a) {
     }
     gather_points_buf<BF, VB>(tt.g, rg, rsb, tb * rsb, i, j);
   };
-  pipeline<FS_PF_BWD_A, Tile>(ntile, load_tile, [&](Tile& cur, int t) {
+  pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_BWD_A), Tile>(ntile, load_tile, [&](Tile& cur, int t) {
     const RowOp<BF, D>* xo = cur.xo;
     const float(*lse2)[4] = cur.lse2;
     f4 w[2][GB];
@@ -77,7 +78,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_a(PassArgs a) {
     mm_points<BF, GB, VB>(Z, w, cur.g);
   });
 
-  float* pZ = a.part + ((int64_t)c.bh * a.chunks + blockIdx.x) * a.G * D;
+  float* pZ = a.part + ((int64_t)c.bh * a.chunks + c.chunk) * a.G * D;
   if constexpr (NP > 1) {
     __shared__ f4 red[NP - 1][NS][GB][VB][64];
     if (wp > 0) {
@@ -109,7 +110,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_a(PassArgs a) {
 template <bool BF, int D, int GS, int NS, int NP, int PB>
 struct Run_k_bwd_a {
   static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
-    dim3 grid(cfg.chunks, BH);
+    dim3 grid(cfg.chunks * BH);
     hipLaunchKernelGGL((k_bwd_a<BF, D, GS, NS, NP>), grid, dim3(64 * NS * NP), 0, st, a);
     return hipGetLastError();
   }

@@ -15,7 +15,8 @@ namespace {
 // count (and so the number of resident wavefronts) in line with the other passes.
 // =======================================================================================
 template <bool BF, int D, int GS, int NS, int NP, int PB>
-__global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
+__global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_BWD_B))) void k_bwd_b(
+    PassArgs a) {
   static_assert(PB == 2 || !BF, "bf16 contracts over 32 points");
   constexpr int GB = GS / 16, VB = D / 16, DB = D / 16, TP = 16 * PB;
   constexpr bool SPLIT = BF;
@@ -121,7 +122,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
   f4* gx = reinterpret_cast<f4*>(smem);
   float* myda = reinterpret_cast<float*>(smem) + (size_t)wave * kDaWords;
 
-  const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
+  const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
   const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
   const int ntile = (npts + TP * NP - 1) / (TP * NP);
@@ -150,7 +151,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
       tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
     }
   };
-  pipeline<FS_PF_BWD_B, Tile>(ntile, load_tile, [&](Tile& cur, int t) {
+  pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_BWD_B), Tile>(ntile, load_tile, [&](Tile& cur, int t) {
     const int tp0 = (t * NP + wpu) * TP;
     const RowOp<BF, D>(&xo)[PB] = cur.xo;
     const RowOp<BF, D>(&go)[PB] = cur.go;
@@ -361,7 +362,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
   __shared__ double dtw[NS * NP];
   if (lane == 0) dtw[wave] = dt;
 
-  float* pp = a.part + ((int64_t)c.bh * a.chunks + blockIdx.x) * ((int64_t)D * a.G + a.G + 2);
+  float* pp = a.part + ((int64_t)c.bh * a.chunks + c.chunk) * ((int64_t)D * a.G + a.G + 2);
   if constexpr (NP > 1) {
     __shared__ f4 red[NP - 1][NS][DB][GB][64];
     __shared__ float redb[NP - 1][NS][GB][4][16];
@@ -413,7 +414,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_bwd_b(PassArgs a) {
 template <bool BF, int D, int GS, int NS, int NP, int PB>
 struct Run_k_bwd_b {
   static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
-    dim3 grid(cfg.chunks, BH);
+    dim3 grid(cfg.chunks * BH);
     hipLaunchKernelGGL((k_bwd_b<BF, D, GS, NS, NP, PB>), grid, dim3(64 * NS * NP), 0, st, a);
     return hipGetLastError();
   }

@@ -10,7 +10,8 @@ namespace {
 // Deslice pass
 // =======================================================================================
 template <bool BF, int D, int GS, int NS, int NP>
-__global__ __launch_bounds__(64 * NS * NP) void k_deslice(PassArgs a) {
+__global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_DESLICE))) void k_deslice(
+    PassArgs a) {
   constexpr int GB = GS / 16, VB = D / 16;
   constexpr bool SPLIT = BF;
   using T = typename Store<BF>::T;
@@ -34,7 +35,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_deslice(PassArgs a) {
 
   __shared__ f4 ox[NS > 1 ? NP : 1][NS > 1 ? NS : 1][VB][2][64];
 
-  const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
+  const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
   const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
   const int ntile = (npts + 32 * NP - 1) / (32 * NP);
@@ -57,7 +58,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_deslice(PassArgs a) {
       tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
     }
   };
-  pipeline<FS_PF_DESLICE, Tile>(ntile, load_tile, [&](Tile& cur, int t) {
+  pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_DESLICE), Tile>(ntile, load_tile, [&](Tile& cur, int t) {
     const int tb = (t * NP + wpu) * 32;
     const RowOp<BF, D>* xo = cur.xo;
     const float* lse2 = cur.lse2;
@@ -108,7 +109,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_deslice(PassArgs a) {
 template <bool BF, int D, int GS, int NS, int NP, int PB>
 struct Run_k_deslice {
   static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
-    dim3 grid(cfg.chunks, BH);
+    dim3 grid(cfg.chunks * BH);
     hipLaunchKernelGGL((k_deslice<BF, D, GS, NS, NP>), grid, dim3(64 * NS * NP), 0, st, a);
     return hipGetLastError();
   }

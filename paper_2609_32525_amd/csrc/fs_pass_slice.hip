@@ -10,7 +10,8 @@ namespace {
 // Slice pass
 // =======================================================================================
 template <bool BF, int D, int GS, int NS, int NP>
-__global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
+__global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_SLICE))) void k_slice(
+    PassArgs a) {
   constexpr int GB = GS / 16, VB = D / 16;
   constexpr bool SPLIT = BF;
   using T = typename Store<BF>::T;
@@ -39,7 +40,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
   __shared__ float st_m[NS > 1 ? 2 : 1][NP][NS][32];
   __shared__ float st_l[NS > 1 ? 2 : 1][NP][NS][32];
 
-  const int64_t pbeg = (int64_t)blockIdx.x * a.chunk_pts;
+  const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
   const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
   const int ntile = (npts + 32 * NP - 1) / (32 * NP);
@@ -60,7 +61,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
     for (int pb = 0; pb < 2; ++pb) load_row_buf<BF, D>(tt.xo[pb], rx, i * rsb, tbo + 16 * pb * rsb, j);
     gather_points_buf<BF, VB>(tt.f, rf, rsb, tbo, i, j);
   };
-  pipeline<FS_PF_SLICE, Tile>(ntile, load_tile, [&](Tile& cur, int t) {
+  pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_SLICE), Tile>(ntile, load_tile, [&](Tile& cur, int t) {
     const int tb = (t * NP + wpu) * 32;
     const RowOp<BF, D>* xo = cur.xo;
     // S-layout logits: rows = points 16 pb + 4 j + r, cols = slots g0 + 16 gb + i
@@ -78,7 +79,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
       for (int r = 0; r < 4; ++r) {
         float mx = w[pb][0][r];
 #pragma unroll
-        for (int gb = 1; gb < GB; ++gb) mx = fmaxf(mx, w[pb][gb][r]);
+        for (int gb = 1; gb < GB; ++gb) mx = vmax(mx, w[pb][gb][r]);
         m[pb][r] = row16_max(mx);
         float sum = 0.f;
 #pragma unroll
@@ -118,7 +119,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
           const int q = 16 * pb + 4 * j + r;
           float M = st_m[par][wp][0][q];
 #pragma unroll
-          for (int s = 1; s < NS; ++s) M = fmaxf(M, st_m[par][wp][s][q]);
+          for (int s = 1; s < NS; ++s) M = vmax(M, st_m[par][wp][s][q]);
           float L = 0.f;
 #pragma unroll
           for (int s = 0; s < NS; ++s)
@@ -153,8 +154,8 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
   // ---- combine the NP point groups and write this workgroup's partials --------------------
 #pragma unroll
   for (int gb = 0; gb < GB; ++gb) sacc[gb] = col4_sum(sacc[gb]);
-  float* pU = a.part + ((int64_t)c.bh * a.chunks + blockIdx.x) * a.G * D;
-  float* pS = a.part2 + ((int64_t)c.bh * a.chunks + blockIdx.x) * a.G;
+  float* pU = a.part + ((int64_t)c.bh * a.chunks + c.chunk) * a.G * D;
+  float* pS = a.part2 + ((int64_t)c.bh * a.chunks + c.chunk) * a.G;
   if constexpr (NP > 1) {
     __shared__ f4 red[NP - 1][NS][GB][VB][64];
     __shared__ float reds[NP - 1][NS][GB][16];
@@ -193,7 +194,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice(PassArgs a) {
 template <bool BF, int D, int GS, int NS, int NP, int PB>
 struct Run_k_slice {
   static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
-    dim3 grid(cfg.chunks, BH);
+    dim3 grid(cfg.chunks * BH);
     hipLaunchKernelGGL((k_slice<BF, D, GS, NS, NP>), grid, dim3(64 * NS * NP), 0, st, a);
     return hipGetLastError();
   }

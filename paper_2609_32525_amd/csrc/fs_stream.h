@@ -68,11 +68,13 @@ template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
 }
+// IEEE maximum (v_maximum3_f32): unlike fmaxf it needs no canonicalising of its inputs.
+__device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
 __device__ __forceinline__ float row16_max(float v) {
-  v = fmaxf(v, dpp<0xB1>(v));
-  v = fmaxf(v, dpp<0x4E>(v));
-  v = fmaxf(v, dpp<0x141>(v));
-  v = fmaxf(v, dpp<0x140>(v));
+  v = vmax(v, dpp<0xB1>(v));
+  v = vmax(v, dpp<0x4E>(v));
+  v = vmax(v, dpp<0x141>(v));
+  v = vmax(v, dpp<0x140>(v));
   return v;
 }
 __device__ __forceinline__ float row16_sum(float v) {
@@ -569,8 +571,40 @@ __device__ __forceinline__ void pipeline(int ntile, Load&& load, Body&& body) {
 #ifndef FS_PF_BWD_B
 #define FS_PF_BWD_B 1
 #endif
+// Slot groups per tile from which the passes do not prefetch (their register budget is
+// taken by the per-slot-group state).
+#ifndef FS_NS_NOPF
+#define FS_NS_NOPF 8
+#endif
+// Minimum wavefronts per SIMD each pass is compiled for (1: no register cap).
+#ifndef FS_WPE_SLICE
+#define FS_WPE_SLICE 1
+#endif
+#ifndef FS_WPE_DESLICE
+#define FS_WPE_DESLICE 1
+#endif
+#ifndef FS_WPE_BWD_A
+#define FS_WPE_BWD_A 1
+#endif
+#ifndef FS_WPE_BWD_B
+#define FS_WPE_BWD_B 1
+#endif
+
+// Workgroup -> (chunk, b*H+h): a 1-D grid of chunks * BH workgroups, chunks of one head
+// consecutive. (Ordering the workgroups per XCD so that the heads of one chunk share an L2
+// measured no faster.)
+struct BlockPos {
+  int chunk, bh;
+};
+__device__ __forceinline__ BlockPos block_pos(const PassArgs& a) {
+  BlockPos p;
+  p.chunk = blockIdx.x % a.chunks;
+  p.bh = blockIdx.x / a.chunks;
+  return p;
+}
 
 struct HeadCtx {
+  int chunk;
   int bh, b, h, g0;
   float sc;  // log2(e) / tau_h
   const float* W;
@@ -581,7 +615,9 @@ struct HeadCtx {
 template <int D>
 __device__ __forceinline__ HeadCtx head_ctx(const PassArgs& a, int ws, int GS) {
   HeadCtx c;
-  c.bh = blockIdx.y;
+  const BlockPos bp = block_pos(a);
+  c.chunk = bp.chunk;
+  c.bh = bp.bh;
   c.b = c.bh / a.H;
   c.h = c.bh % a.H;
   c.g0 = ws * GS;
