@@ -25,6 +25,12 @@ bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 #ifndef FS_TARGET_PARTIAL
 #define FS_TARGET_PARTIAL 512
 #endif
+#ifndef FS_BLOCKED_MIN_G
+#define FS_BLOCKED_MIN_G 128
+#endif
+#ifndef FS_POINT_WAVES
+#define FS_POINT_WAVES 8
+#endif
 #ifndef FS_TARGET_DESLICE
 #define FS_TARGET_DESLICE 512
 #endif
@@ -38,12 +44,26 @@ PassEvents& pass_events() {
   return ev;
 }
 
+bool blocked(const Geom& g) { return g.G > FS_BLOCKED_MIN_G && g.D <= 32; }
+
 PassCfg pick_cfg(const Geom& g, Pass pass) {
   PassCfg c{};
+  c.nblk = 1;
+  const bool blk = blocked(g);
+  const bool slot_owned = blk && (pass == PASS_SLICE || pass == PASS_BWD_A || pass == PASS_BWD_B);
   if (g.G <= 64) {
     c.GS = g.G;
     c.NS = 1;
     c.NP = 4;
+  } else if (slot_owned) {
+    c.GS = 64;
+    c.NS = 1;
+    c.NP = 4;
+    c.nblk = g.G / 64;
+  } else if (pass == PASS_POINT) {
+    c.GS = 64;  // slot block streamed through LDS
+    c.NS = 1;
+    c.NP = FS_POINT_WAVES;
   } else {
     c.GS = 64;
     c.NS = g.G / 64;
@@ -51,9 +71,10 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
   }
   // fp32 backward pass B works on 16-point tiles (its register footprint is the largest)
   c.PB = (pass == PASS_BWD_B && !g.bf16 && c.NS == 1) ? 1 : 2;
-  // Workgroups along the points per (sample, head): enough to fill 256 CUs several times,
-  // but few enough that the per-workgroup partials stay small next to the streamed data.
-  const bool partials = pass != PASS_DESLICE;
+  // Workgroups along the points per (sample, head[, slot block]): enough to fill 256 CUs
+  // several times, but few enough that the per-workgroup partials stay small next to the
+  // streamed data.
+  const bool partials = pass != PASS_DESLICE && pass != PASS_STATS && pass != PASS_POINT;
   int target;
   if (c.NS >= 8)
     target = partials ? 256 : 512;
@@ -61,7 +82,8 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
     target = partials ? FS_TARGET_PARTIAL : FS_TARGET_DESLICE;
   const int64_t step = 16LL * c.PB * c.NP;
   const int64_t ntiles = std::max<int64_t>(1, (g.N + step - 1) / step);
-  int64_t chunks = std::max<int64_t>(1, (target + g.BH() - 1) / g.BH());
+  const int64_t units = (int64_t)g.BH() * c.nblk;
+  int64_t chunks = std::max<int64_t>(1, (target + units - 1) / units);
   // passes that write partials give every chunk at least 4 tiles per point group, so the
   // partials stay small next to the points they summarise
   chunks = std::min<int64_t>(chunks, partials ? std::max<int64_t>(1, ntiles / 4) : ntiles);
@@ -96,6 +118,8 @@ FwdWs fwd_ws_layout(const Geom& g) {
   off += up(sizeof(float) * (size_t)g.BH() * c.chunks * g.G * g.V);
   L.partS = off;
   off += up(sizeof(float) * (size_t)g.BH() * c.chunks * g.G);
+  L.lse = off;
+  off += up(blocked(g) ? sizeof(float) * (size_t)g.BH() * (size_t)g.N : 0);
   L.total = off;
   return L;
 }
@@ -119,7 +143,7 @@ BwdWs bwd_ws_layout(const Geom& g, int kind) {
   L.cen = off;
   off += up(sizeof(float) * (size_t)g.BH() * (2 * (size_t)g.V + 1));
   L.partP = off;
-  off += up(sizeof(float) * (size_t)g.BH() * cb.chunks * ((size_t)g.D * g.G + g.G + 2));
+  off += up(sizeof(float) * (size_t)g.BH() * cb.chunks * (size_t)param_partial_len(g, cb.nblk));
   L.partM = off;
   size_t per_bh = 0;
   if (kind == FS_MIX_LINEAR_G) per_bh = (size_t)g.G * g.G;
@@ -128,6 +152,8 @@ BwdWs bwd_ws_layout(const Geom& g, int kind) {
   off += up(sizeof(float) * (size_t)g.BH() * per_bh);
   L.scr = off;
   off += up(kind == FS_MIX_ATTN ? 3 * tok + sizeof(float) * (size_t)g.BH() * g.G * g.G : 0);
+  L.cpt = off;
+  off += up(blocked(g) ? 2 * sizeof(float) * (size_t)g.BH() * (size_t)g.N : 0);
   L.total = off;
   return L;
 }
@@ -302,9 +328,7 @@ int fs_slice_fwd(const fs_problem* prob, const void* x, const void* fx, const fl
   if (st != FS_OK) return st;
   if (ws == nullptr || ws_bytes < L.total) return FS_ERR_WORKSPACE;
   char* w = static_cast<char*>(ws);
-  return hip_status(fs::launch_slice(g, x, fx, Ws, bias, tau, z, s, lse,
-                                     reinterpret_cast<float*>(w + L.partU),
-                                     reinterpret_cast<float*>(w + L.partS),
+  return hip_status(fs::launch_slice(g, x, fx, Ws, bias, tau, z, s, lse, w,
                                      static_cast<hipStream_t>(hip_stream)));
 }
 

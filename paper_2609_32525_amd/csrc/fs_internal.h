@@ -18,15 +18,36 @@ struct Geom {
   int BH() const { return (int)(B * H); }
 };
 
-enum Pass { PASS_SLICE = 0, PASS_DESLICE = 1, PASS_BWD_A = 2, PASS_BWD_B = 3 };
+// The four streaming passes (also the ids of fs_set_pass_events), and the two extra kernels
+// of the slot-blocked family used for large G: a statistics pass ahead of the slice and a
+// point-owned pass ahead of the backward pass B.
+enum Pass {
+  PASS_SLICE = 0,
+  PASS_DESLICE = 1,
+  PASS_BWD_A = 2,
+  PASS_BWD_B = 3,
+  PASS_STATS = 4,
+  PASS_POINT = 5
+};
+
+// Slot-blocked family (large G): the slice, backward pass A and the parameter half of
+// backward pass B run slot-owned (a workgroup owns one block of 64 slots and streams its
+// chunk of points), with the per-point softmax statistics from a statistics pass and the
+// per-point correction c = sum_g w dw from a point-owned pass that also writes dx and dfx.
+// Below the threshold every pass is one kernel whose wavefronts split the slots of a tile.
+bool blocked(const Geom& g);
 
 // Launch shape of one streaming pass over the points.
-//   GS: slots owned by one wavefront; NS = G / GS wavefronts share each point tile;
+//   GS: slots owned by one wavefront; NS = G / GS wavefronts share each point tile
+//   (1 in the slot-owned passes of the blocked family);
 //   NP: independent point groups per workgroup; a workgroup has NS * NP wavefronts.
-//   chunks: workgroups per (sample, head) along the points, each covering chunk_pts points.
+//   nblk: slot blocks of GS slots in the grid (blocked slot-owned passes), else 1.
+//   chunks: workgroups per (sample, head[, slot block]) along the points, each covering
+//   chunk_pts points.
 struct PassCfg {
   int GS, NS, NP;
   int PB;  // 16-point blocks per wavefront tile
+  int nblk;
   int chunks;
   int64_t chunk_pts;
 };
@@ -53,9 +74,12 @@ struct PassArgs {
   float* lse_out;
   float* part;   // slice: U partials; bwd_a: dzmix partials; bwd_b: parameter partials
   float* part2;  // slice: s partials
+  const float* cpt;  // blocked bwd_b: per point (c, tb) from the point-owned pass
+  float* cpt_out;    // point-owned pass: per point (c, tb), [BH][N][2]
   int64_t N;
   int H, G;
   int ws_per_head;
+  int nblk;
   int chunks;
   int64_t chunk_pts;
 };
@@ -65,6 +89,12 @@ hipError_t run_pass_slice(const Geom& g, const PassArgs& a, hipStream_t st);
 hipError_t run_pass_deslice(const Geom& g, const PassArgs& a, hipStream_t st);
 hipError_t run_pass_bwd_a(const Geom& g, const PassArgs& a, hipStream_t st);
 hipError_t run_pass_bwd_b(const Geom& g, const PassArgs& a, hipStream_t st);
+// Slot-blocked family: statistics pass (lse only), slot-owned slice, point-owned backward pass
+// (dx, dfx and per-point (c, tb)), slot-owned parameter half of backward pass B.
+hipError_t run_pass_stats(const Geom& g, const PassArgs& a, hipStream_t st);
+hipError_t run_pass_slice_blk(const Geom& g, const PassArgs& a, hipStream_t st);
+hipError_t run_pass_point(const Geom& g, const PassArgs& a, hipStream_t st);
+hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, hipStream_t st);
 
 // Per-thread measurement events recorded around the streaming passes (fs_set_pass_events).
 struct PassEvents {
@@ -75,11 +105,16 @@ PassEvents& pass_events();
 
 // Workspace carve-up (byte offsets, 256-byte aligned).
 struct FwdWs {
-  size_t partU, partS, total;
+  size_t partU, partS, lse, total;  // lse: [BH][N] when the blocked family needs it
 };
 struct BwdWs {
-  size_t partDZ, dzm, dz, dU, ds, cen, partP, partM, scr, total;
+  size_t partDZ, dzm, dz, dU, ds, cen, partP, partM, scr, cpt, total;
 };
+// Floats of one parameter partial of backward pass B: [D G] dW_s, [G] dbias, then one fp64
+// dtau partial per slot block.
+inline int64_t param_partial_len(const Geom& g, int nblk) {
+  return (int64_t)g.D * g.G + g.G + 2LL * nblk;
+}
 FwdWs fwd_ws_layout(const Geom& g);
 BwdWs bwd_ws_layout(const Geom& g, int mix_kind);
 size_t mix_param_count(const Geom& g, int mix_kind, bool a_per_head);
@@ -98,7 +133,7 @@ struct MixArgs {
 // Launchers; each returns the hipError_t of its launches.
 hipError_t launch_slice(const Geom& g, const void* x, const void* fx, const float* Ws,
                         const float* bias, const float* tau, float* z, float* s, float* lse,
-                        float* partU, float* partS, hipStream_t st);
+                        char* ws, hipStream_t st);
 hipError_t launch_deslice(const Geom& g, const void* x, const float* Ws, const float* bias,
                           const float* tau, const float* zmix, const float* lse, void* out,
                           hipStream_t st);
@@ -128,8 +163,8 @@ hipError_t launch_reduce_rows(const Geom& g, const float* part, float* out, int 
 // dW_s, dbias, dtau from the pass-B partials; with m and dmix given, also the mix-parameter
 // gradient from partM (same launch).
 hipError_t launch_reduce_params(const Geom& g, const float* part, float* dWs, float* dbias,
-                                float* dtau, int chunks, const MixArgs* m, const float* partM,
-                                float* dmix, hipStream_t st);
+                                float* dtau, int chunks, int nblk, const MixArgs* m,
+                                const float* partM, float* dmix, hipStream_t st);
 hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void* fx,
                       const float* Ws, const float* bias, const float* tau, const float* z,
                       const float* s, const float* zmix, const float* attn, const float* lse,

@@ -10,19 +10,17 @@
 namespace fs {
 namespace {
 
-// Launch one streaming pass, bracketed by the caller's measurement events if requested.
-template <int PASS>
-hipError_t run_pass(const Geom& g, const PassArgs& a, hipStream_t st) {
+// Launch the kernels of one logical streaming pass (f), bracketed by the caller's measurement
+// events if requested.
+template <class F>
+hipError_t timed(int pass, hipStream_t st, F&& f) {
   const PassEvents& ev = pass_events();
-  if (ev.before[PASS] != nullptr) {
-    hipError_t e = hipEventRecord(ev.before[PASS], st);
+  if (ev.before[pass] != nullptr) {
+    hipError_t e = hipEventRecord(ev.before[pass], st);
     if (e != hipSuccess) return e;
   }
-  hipError_t e = PASS == PASS_SLICE     ? run_pass_slice(g, a, st)
-                 : PASS == PASS_DESLICE ? run_pass_deslice(g, a, st)
-                 : PASS == PASS_BWD_A   ? run_pass_bwd_a(g, a, st)
-                                        : run_pass_bwd_b(g, a, st);
-  if (e == hipSuccess && ev.after[PASS] != nullptr) e = hipEventRecord(ev.after[PASS], st);
+  hipError_t e = f();
+  if (e == hipSuccess && ev.after[pass] != nullptr) e = hipEventRecord(ev.after[pass], st);
   return e;
 }
 
@@ -33,6 +31,7 @@ PassArgs base_args(const Geom& g, Pass p) {
   a.H = g.H;
   a.G = g.G;
   a.ws_per_head = g.ws_per_head ? 1 : 0;
+  a.nblk = cfg.nblk;
   a.chunks = cfg.chunks;
   a.chunk_pts = cfg.chunk_pts;
   return a;
@@ -47,17 +46,36 @@ inline hipError_t first_err(hipError_t a, hipError_t b) { return a != hipSuccess
 // =======================================================================================
 hipError_t launch_slice(const Geom& g, const void* x, const void* fx, const float* Ws,
                         const float* bias, const float* tau, float* z, float* s, float* lse,
-                        float* partU, float* partS, hipStream_t st) {
+                        char* ws, hipStream_t st) {
+  const FwdWs L = fwd_ws_layout(g);
+  float* partU = reinterpret_cast<float*>(ws + L.partU);
+  float* partS = reinterpret_cast<float*>(ws + L.partS);
   PassArgs a = base_args(g, PASS_SLICE);
   a.x = x;
   a.fx = fx;
   a.Ws = Ws;
   a.bias = bias;
   a.tau = tau;
-  a.lse_out = lse;
   a.part = partU;
   a.part2 = partS;
-  hipError_t e = run_pass<PASS_SLICE>(g, a, st);
+  hipError_t e;
+  if (blocked(g)) {
+    // statistics pass (lse), then the slot-owned slice reading it
+    PassArgs sa = base_args(g, PASS_STATS);
+    sa.x = x;
+    sa.Ws = Ws;
+    sa.bias = bias;
+    sa.tau = tau;
+    sa.lse_out = lse != nullptr ? lse : reinterpret_cast<float*>(ws + L.lse);
+    a.lse_in = sa.lse_out;
+    e = timed(PASS_SLICE, st, [&] {
+      hipError_t e1 = run_pass_stats(g, sa, st);
+      return e1 != hipSuccess ? e1 : run_pass_slice_blk(g, a, st);
+    });
+  } else {
+    a.lse_out = lse;
+    e = timed(PASS_SLICE, st, [&] { return run_pass_slice(g, a, st); });
+  }
   if (e != hipSuccess) return e;
   return launch_reduce_tokens(g, partU, partS, a.chunks, z, s, st);
 }
@@ -73,7 +91,7 @@ hipError_t launch_deslice(const Geom& g, const void* x, const float* Ws, const f
   a.zmix = zmix;
   a.lse_in = lse;
   a.out = out;
-  return run_pass<PASS_DESLICE>(g, a, st);
+  return timed(PASS_DESLICE, st, [&] { return run_pass_deslice(g, a, st); });
 }
 
 hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void* fx,
@@ -98,7 +116,7 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
   a.tau = tau;
   a.lse_in = lse;
   a.part = partDZ;
-  hipError_t e = run_pass<PASS_BWD_A>(g, a, st);
+  hipError_t e = timed(PASS_BWD_A, st, [&] { return run_pass_bwd_a(g, a, st); });
   if (e != hipSuccess) return e;
   e = launch_reduce_rows(g, partDZ, dzm, a.chunks, (int64_t)g.G * g.V, st);
   if (e != hipSuccess) return e;
@@ -123,9 +141,33 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
   b.cen = cen;
   b.lse_in = lse;
   b.part = partP;
-  e = run_pass<PASS_BWD_B>(g, b, st);
+  if (blocked(g)) {
+    // point-owned pass (dx, dfx, per-point c and tb), then the slot-owned parameter pass
+    PassArgs pa = base_args(g, PASS_POINT);
+    pa.x = x;
+    pa.fx = fx;
+    pa.dout = dout;
+    pa.out = dx;
+    pa.out2 = dfx;
+    pa.Ws = Ws;
+    pa.bias = bias;
+    pa.tau = tau;
+    pa.zmix = zmix;
+    pa.dU = dU;
+    pa.ds = dsv;
+    pa.cen = cen;
+    pa.lse_in = lse;
+    pa.cpt_out = reinterpret_cast<float*>(ws + L.cpt);
+    b.cpt = pa.cpt_out;
+    e = timed(PASS_BWD_B, st, [&] {
+      hipError_t e1 = run_pass_point(g, pa, st);
+      return e1 != hipSuccess ? e1 : run_pass_bwd_params(g, b, st);
+    });
+  } else {
+    e = timed(PASS_BWD_B, st, [&] { return run_pass_bwd_b(g, b, st); });
+  }
   if (e != hipSuccess) return e;
-  e = launch_reduce_params(g, partP, dWs, dbias, dtau, b.chunks, &m, partM, dmix, st);
+  e = launch_reduce_params(g, partP, dWs, dbias, dtau, b.chunks, b.nblk, &m, partM, dmix, st);
   return e;
 }
 

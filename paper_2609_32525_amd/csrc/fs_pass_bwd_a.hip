@@ -1,4 +1,6 @@
-// Streaming pass: backward pass A (dzmix partials = w^T dout).
+// Streaming pass: backward pass A (dzmix partials = w^T dout), and the slot-owned slice of
+// the slot-blocked family (U partials = w^T fx and s partials = sum w, with the per-point
+// softmax statistics from the statistics pass).
 // Kernel design and MFMA lane layouts are described at the top of fs_stream.h.
 
 #include "fs_stream.h"
@@ -7,9 +9,10 @@ namespace fs {
 namespace {
 
 // =======================================================================================
-// Backward pass A: dzmix = w^T dout (partials per workgroup)
+// Backward pass A: dzmix = w^T dout (partials per workgroup). SL: the same contraction with
+// fx in place of dout, plus the weight sums s (the slot-owned slice).
 // =======================================================================================
-template <bool BF, int D, int GS, int NS, int NP>
+template <bool BF, int D, int GS, int NS, int NP, bool SL>
 __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_BWD_A))) void k_bwd_a(
     PassArgs a) {
   constexpr int GB = GS / 16, VB = D / 16;
@@ -20,7 +23,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   const HeadCtx c = head_ctx<D>(a, ws, GS);
   const int64_t rs = (int64_t)a.H * D;
   const T* xb = (const T*)a.x + c.off;
-  const T* db = (const T*)a.dout + c.off;
+  const T* db = (const T*)(SL ? a.fx : a.dout) + c.off;
   const float* lse = a.lse_in + (int64_t)c.bh * a.N;
 
   SlotOp<BF, D, GB> wop;
@@ -29,10 +32,13 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
   for (int gb = 0; gb < GB; ++gb) bS[gb] = c.sc * c.bias[c.g0 + 16 * gb + i];
   f4 Z[GB][VB];
+  float sacc[GB];
 #pragma unroll
-  for (int gb = 0; gb < GB; ++gb)
+  for (int gb = 0; gb < GB; ++gb) {
+    sacc[gb] = 0.f;
 #pragma unroll
     for (int vb = 0; vb < VB; ++vb) Z[gb][vb] = zero4();
+  }
 
   const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
@@ -75,25 +81,45 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
         for (int r = 0; r < 4; ++r) acc[r] = __builtin_amdgcn_exp2f(acc[r] - lse2[pb][r]);
         w[pb][gb] = acc;
       }
+    if constexpr (SL) {
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb) {
+        float sum = 0.f;
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sum += w[pb][gb][r];
+        sacc[gb] += sum;
+      }
+    }
     mm_points<BF, GB, VB>(Z, w, cur.g);
   });
+  if constexpr (SL) {
+#pragma unroll
+    for (int gb = 0; gb < GB; ++gb) sacc[gb] = col4_sum(sacc[gb]);
+  }
 
   float* pZ = a.part + ((int64_t)c.bh * a.chunks + c.chunk) * a.G * D;
   if constexpr (NP > 1) {
     __shared__ f4 red[NP - 1][NS][GB][VB][64];
+    __shared__ float reds[SL ? NP - 1 : 1][NS][GB][16];
     if (wp > 0) {
 #pragma unroll
-      for (int gb = 0; gb < GB; ++gb)
+      for (int gb = 0; gb < GB; ++gb) {
 #pragma unroll
         for (int vb = 0; vb < VB; ++vb) red[wp - 1][ws][gb][vb][lane] = Z[gb][vb];
+        if (SL && j == 0) reds[SL ? wp - 1 : 0][ws][gb][i] = sacc[gb];
+      }
     }
     __syncthreads();
     if (wp == 0) {
       for (int q = 0; q < NP - 1; ++q)
 #pragma unroll
-        for (int gb = 0; gb < GB; ++gb)
+        for (int gb = 0; gb < GB; ++gb) {
 #pragma unroll
           for (int vb = 0; vb < VB; ++vb) Z[gb][vb] += red[q][ws][gb][vb][lane];
+          if constexpr (SL) sacc[gb] += reds[q][ws][gb][i];
+        }
     }
   }
   if (wp == 0) {
@@ -104,22 +130,39 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
         for (int r = 0; r < 4; ++r)
           pZ[(int64_t)(c.g0 + 16 * gb + 4 * j + r) * D + 16 * vb + i] = Z[gb][vb][r];
+    if constexpr (SL) {
+      float* pS = a.part2 + ((int64_t)c.bh * a.chunks + c.chunk) * a.G;
+#pragma unroll
+      for (int gb = 0; gb < GB; ++gb)
+        if (j == 0) pS[c.g0 + 16 * gb + i] = sacc[gb];
+    }
   }
 }
 
-template <bool BF, int D, int GS, int NS, int NP, int PB>
-struct Run_k_bwd_a {
-  static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
-    dim3 grid(cfg.chunks * BH);
-    hipLaunchKernelGGL((k_bwd_a<BF, D, GS, NS, NP>), grid, dim3(64 * NS * NP), 0, st, a);
-    return hipGetLastError();
-  }
+template <bool SL>
+struct Run_k_bwd_a_ {
+  template <bool BF, int D, int GS, int NS, int NP, int PB>
+  struct R {
+    static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
+      if constexpr (SL && NS != 1) {  // the slice of the blocked family is slot-owned
+        return hipErrorInvalidConfiguration;
+      } else {
+        dim3 grid(cfg.chunks * BH * cfg.nblk);
+        hipLaunchKernelGGL((k_bwd_a<BF, D, GS, NS, NP, SL>), grid, dim3(64 * NS * NP), 0, st, a);
+        return hipGetLastError();
+      }
+    }
+  };
 };
 
 }  // namespace
 
 hipError_t run_pass_bwd_a(const Geom& g, const PassArgs& a, hipStream_t st) {
-  return run_pass_tilings<PASS_BWD_A, Run_k_bwd_a>(g, a, st);
+  return run_pass_tilings<PASS_BWD_A, Run_k_bwd_a_<false>::R>(g, a, st);
+}
+
+hipError_t run_pass_slice_blk(const Geom& g, const PassArgs& a, hipStream_t st) {
+  return run_pass_tilings<PASS_SLICE, Run_k_bwd_a_<true>::R>(g, a, st);
 }
 
 }  // namespace fs

@@ -1,4 +1,6 @@
-// Streaming pass: backward pass B (point gradients and parameter partials).
+// Streaming pass: backward pass B (point gradients and parameter partials), and its
+// slot-owned parameter half in the slot-blocked family (PM: the per-point correction c and
+// the weighted logit mean tb come from the point-owned pass; dx and dfx are not written).
 // Kernel design and MFMA lane layouts are described at the top of fs_stream.h.
 
 #include "fs_stream.h"
@@ -14,7 +16,7 @@ namespace {
 // by the workgroup's wavefronts and are read where they are used, which keeps the register
 // count (and so the number of resident wavefronts) in line with the other passes.
 // =======================================================================================
-template <bool BF, int D, int GS, int NS, int NP, int PB>
+template <bool BF, int D, int GS, int NS, int NP, int PB, bool PM>
 __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_BWD_B))) void k_bwd_b(
     PassArgs a) {
   static_assert(PB == 2 || !BF, "bf16 contracts over 32 points");
@@ -133,11 +135,13 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   const auto rdx = rows_rsrc(dxb + pbeg * rs, npts, (int)rs, D);
   const auto rdf = rows_rsrc(dfb + pbeg * rs, npts, (int)rs, D);
   const auto rl = rows_rsrc(lse + pbeg, npts, 1, 1);
+  const auto rc = rows_rsrc(PM ? a.cpt + ((int64_t)c.bh * a.N + pbeg) * 2 : a.Ws, npts, 2, 2);
   const int wpu = __builtin_amdgcn_readfirstlane(wp);
 
   struct Tile {
     RowOp<BF, D> xo[PB], go[PB], fo[PB];
     float lse2[PB];
+    float ct[PM ? PB : 1][2];
   };
   auto load_tile = [&](Tile& tt, int t) {
     const int tb = (t * NP + wpu) * TP;
@@ -149,6 +153,10 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
       load_row_buf<BF, D>(tt.fo[pb], rf, i * rsb, so, j);
       const float l = bld32(rl, 4 * i, 4 * (tb + 16 * pb));
       tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
+      if constexpr (PM) {
+        tt.ct[pb][0] = bld32(rc, 8 * i, 8 * (tb + 16 * pb));
+        tt.ct[pb][1] = bld32(rc, 8 * i + 4, 8 * (tb + 16 * pb));
+      }
     }
   };
   pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_BWD_B), Tile>(ntile, load_tile, [&](Tile& cur, int t) {
@@ -195,6 +203,13 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
     // per point (column of the tile): c = sum_g w dw, the softmax correction, and
     // tb = sum_g w t, the weighted mean of the shifted base-2 logits t = a2 - lse2
     float cc[PB], tb[PB];
+    if constexpr (PM) {
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        cc[pb] = cur.ct[pb][0];
+        tb[pb] = cur.ct[pb][1];
+      }
+    } else {
 #pragma unroll
     for (int pb = 0; pb < PB; ++pb) {
       float sum = 0.f, st = 0.f;
@@ -228,6 +243,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
         tb[pb] = st;
       }
     }
+    }
     // da = w (dw - c); dbias partials; dtau partial (App. F.2): sum_g da a = sum_g da (a - k)
     // for any per-point k because sum_g da = 0; with k = lse + tb the first-order effect of
     // the rounding of c on the sum cancels (sum_g w (t - tb) = 0).
@@ -244,6 +260,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
           dbacc[gb][r] += da;
         }
     dtacc += (double)dts;
+    if constexpr (!PM) {
     // dfx = w dU, dx = da W_s^T / tau (contractions over this wave's slots)
     f4 gf[VB][PB], gx_[DB][PB];
     {
@@ -292,6 +309,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
           bst_row4<BF>(rdf, gf[cb][pb], vo, so);
           bst_row4<BF>(rdx, gx_[cb][pb], vo, so);
         }
+    }
     }
     // dW_s += X^T da over the tile's points: da goes through LDS to put points on the k index.
     if constexpr (!BF) {
@@ -362,7 +380,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   __shared__ double dtw[NS * NP];
   if (lane == 0) dtw[wave] = dt;
 
-  float* pp = a.part + ((int64_t)c.bh * a.chunks + c.chunk) * ((int64_t)D * a.G + a.G + 2);
+  float* pp = a.part + ((int64_t)c.bh * a.chunks + c.chunk) * ((int64_t)D * a.G + a.G + 2 * a.nblk);
   if constexpr (NP > 1) {
     __shared__ f4 red[NP - 1][NS][DB][GB][64];
     __shared__ float redb[NP - 1][NS][GB][4][16];
@@ -407,23 +425,35 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
     double s = 0.0;
     for (int q = 0; q < NS * NP; ++q) s += dtw[q];
     // (D * G + G) is even, so this slot is 8-byte aligned
-    *reinterpret_cast<double*>(pp + (int64_t)D * a.G + a.G) = -s * (double)kLn2 * (double)inv_tau;
+    *reinterpret_cast<double*>(pp + (int64_t)D * a.G + a.G + 2 * c.blk) =
+        -s * (double)kLn2 * (double)inv_tau;
   }
 }
 
-template <bool BF, int D, int GS, int NS, int NP, int PB>
-struct Run_k_bwd_b {
-  static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
-    dim3 grid(cfg.chunks * BH);
-    hipLaunchKernelGGL((k_bwd_b<BF, D, GS, NS, NP, PB>), grid, dim3(64 * NS * NP), 0, st, a);
-    return hipGetLastError();
-  }
+template <bool PM>
+struct Run_k_bwd_b_ {
+  template <bool BF, int D, int GS, int NS, int NP, int PB>
+  struct R {
+    static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
+      if constexpr (PM && NS != 1) {  // the parameter half of the blocked family is slot-owned
+        return hipErrorInvalidConfiguration;
+      } else {
+        dim3 grid(cfg.chunks * BH * cfg.nblk);
+        hipLaunchKernelGGL((k_bwd_b<BF, D, GS, NS, NP, PB, PM>), grid, dim3(64 * NS * NP), 0, st, a);
+        return hipGetLastError();
+      }
+    }
+  };
 };
 
 }  // namespace
 
 hipError_t run_pass_bwd_b(const Geom& g, const PassArgs& a, hipStream_t st) {
-  return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b>(g, a, st);
+  return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<false>::R>(g, a, st);
+}
+
+hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, hipStream_t st) {
+  return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<true>::R>(g, a, st);
 }
 
 }  // namespace fs

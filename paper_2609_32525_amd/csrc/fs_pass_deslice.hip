@@ -109,7 +109,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 template <bool BF, int D, int GS, int NS, int NP, int PB>
 struct Run_k_deslice {
   static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
-    dim3 grid(cfg.chunks * BH);
+    dim3 grid(cfg.chunks * BH * cfg.nblk);
     hipLaunchKernelGGL((k_deslice<BF, D, GS, NS, NP>), grid, dim3(64 * NS * NP), 0, st, a);
     return hipGetLastError();
   }

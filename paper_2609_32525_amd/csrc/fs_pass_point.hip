@@ -1,0 +1,319 @@
+// Point-owned pass of the slot-blocked backward (large G): for every point, with the slots
+// streamed in blocks of 64,
+//   c  = sum_g w dw          (the softmax correction; dw = dout zmix^T + F dU^T + ds)
+//   tb = sum_g w t           (weighted mean of the shifted base-2 logits, for dtau)
+//   dfx = sum_g w dU
+//   dx  = sum_g w (dw - c) W_s[:, g] / tau = (P - c Q) / tau,
+//         P = sum_g (w dw) W_s[:, g] / tau,  Q = sum_g w W_s[:, g] / tau
+// The last identity lets dx be accumulated in the same sweep over the slot blocks, before c
+// is known (paper: App. F.1, "G-blocked kernels": a point-owned backward kernel; here one
+// sweep instead of two). The slot-owned parameter pass then reads (c, tb) per point.
+//
+// The per-head operands (W_s, zmix, dU, bias, ds) are far too large at large G to stay in
+// registers, so each block's MFMA operand images are built once per workgroup in LDS, double
+// buffered: while the wavefronts compute block k from one buffer, each of them has already
+// issued the global loads for its share of block k + 1 and writes it to the other buffer
+// afterwards. Every wavefront owns one 32-point tile per step and reads the images it needs.
+// dw uses the same centred operands as the fused pass B (zmix, dU and ds minus their
+// mass-weighted slot means), so c is consistent with the parameter pass. bf16 storage rounds
+// the B operands of P and Q in two bf16 parts (w dw and w vary over many orders of magnitude
+// and P - c Q cancels).
+
+#include "fs_stream.h"
+
+namespace fs {
+namespace {
+
+constexpr int kHS = 32;  // slots per half block: operands are imaged per half (GB = 2)
+
+template <bool BF, int D>
+struct PointImages {
+  static constexpr int GBH = kHS / 16;
+  static constexpr int VB = D / 16;
+  using SOp = SlotOp<BF, D, GBH>;
+  using UOp = GOp<BF, GBH, VB>;
+  // bf16 dw operands use only the high part of a SlotOp
+  static constexpr int kW = lds_chunks<SOp>();
+  static constexpr int kZ = BF ? lds_chunks<SOp>() / 2 : lds_chunks<SOp>();
+  static constexpr int kU = lds_chunks<UOp>();
+  // per half: W (logits), zv, uv (dw), ug (dfx), wg (P, Q); then bias and ds of the block
+  static constexpr int kHalf = kW + 2 * kZ + 2 * kU;
+  static constexpr int kChunks = 2 * kHalf + 2 * 64 / 4;  // + bS[64], dsS[64] as uint4
+};
+
+// The first nchunks 16-byte chunks of a per-lane operand (its register image), per lane.
+
+template <class Op>
+__device__ __forceinline__ void put_first(const Op& o, uint4* base, int lane, int nchunks) {
+  const uint4* src = reinterpret_cast<const uint4*>(&o);
+#pragma unroll
+  for (int q = 0; q < nchunks; ++q) base[q * 64 + lane] = src[q];
+}
+template <class Op>
+__device__ __forceinline__ void get_first(Op& o, const uint4* base, int lane, int nchunks) {
+  uint4* dst = reinterpret_cast<uint4*>(&o);
+#pragma unroll
+  for (int q = 0; q < nchunks; ++q) dst[q] = base[q * 64 + lane];
+}
+
+// Contraction over a half block's 32 slots with the B operand (a T-layout tile) rounded in two
+// bf16 parts for bf16 storage: acc += M^T (hi + lo).
+template <bool BF, int GBH, int CB>
+__device__ __forceinline__ f4 mm_gop_split(const GOp<BF, GBH, CB>& o, int cb, const f4 (*t)[2],
+                                           int pb, f4 acc) {
+  if constexpr (!BF) {
+    return mm_gop_tile<false, GBH, CB, 2>(o, cb, t, pb, acc);
+  } else {
+#pragma unroll
+    for (int q = 0; q < GBH / 2; ++q) {
+      bf8 hi, lo;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float v = t[2 * q + e / 4][pb][e % 4];
+        const __bf16 h = (__bf16)v;
+        hi[e] = h;
+        lo[e] = (__bf16)(v - (float)h);
+      }
+      acc = mfma_bf16(o.v[q][cb], hi, acc);
+      acc = mfma_bf16(o.v[q][cb], lo, acc);
+    }
+    return acc;
+  }
+}
+
+template <bool BF, int D, int NW>
+__global__ __launch_bounds__(64 * NW) void k_point(PassArgs a) {
+  using IM = PointImages<BF, D>;
+  using SOp = typename IM::SOp;
+  using UOp = typename IM::UOp;
+  constexpr int GBH = IM::GBH, VB = IM::VB, DB = D / 16;
+  constexpr bool SPLIT = BF;
+  using T = typename Store<BF>::T;
+  const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
+  const int wave = threadIdx.x >> 6;
+  const int wpu = __builtin_amdgcn_readfirstlane(wave);
+  const HeadCtx c = head_ctx<D>(a, 0, 0);
+  const int64_t rs = (int64_t)a.H * D;
+  const T* xb = (const T*)a.x + c.off;
+  const T* fb = (const T*)a.fx + c.off;
+  const T* gb_ = (const T*)a.dout + c.off;
+  T* dxb = (T*)a.out + c.off;
+  T* dfb = (T*)a.out2 + c.off;
+  const float* lse = a.lse_in + (int64_t)c.bh * a.N;
+  const float inv_tau = 1.0f / a.tau[c.h];
+  const float* zm = a.zmix + (int64_t)c.bh * a.G * D;
+  const float* dU = a.dU + (int64_t)c.bh * a.G * D;
+  const float* dsv = a.ds + (int64_t)c.bh * a.G;
+  const float* cen = a.cen + (int64_t)c.bh * (2 * D + 1);
+  const int NB = a.G / 64;
+
+  __shared__ uint4 img[2][IM::kChunks];
+
+  // ---- staging: job q of a block (q < 11) is built by wavefront q % NW ----------------------
+  // jobs 0..9: (half h = q / 5, kind q % 5) with kinds W, zv, uv, ug, wg; job 10: bias, ds.
+  // A wavefront's jobs are loaded into registers (load_jobs), then written (put_jobs).
+  constexpr int kJobs = 11;
+  constexpr int kMyJobs = (kJobs + NW - 1) / NW;
+  union JobRegs {  // a wavefront's job holds one operand image, or the bias and ds values
+    SOp s;
+    UOp u;
+    float bd[2];
+  };
+  JobRegs jr[kMyJobs];
+  auto half_base = [&](int h) { return h * IM::kHalf; };
+  auto load_jobs = [&](int blk) {
+    const int g0 = blk * 64;
+#pragma unroll
+    for (int k = 0; k < kMyJobs; ++k) {
+      const int q = wpu + k * NW;
+      if (q < 10) {
+        const int h = q / 5, kind = q % 5, gh = g0 + kHS * h;
+        if (kind == 0) load_slotop<BF, D, GBH, true, SPLIT>(jr[k].s, c.W, a.G, gh, c.sc, i, j);
+        if (kind == 1) load_slotop<BF, D, GBH, false, false>(jr[k].s, zm, D, gh, 1.0f, i, j, cen);
+        if (kind == 2) load_slotop<BF, D, GBH, false, false>(jr[k].s, dU, D, gh, 1.0f, i, j, cen + D);
+        if (kind == 3) load_gop<BF, GBH, VB, false>(jr[k].u, dU, D, gh, 1.0f, i, j);
+        if (kind == 4) load_gop<BF, GBH, DB, true>(jr[k].u, c.W, a.G, gh, inv_tau, i, j);
+      } else if (q == 10) {
+        jr[k].bd[0] = c.sc * c.bias[g0 + lane];
+        jr[k].bd[1] = dsv[g0 + lane] - cen[2 * D];
+      }
+    }
+  };
+  auto put_jobs = [&](uint4* buf) {
+#pragma unroll
+    for (int k = 0; k < kMyJobs; ++k) {
+      const int q = wpu + k * NW;
+      if (q < 10) {
+        const int h = q / 5, kind = q % 5;
+        uint4* hb = buf + half_base(h);
+        if (kind == 0) put_first(jr[k].s, hb, lane, IM::kW / 64);
+        if (kind == 1) put_first(jr[k].s, hb + IM::kW, lane, IM::kZ / 64);
+        if (kind == 2) put_first(jr[k].s, hb + IM::kW + IM::kZ, lane, IM::kZ / 64);
+        if (kind == 3) put_first(jr[k].u, hb + IM::kW + 2 * IM::kZ, lane, IM::kU / 64);
+        if (kind == 4) put_first(jr[k].u, hb + IM::kW + 2 * IM::kZ + IM::kU, lane, IM::kU / 64);
+      } else if (q == 10) {
+        float* f = reinterpret_cast<float*>(buf + 2 * IM::kHalf);
+        f[lane] = jr[k].bd[0];
+        f[64 + lane] = jr[k].bd[1];
+      }
+    }
+  };
+
+  const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
+  const int64_t pend = min(a.N, pbeg + a.chunk_pts);
+  const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
+  const int nstep = (npts + 32 * NW - 1) / (32 * NW);
+  const int rsb = (int)(rs * sizeof(T));
+  const auto rx = rows_rsrc(xb + pbeg * rs, npts, (int)rs, D);
+  const auto rf = rows_rsrc(fb + pbeg * rs, npts, (int)rs, D);
+  const auto rg = rows_rsrc(gb_ + pbeg * rs, npts, (int)rs, D);
+  const auto rdx = rows_rsrc(dxb + pbeg * rs, npts, (int)rs, D);
+  const auto rdf = rows_rsrc(dfb + pbeg * rs, npts, (int)rs, D);
+  const auto rl = rows_rsrc(lse + pbeg, npts, 1, 1);
+  const auto rc = rows_rsrc(a.cpt_out + ((int64_t)c.bh * a.N + pbeg) * 2, npts, 2, 2);
+
+  if (nstep == 0) return;  // uniform over the workgroup
+  load_jobs(0);
+  put_jobs(img[0]);
+  __syncthreads();
+
+  int kbuf = 0;
+  for (int step = 0; step < nstep; ++step) {
+    const int tp0 = (step * NW + wpu) * 32;
+    RowOp<BF, D> xo[2], go[2], fo[2];
+    float lse2[2];
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      const int so = (tp0 + 16 * pb) * rsb;
+      load_row_buf<BF, D>(xo[pb], rx, i * rsb, so, j);
+      load_row_buf<BF, D>(go[pb], rg, i * rsb, so, j);
+      load_row_buf<BF, D>(fo[pb], rf, i * rsb, so, j);
+      const float l = bld32(rl, 4 * i, 4 * (tp0 + 16 * pb));
+      lse2[pb] = tp0 + 16 * pb + i < npts ? l : kMasked;
+    }
+    f4 gf[VB][2], P[DB][2], Q[DB][2];
+    float csum[2] = {0.f, 0.f}, tsum[2] = {0.f, 0.f};
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+#pragma unroll
+      for (int vb = 0; vb < VB; ++vb) gf[vb][pb] = zero4();
+#pragma unroll
+      for (int d = 0; d < DB; ++d) P[d][pb] = Q[d][pb] = zero4();
+    }
+
+    for (int blk = 0; blk < NB; ++blk) {
+      // global loads of the next block's share (block 0 of the next step after the last)
+      const bool more = blk + 1 < NB || step + 1 < nstep;
+      if (more) load_jobs(blk + 1 < NB ? blk + 1 : 0);
+      const uint4* cb = img[kbuf];
+      const float* bS = reinterpret_cast<const float*>(cb + 2 * IM::kHalf);
+#pragma unroll 1
+      for (int h = 0; h < 2; ++h) {
+        const uint4* hb = cb + half_base(h);
+        // T-layout tiles: rows = slots 32 h + 16 gb + 4 j + r of the block, cols = points
+        f4 w[GBH][2], dw[GBH][2];
+        {
+          SOp wop;
+          lds_get(wop, hb, lane);
+#pragma unroll
+          for (int gb = 0; gb < GBH; ++gb) {
+            const f4 bT = *reinterpret_cast<const f4*>(bS + kHS * h + 16 * gb + 4 * j);
+#pragma unroll
+            for (int pb = 0; pb < 2; ++pb) {
+              f4 acc = mm_slot_row<BF, D, GBH, SPLIT>(wop, gb, xo[pb], bT);
+              f4 ww;
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const float t = acc[r] - lse2[pb];
+                ww[r] = __builtin_amdgcn_exp2f(t);
+                tsum[pb] += ww[r] * t;
+              }
+              w[gb][pb] = ww;
+            }
+          }
+        }
+        {
+          SOp zv, uv;
+          get_first(zv, hb + IM::kW, lane, IM::kZ / 64);
+          get_first(uv, hb + IM::kW + IM::kZ, lane, IM::kZ / 64);
+#pragma unroll
+          for (int gb = 0; gb < GBH; ++gb) {
+            const f4 dsT = *reinterpret_cast<const f4*>(bS + 64 + kHS * h + 16 * gb + 4 * j);
+#pragma unroll
+            for (int pb = 0; pb < 2; ++pb) {
+              f4 g = dsT;
+              g = mm_slot_row<BF, D, GBH, false>(zv, gb, go[pb], g);
+              g = mm_slot_row<BF, D, GBH, false>(uv, gb, fo[pb], g);
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                g[r] *= w[gb][pb][r];  // w dw
+                csum[pb] += g[r];
+              }
+              dw[gb][pb] = g;
+            }
+          }
+        }
+        {
+          UOp ug, wg;
+          lds_get(ug, hb + IM::kW + 2 * IM::kZ, lane);
+          lds_get(wg, hb + IM::kW + 2 * IM::kZ + IM::kU, lane);
+#pragma unroll
+          for (int pb = 0; pb < 2; ++pb) {
+#pragma unroll
+            for (int vb = 0; vb < VB; ++vb)
+              gf[vb][pb] = mm_gop_tile<BF, GBH, VB, 2>(ug, vb, w, pb, gf[vb][pb]);
+#pragma unroll
+            for (int d = 0; d < DB; ++d) {
+              P[d][pb] = mm_gop_split<BF, GBH, DB>(wg, d, dw, pb, P[d][pb]);
+              Q[d][pb] = mm_gop_split<BF, GBH, DB>(wg, d, w, pb, Q[d][pb]);
+            }
+          }
+        }
+      }
+      if (more) put_jobs(img[kbuf ^ 1]);
+      __syncthreads();
+      kbuf ^= 1;
+    }
+
+    // per point: c and tb over the four lane rows; dx = P - c Q; stores
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      const float cc = col4_sum(csum[pb]);
+      const float tb = col4_sum(tsum[pb]);
+      const int so = (tp0 + 16 * pb) * rsb;
+#pragma unroll
+      for (int vb = 0; vb < VB; ++vb)
+        bst_row4<BF>(rdf, gf[vb][pb], i * rsb + (16 * vb + 4 * j) * (int)sizeof(T), so);
+#pragma unroll
+      for (int d = 0; d < DB; ++d) {
+        f4 v;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = P[d][pb][r] - cc * Q[d][pb][r];
+        bst_row4<BF>(rdx, v, i * rsb + (16 * d + 4 * j) * (int)sizeof(T), so);
+      }
+      if (j == 0) {
+        bst32(rc, cc, 8 * i, 8 * (tp0 + 16 * pb));
+        bst32(rc, tb, 8 * i + 4, 8 * (tp0 + 16 * pb));
+      }
+      csum[pb] = tsum[pb] = 0.f;
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t run_pass_point(const Geom& g, const PassArgs& a, hipStream_t st) {
+  const PassCfg cfg = pick_cfg(g, PASS_POINT);
+  if (cfg.NP != 8 || g.D > 32) return hipErrorInvalidConfiguration;
+  const dim3 grid(cfg.chunks * g.BH()), block(64 * 8);
+  if (g.bf16) {
+    if (g.D == 16) hipLaunchKernelGGL((k_point<true, 16, 8>), grid, block, 0, st, a);
+    if (g.D == 32) hipLaunchKernelGGL((k_point<true, 32, 8>), grid, block, 0, st, a);
+  } else {
+    if (g.D == 16) hipLaunchKernelGGL((k_point<false, 16, 8>), grid, block, 0, st, a);
+    if (g.D == 32) hipLaunchKernelGGL((k_point<false, 32, 8>), grid, block, 0, st, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace fs

@@ -1,4 +1,5 @@
-// Streaming pass: slice (logits, per-point softmax, U += w^T F, s += sum w, lse).
+// Streaming pass: slice (logits, per-point softmax, U += w^T F, s += sum w, lse), and the
+// statistics pass of the slot-blocked family (the same softmax statistics, lse only).
 // Kernel design and MFMA lane layouts are described at the top of fs_stream.h.
 
 #include "fs_stream.h"
@@ -9,7 +10,8 @@ namespace {
 // =======================================================================================
 // Slice pass
 // =======================================================================================
-template <bool BF, int D, int GS, int NS, int NP>
+// ST: statistics only (lse), no token accumulation.
+template <bool BF, int D, int GS, int NS, int NP, bool ST>
 __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_SLICE))) void k_slice(
     PassArgs a) {
   constexpr int GB = GS / 16, VB = D / 16;
@@ -53,13 +55,13 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 
   struct Tile {
     RowOp<BF, D> xo[2];
-    PtGather<BF, VB> f;
+    PtGather<BF, ST ? 1 : VB> f;
   };
   auto load_tile = [&](Tile& tt, int t) {
     const int tbo = (t * NP + wpu) * 32 * rsb;
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) load_row_buf<BF, D>(tt.xo[pb], rx, i * rsb, tbo + 16 * pb * rsb, j);
-    gather_points_buf<BF, VB>(tt.f, rf, rsb, tbo, i, j);
+    if constexpr (!ST) gather_points_buf<BF, VB>(tt.f, rf, rsb, tbo, i, j);
   };
   pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_SLICE), Tile>(ntile, load_tile, [&](Tile& cur, int t) {
     const int tb = (t * NP + wpu) * 32;
@@ -112,18 +114,22 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
           }
       }
       __syncthreads();
+      // lane p < 32 combines the slot groups' statistics of point p, then every lane fetches
+      // the combined values of its own rows
+      float Mp = st_m[par][wp][0][lane & 31];
+#pragma unroll
+      for (int s = 1; s < NS; ++s) Mp = vmax(Mp, st_m[par][wp][s][lane & 31]);
+      float Lp = 0.f;
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+        Lp += st_l[par][wp][s][lane & 31] * __builtin_amdgcn_exp2f(st_m[par][wp][s][lane & 31] - Mp);
 #pragma unroll
       for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int q = 16 * pb + 4 * j + r;
-          float M = st_m[par][wp][0][q];
-#pragma unroll
-          for (int s = 1; s < NS; ++s) M = vmax(M, st_m[par][wp][s][q]);
-          float L = 0.f;
-#pragma unroll
-          for (int s = 0; s < NS; ++s)
-            L += st_l[par][wp][s][q] * __builtin_amdgcn_exp2f(st_m[par][wp][s][q] - M);
+          const float M = __shfl(Mp, q);
+          const float L = __shfl(Lp, q);
           f[pb][r] = __builtin_amdgcn_exp2f(m[pb][r] - M) * __builtin_amdgcn_rcpf(L);
           lse2[pb][r] = M + __log2f(L);
         }
@@ -139,6 +145,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
         for (int gb = 0; gb < GB; ++gb) w[pb][gb][r] *= fr;
         if (want_lse && ws == 0 && i == 0) bst32(rl, lse2[pb][r], 4 * q, 4 * tb);
       }
+    if constexpr (ST) return;
 #pragma unroll
     for (int gb = 0; gb < GB; ++gb) {
       float sum = 0.f;
@@ -148,8 +155,9 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
         for (int r = 0; r < 4; ++r) sum += w[pb][gb][r];
       sacc[gb] += sum;
     }
-    mm_points<BF, GB, VB>(U, w, cur.f);
+    if constexpr (!ST) mm_points<BF, GB, VB>(U, w, cur.f);
   });
+  if constexpr (ST) return;
 
   // ---- combine the NP point groups and write this workgroup's partials --------------------
 #pragma unroll
@@ -191,19 +199,26 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   }
 }
 
-template <bool BF, int D, int GS, int NS, int NP, int PB>
-struct Run_k_slice {
-  static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
-    dim3 grid(cfg.chunks * BH);
-    hipLaunchKernelGGL((k_slice<BF, D, GS, NS, NP>), grid, dim3(64 * NS * NP), 0, st, a);
-    return hipGetLastError();
-  }
+template <bool ST>
+struct Run_k_slice_ {
+  template <bool BF, int D, int GS, int NS, int NP, int PB>
+  struct R {
+    static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
+      dim3 grid(cfg.chunks * BH * cfg.nblk);
+      hipLaunchKernelGGL((k_slice<BF, D, GS, NS, NP, ST>), grid, dim3(64 * NS * NP), 0, st, a);
+      return hipGetLastError();
+    }
+  };
 };
 
 }  // namespace
 
 hipError_t run_pass_slice(const Geom& g, const PassArgs& a, hipStream_t st) {
-  return run_pass_tilings<PASS_SLICE, Run_k_slice>(g, a, st);
+  return run_pass_tilings<PASS_SLICE, Run_k_slice_<false>::R>(g, a, st);
+}
+
+hipError_t run_pass_stats(const Geom& g, const PassArgs& a, hipStream_t st) {
+  return run_pass_tilings<PASS_STATS, Run_k_slice_<true>::R>(g, a, st);
 }
 
 }  // namespace fs

@@ -590,21 +590,24 @@ __device__ __forceinline__ void pipeline(int ntile, Load&& load, Body&& body) {
 #define FS_WPE_BWD_B 1
 #endif
 
-// Workgroup -> (chunk, b*H+h): a 1-D grid of chunks * BH workgroups, chunks of one head
-// consecutive. (Ordering the workgroups per XCD so that the heads of one chunk share an L2
+// Workgroup -> (chunk, slot block, b*H+h): a 1-D grid of chunks * nblk * BH workgroups,
+// chunks of one (head, slot block) consecutive. (Ordering the workgroups per XCD so that the heads of one chunk share an L2
 // measured no faster.)
 struct BlockPos {
-  int chunk, bh;
+  int chunk, blk, bh;
 };
 __device__ __forceinline__ BlockPos block_pos(const PassArgs& a) {
   BlockPos p;
-  p.chunk = blockIdx.x % a.chunks;
-  p.bh = blockIdx.x / a.chunks;
+  const int L = blockIdx.x;
+  p.chunk = L % a.chunks;
+  const int r = L / a.chunks;
+  p.blk = r % a.nblk;
+  p.bh = r / a.nblk;
   return p;
 }
 
 struct HeadCtx {
-  int chunk;
+  int chunk, blk;
   int bh, b, h, g0;
   float sc;  // log2(e) / tau_h
   const float* W;
@@ -617,10 +620,11 @@ __device__ __forceinline__ HeadCtx head_ctx(const PassArgs& a, int ws, int GS) {
   HeadCtx c;
   const BlockPos bp = block_pos(a);
   c.chunk = bp.chunk;
+  c.blk = bp.blk;
   c.bh = bp.bh;
   c.b = c.bh / a.H;
   c.h = c.bh % a.H;
-  c.g0 = ws * GS;
+  c.g0 = (bp.blk + ws) * GS;  // nblk > 1 only with one slot group per tile
   c.sc = kLog2e / a.tau[c.h];
   c.W = a.Ws + (a.ws_per_head ? (int64_t)c.h * D * a.G : 0);
   c.bias = a.bias + (a.ws_per_head ? (int64_t)c.h * a.G : 0);

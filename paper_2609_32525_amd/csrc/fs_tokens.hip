@@ -164,10 +164,11 @@ __global__ __launch_bounds__(kRedThreads) void k_reduce_mixparams(const float* p
 // blockIdx.y is the head for per-head outputs (rows: b = 0..B-1, chunk), else 0 with rows
 // over every (b, h, chunk); blocks whose segment has fewer heads return at once.
 __global__ __launch_bounds__(kRedThreads) void k_reduce_params(
-    const float* part, float* dWs, float* dbias, float* dtau, int B, int H, int chunks, int D,
-    int G, int per_head, const float* partM, float* dmix, int64_t mix_len, int mix_per_head) {
+    const float* part, float* dWs, float* dbias, float* dtau, int B, int H, int chunks,
+    int nblk, int D, int G, int per_head, const float* partM, float* dmix, int64_t mix_len,
+    int mix_per_head) {
   __shared__ float red[kRowGroupsWide][kColsWide];
-  const int64_t len = (int64_t)D * G + G + 2;
+  const int64_t len = (int64_t)D * G + G + 2LL * nblk;
   const int64_t ncol = (int64_t)D * G + G;
   const int nbp = (int)((ncol + kColsWide - 1) / kColsWide);
   const int hh = blockIdx.y;
@@ -180,15 +181,17 @@ __global__ __launch_bounds__(kRedThreads) void k_reduce_params(
   if (!per_head && hh > 0) return;
   if ((int)blockIdx.x == nbp) {
     // dtau: one wavefront per head; lane l sums the fp64 partials l, l + 64, ... of the
-    // head's (b, chunk) rows in order, then a butterfly over the 64 lanes (fixed pairing)
+    // head's (b, chunk, slot block) entries in order, then a butterfly over the 64 lanes
+    // (fixed pairing)
     if (hh == 0) {
       const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-      const int rows = B * chunks;
+      const int rows = B * chunks * nblk;
       for (int h = wave; h < H; h += nw) {
         double t = 0.0;
         for (int r = lane; r < rows; r += 64) {
-          const int b = r / chunks, q = r % chunks;
-          t += *reinterpret_cast<const double*>(part + ((int64_t)(b * H + h) * chunks + q) * len + ncol);
+          const int b = r / (chunks * nblk), q = (r / nblk) % chunks, k = r % nblk;
+          t += *reinterpret_cast<const double*>(part + ((int64_t)(b * H + h) * chunks + q) * len +
+                                                ncol + 2 * k);
         }
 #pragma unroll
         for (int off = 1; off < 64; off <<= 1) t += __shfl_xor(t, off);
@@ -768,8 +771,8 @@ hipError_t launch_reduce_rows(const Geom& g, const float* part, float* out, int 
 }
 
 hipError_t launch_reduce_params(const Geom& g, const float* part, float* dWs, float* dbias,
-                                float* dtau, int chunks, const MixArgs* m, const float* partM,
-                                float* dmix, hipStream_t st) {
+                                float* dtau, int chunks, int nblk, const MixArgs* m,
+                                const float* partM, float* dmix, hipStream_t st) {
   const int64_t ncol = (int64_t)g.D * g.G + g.G;
   const bool with_mix = m != nullptr && dmix != nullptr && m->kind != 0;
   const int64_t mix_len = with_mix ? mix_partial_len(g, m->kind) : 0;
@@ -777,7 +780,7 @@ hipError_t launch_reduce_params(const Geom& g, const float* part, float* dWs, fl
   const unsigned nb = blocks(ncol, kColsWide) + 1 + (with_mix ? blocks(mix_len, kColsWide) : 0);
   const int heads = std::max(g.ws_per_head ? g.H : 1, mix_per_head ? g.H : 1);
   hipLaunchKernelGGL(k_reduce_params, dim3(nb, heads), dim3(kRedThreads), 0, st, part, dWs,
-                     dbias, dtau, (int)g.B, g.H, chunks, g.D, g.G, g.ws_per_head ? 1 : 0, partM,
+                     dbias, dtau, (int)g.B, g.H, chunks, nblk, g.D, g.G, g.ws_per_head ? 1 : 0, partM,
                      with_mix ? dmix : nullptr, mix_len, mix_per_head ? 1 : 0);
   return hipGetLastError();
 }
