@@ -154,6 +154,8 @@ BwdWs bwd_ws_layout(const Geom& g, int kind) {
   off += up(kind == FS_MIX_ATTN ? 3 * tok + sizeof(float) * (size_t)g.BH() * g.G * g.G : 0);
   L.cpt = off;
   off += up(blocked(g) ? 2 * sizeof(float) * (size_t)g.BH() * (size_t)g.N : 0);
+  L.img = off;
+  off += up(blocked(g) ? point_image_bytes(g) : 0);
   L.total = off;
   return L;
 }

@@ -74,6 +74,7 @@ struct PassArgs {
   float* lse_out;
   float* part;   // slice: U partials; bwd_a: dzmix partials; bwd_b: parameter partials
   float* part2;  // slice: s partials
+  const void* img;   // point-owned pass: per-(b, h) operand images of the slot blocks
   const float* cpt;  // blocked bwd_b: per point (c, tb) from the point-owned pass
   float* cpt_out;    // point-owned pass: per point (c, tb), [BH][N][2]
   int64_t N;
@@ -94,6 +95,7 @@ hipError_t run_pass_bwd_b(const Geom& g, const PassArgs& a, hipStream_t st);
 hipError_t run_pass_stats(const Geom& g, const PassArgs& a, hipStream_t st);
 hipError_t run_pass_slice_blk(const Geom& g, const PassArgs& a, hipStream_t st);
 hipError_t run_pass_point(const Geom& g, const PassArgs& a, hipStream_t st);
+size_t point_image_bytes(const Geom& g);  // workspace of the point-owned pass's operand images
 hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, hipStream_t st);
 
 // Per-thread measurement events recorded around the streaming passes (fs_set_pass_events).
@@ -108,7 +110,7 @@ struct FwdWs {
   size_t partU, partS, lse, total;  // lse: [BH][N] when the blocked family needs it
 };
 struct BwdWs {
-  size_t partDZ, dzm, dz, dU, ds, cen, partP, partM, scr, cpt, total;
+  size_t partDZ, dzm, dz, dU, ds, cen, partP, partM, scr, cpt, img, total;
 };
 // Floats of one parameter partial of backward pass B: [D G] dW_s, [G] dbias, then one fp64
 // dtau partial per slot block.

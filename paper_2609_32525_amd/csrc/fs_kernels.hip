@@ -158,6 +158,7 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
     pa.cen = cen;
     pa.lse_in = lse;
     pa.cpt_out = reinterpret_cast<float*>(ws + L.cpt);
+    pa.img = ws + L.img;
     b.cpt = pa.cpt_out;
     e = timed(PASS_BWD_B, st, [&] {
       hipError_t e1 = run_pass_point(g, pa, st);

@@ -39,6 +39,9 @@ struct PointImages {
   // per half: W (logits), zv, uv (dw), ug (dfx), wg (P, Q); then bias and ds of the block
   static constexpr int kHalf = kW + 2 * kZ + 2 * kU;
   static constexpr int kChunks = 2 * kHalf + 2 * 64 / 4;  // + bS[64], dsS[64] as uint4
+  // stride of one block's image set, padded so that a 512-thread workgroup copies it in
+  // whole rounds
+  static constexpr int kStride = (kChunks + 511) / 512 * 512;
 };
 
 // The first nchunks 16-byte chunks of a per-lane operand (its register image), per lane.
@@ -54,6 +57,88 @@ __device__ __forceinline__ void get_first(Op& o, const uint4* base, int lane, in
   uint4* dst = reinterpret_cast<uint4*>(&o);
 #pragma unroll
   for (int q = 0; q < nchunks; ++q) dst[q] = base[q * 64 + lane];
+}
+
+// Builds job q (q < 11) of slot block blk's image set for one (b, h) into `out` (global or
+// LDS, same layout): jobs 0..9 are (half h = q / 5, kind q % 5) with kinds W (logits, scaled by
+// log2(e)/tau), zv and uv (centred zmix and dU for dw), ug (dU for dfx), wg (W^T / tau for P
+// and Q); job 10 is the block's scaled bias and centred ds. Called by a whole wavefront.
+template <bool BF, int D>
+__device__ __forceinline__ void build_job(int q, int blk, const HeadCtx& c, const PassArgs& a,
+                                          uint4* out, int lane) {
+  using IM = PointImages<BF, D>;
+  using SOp = typename IM::SOp;
+  using UOp = typename IM::UOp;
+  constexpr int GBH = IM::GBH, VB = IM::VB, DB = D / 16;
+  const int i = lane & 15, j = lane >> 4;
+  const float inv_tau = 1.0f / a.tau[c.h];
+  const float* zm = a.zmix + (int64_t)c.bh * a.G * D;
+  const float* dU = a.dU + (int64_t)c.bh * a.G * D;
+  const float* dsv = a.ds + (int64_t)c.bh * a.G;
+  const float* cen = a.cen + (int64_t)c.bh * (2 * D + 1);
+  const int g0 = blk * 64;
+  if (q < 10) {
+    const int h = q / 5, kind = q % 5, gh = g0 + kHS * h;
+    uint4* hb = out + h * IM::kHalf;
+    if (kind <= 2) {
+      SOp o;
+      if (kind == 0) load_slotop<BF, D, GBH, true, BF>(o, c.W, a.G, gh, c.sc, i, j);
+      if (kind == 1) load_slotop<BF, D, GBH, false, false>(o, zm, D, gh, 1.0f, i, j, cen);
+      if (kind == 2) load_slotop<BF, D, GBH, false, false>(o, dU, D, gh, 1.0f, i, j, cen + D);
+      if (kind == 0) put_first(o, hb, lane, IM::kW / 64);
+      if (kind == 1) put_first(o, hb + IM::kW, lane, IM::kZ / 64);
+      if (kind == 2) put_first(o, hb + IM::kW + IM::kZ, lane, IM::kZ / 64);
+    } else {
+      UOp o;
+      if (kind == 3) load_gop<BF, GBH, VB, false>(o, dU, D, gh, 1.0f, i, j);
+      if (kind == 4) load_gop<BF, GBH, DB, true>(o, c.W, a.G, gh, inv_tau, i, j);
+      put_first(o, hb + IM::kW + 2 * IM::kZ + (kind == 4 ? IM::kU : 0), lane, IM::kU / 64);
+    }
+  } else if (q == 10) {
+    float* f = reinterpret_cast<float*>(out + 2 * IM::kHalf);
+    f[lane] = c.sc * c.bias[g0 + lane];
+    f[64 + lane] = dsv[g0 + lane] - cen[2 * D];
+  }
+}
+
+// Image sets of every slot block of every (b, h), [BH][G / 64][kChunks] uint4: built once per
+// backward so that the point-owned pass only copies them. grid (G / 64) * BH, 11 wavefronts.
+template <bool BF, int D>
+__global__ __launch_bounds__(64 * 11) void k_point_images(PassArgs a, uint4* img) {
+  using IM = PointImages<BF, D>;
+  const int NB = a.G / 64;
+  const int blk = blockIdx.x % NB;
+  const int bh = blockIdx.x / NB;
+  HeadCtx c;
+  c.bh = bh;
+  c.b = bh / a.H;
+  c.h = bh % a.H;
+  c.sc = kLog2e / a.tau[c.h];
+  c.W = a.Ws + (a.ws_per_head ? (int64_t)c.h * D * a.G : 0);
+  c.bias = a.bias + (a.ws_per_head ? (int64_t)c.h * a.G : 0);
+  build_job<BF, D>(threadIdx.x >> 6, blk, c, a, img + ((int64_t)bh * NB + blk) * IM::kStride,
+                   threadIdx.x & 63);
+}
+
+// A thread's share of one block's image set on its way from global memory to LDS: chunks
+// t, t + NT, ... (compile-time recursion keeps every index constant, so it stays in registers).
+template <int N>
+struct Stage {
+  uint4 v[N];
+};
+template <int U, int N, int NT>
+__device__ __forceinline__ void stage_load(Stage<N>& s, const uint4* src) {
+  if constexpr (U < N) {
+    s.v[U] = src[threadIdx.x + U * NT];
+    stage_load<U + 1, N, NT>(s, src);
+  }
+}
+template <int U, int N, int NT>
+__device__ __forceinline__ void stage_put(const Stage<N>& s, uint4* dst) {
+  if constexpr (U < N) {
+    dst[threadIdx.x + U * NT] = s.v[U];
+    stage_put<U + 1, N, NT>(s, dst);
+  }
 }
 
 // Contraction over a half block's 32 slots with the B operand (a T-layout tile) rounded in two
@@ -82,7 +167,8 @@ __device__ __forceinline__ f4 mm_gop_split(const GOp<BF, GBH, CB>& o, int cb, co
 }
 
 template <bool BF, int D, int NW>
-__global__ __launch_bounds__(64 * NW) void k_point(PassArgs a) {
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_point(
+    PassArgs a) {
   using IM = PointImages<BF, D>;
   using SOp = typename IM::SOp;
   using UOp = typename IM::UOp;
@@ -100,64 +186,9 @@ __global__ __launch_bounds__(64 * NW) void k_point(PassArgs a) {
   T* dxb = (T*)a.out + c.off;
   T* dfb = (T*)a.out2 + c.off;
   const float* lse = a.lse_in + (int64_t)c.bh * a.N;
-  const float inv_tau = 1.0f / a.tau[c.h];
-  const float* zm = a.zmix + (int64_t)c.bh * a.G * D;
-  const float* dU = a.dU + (int64_t)c.bh * a.G * D;
-  const float* dsv = a.ds + (int64_t)c.bh * a.G;
-  const float* cen = a.cen + (int64_t)c.bh * (2 * D + 1);
   const int NB = a.G / 64;
 
-  __shared__ uint4 img[2][IM::kChunks];
-
-  // ---- staging: job q of a block (q < 11) is built by wavefront q % NW ----------------------
-  // jobs 0..9: (half h = q / 5, kind q % 5) with kinds W, zv, uv, ug, wg; job 10: bias, ds.
-  // A wavefront's jobs are loaded into registers (load_jobs), then written (put_jobs).
-  constexpr int kJobs = 11;
-  constexpr int kMyJobs = (kJobs + NW - 1) / NW;
-  union JobRegs {  // a wavefront's job holds one operand image, or the bias and ds values
-    SOp s;
-    UOp u;
-    float bd[2];
-  };
-  JobRegs jr[kMyJobs];
-  auto half_base = [&](int h) { return h * IM::kHalf; };
-  auto load_jobs = [&](int blk) {
-    const int g0 = blk * 64;
-#pragma unroll
-    for (int k = 0; k < kMyJobs; ++k) {
-      const int q = wpu + k * NW;
-      if (q < 10) {
-        const int h = q / 5, kind = q % 5, gh = g0 + kHS * h;
-        if (kind == 0) load_slotop<BF, D, GBH, true, SPLIT>(jr[k].s, c.W, a.G, gh, c.sc, i, j);
-        if (kind == 1) load_slotop<BF, D, GBH, false, false>(jr[k].s, zm, D, gh, 1.0f, i, j, cen);
-        if (kind == 2) load_slotop<BF, D, GBH, false, false>(jr[k].s, dU, D, gh, 1.0f, i, j, cen + D);
-        if (kind == 3) load_gop<BF, GBH, VB, false>(jr[k].u, dU, D, gh, 1.0f, i, j);
-        if (kind == 4) load_gop<BF, GBH, DB, true>(jr[k].u, c.W, a.G, gh, inv_tau, i, j);
-      } else if (q == 10) {
-        jr[k].bd[0] = c.sc * c.bias[g0 + lane];
-        jr[k].bd[1] = dsv[g0 + lane] - cen[2 * D];
-      }
-    }
-  };
-  auto put_jobs = [&](uint4* buf) {
-#pragma unroll
-    for (int k = 0; k < kMyJobs; ++k) {
-      const int q = wpu + k * NW;
-      if (q < 10) {
-        const int h = q / 5, kind = q % 5;
-        uint4* hb = buf + half_base(h);
-        if (kind == 0) put_first(jr[k].s, hb, lane, IM::kW / 64);
-        if (kind == 1) put_first(jr[k].s, hb + IM::kW, lane, IM::kZ / 64);
-        if (kind == 2) put_first(jr[k].s, hb + IM::kW + IM::kZ, lane, IM::kZ / 64);
-        if (kind == 3) put_first(jr[k].u, hb + IM::kW + 2 * IM::kZ, lane, IM::kU / 64);
-        if (kind == 4) put_first(jr[k].u, hb + IM::kW + 2 * IM::kZ + IM::kU, lane, IM::kU / 64);
-      } else if (q == 10) {
-        float* f = reinterpret_cast<float*>(buf + 2 * IM::kHalf);
-        f[lane] = jr[k].bd[0];
-        f[64 + lane] = jr[k].bd[1];
-      }
-    }
-  };
+  __shared__ uint4 img[2][IM::kStride];
 
   const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
@@ -172,9 +203,15 @@ __global__ __launch_bounds__(64 * NW) void k_point(PassArgs a) {
   const auto rl = rows_rsrc(lse + pbeg, npts, 1, 1);
   const auto rc = rows_rsrc(a.cpt_out + ((int64_t)c.bh * a.N + pbeg) * 2, npts, 2, 2);
 
+  // staging: thread t copies chunks t, t + 64 NW, ... of a block's image set
+  static_assert(IM::kStride % (64 * NW) == 0, "image stride must be whole copy rounds");
+  constexpr int kCopy = IM::kStride / (64 * NW);
+  const uint4* himg = static_cast<const uint4*>(a.img) + (int64_t)c.bh * NB * IM::kStride;
+  Stage<kCopy> stg;
+
   if (nstep == 0) return;  // uniform over the workgroup
-  load_jobs(0);
-  put_jobs(img[0]);
+  stage_load<0, kCopy, 64 * NW>(stg, himg);
+  stage_put<0, kCopy, 64 * NW>(stg, img[0]);
   __syncthreads();
 
   int kbuf = 0;
@@ -204,12 +241,14 @@ __global__ __launch_bounds__(64 * NW) void k_point(PassArgs a) {
     for (int blk = 0; blk < NB; ++blk) {
       // global loads of the next block's share (block 0 of the next step after the last)
       const bool more = blk + 1 < NB || step + 1 < nstep;
-      if (more) load_jobs(blk + 1 < NB ? blk + 1 : 0);
+      if (more)
+        stage_load<0, kCopy, 64 * NW>(
+            stg, himg + (int64_t)(blk + 1 < NB ? blk + 1 : 0) * IM::kStride);
       const uint4* cb = img[kbuf];
       const float* bS = reinterpret_cast<const float*>(cb + 2 * IM::kHalf);
 #pragma unroll 1
       for (int h = 0; h < 2; ++h) {
-        const uint4* hb = cb + half_base(h);
+        const uint4* hb = cb + h * IM::kHalf;
         // T-layout tiles: rows = slots 32 h + 16 gb + 4 j + r of the block, cols = points
         f4 w[GBH][2], dw[GBH][2];
         {
@@ -234,6 +273,10 @@ __global__ __launch_bounds__(64 * NW) void k_point(PassArgs a) {
         }
         {
           SOp zv, uv;
+          if constexpr (BF) {  // only the high parts are imaged; the low parts are unused
+            zv = SOp{};
+            uv = SOp{};
+          }
           get_first(zv, hb + IM::kW, lane, IM::kZ / 64);
           get_first(uv, hb + IM::kW + IM::kZ, lane, IM::kZ / 64);
 #pragma unroll
@@ -270,7 +313,7 @@ __global__ __launch_bounds__(64 * NW) void k_point(PassArgs a) {
           }
         }
       }
-      if (more) put_jobs(img[kbuf ^ 1]);
+      if (more) stage_put<0, kCopy, 64 * NW>(stg, img[kbuf ^ 1]);
       __syncthreads();
       kbuf ^= 1;
     }
@@ -302,18 +345,33 @@ __global__ __launch_bounds__(64 * NW) void k_point(PassArgs a) {
 
 }  // namespace
 
+size_t point_image_bytes(const Geom& g) {
+  if (g.D > 32) return 0;
+  const int ch = g.bf16 ? (g.D == 16 ? PointImages<true, 16>::kStride : PointImages<true, 32>::kStride)
+                        : (g.D == 16 ? PointImages<false, 16>::kStride : PointImages<false, 32>::kStride);
+  return (size_t)g.BH() * (g.G / 64) * ch * 16;
+}
+
 hipError_t run_pass_point(const Geom& g, const PassArgs& a, hipStream_t st) {
   const PassCfg cfg = pick_cfg(g, PASS_POINT);
   if (cfg.NP != 8 || g.D > 32) return hipErrorInvalidConfiguration;
+  uint4* img = static_cast<uint4*>(const_cast<void*>(a.img));
+  const dim3 igrid((g.G / 64) * g.BH()), iblock(64 * 11);
   const dim3 grid(cfg.chunks * g.BH()), block(64 * 8);
-  if (g.bf16) {
-    if (g.D == 16) hipLaunchKernelGGL((k_point<true, 16, 8>), grid, block, 0, st, a);
-    if (g.D == 32) hipLaunchKernelGGL((k_point<true, 32, 8>), grid, block, 0, st, a);
-  } else {
-    if (g.D == 16) hipLaunchKernelGGL((k_point<false, 16, 8>), grid, block, 0, st, a);
-    if (g.D == 32) hipLaunchKernelGGL((k_point<false, 32, 8>), grid, block, 0, st, a);
+#define FS_POINT(BF_, D_)                                                                \
+  {                                                                                      \
+    hipLaunchKernelGGL((k_point_images<BF_, D_>), igrid, iblock, 0, st, a, img);         \
+    hipError_t e = hipGetLastError();                                                    \
+    if (e != hipSuccess) return e;                                                       \
+    hipLaunchKernelGGL((k_point<BF_, D_, 8>), grid, block, 0, st, a);                    \
+    return hipGetLastError();                                                            \
   }
-  return hipGetLastError();
+  if (g.bf16 && g.D == 16) FS_POINT(true, 16)
+  if (g.bf16 && g.D == 32) FS_POINT(true, 32)
+  if (!g.bf16 && g.D == 16) FS_POINT(false, 16)
+  if (!g.bf16 && g.D == 32) FS_POINT(false, 32)
+#undef FS_POINT
+  return hipErrorInvalidConfiguration;
 }
 
 }  // namespace fs

@@ -19,7 +19,6 @@ constexpr int kCols = 64;          // columns per workgroup (chunk reductions)
 constexpr int kRowGroups = kRedThreads / kCols;
 constexpr int kColsWide = 16;      // long reductions (over samples, heads and chunks)
 constexpr int kRowGroupsWide = kRedThreads / kColsWide;
-constexpr int kAttnThreads = 1024;
 
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
@@ -218,78 +217,73 @@ __global__ __launch_bounds__(kRedThreads) void k_reduce_params(
 }
 
 // ---------------------------------------------------------------------------------------
-// Token mix: identity, fixed G x G matrix, per-token channel map (one thread per output).
+// Linear token maps for token sets too large for the single-workgroup LDS kernels: batched
+// fp32 products C_o = alpha sum_s A_{o,s} B_{o,s} on MFMA, one wavefront per 16 x 16 output
+// tile, operands read straight from global memory (they are small and cache resident). A
+// strided descriptor covers the forward map, its transpose, and the parameter gradients
+// summed over samples and heads without partials.
 // ---------------------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void k_mix_linear(const float* z, float* zmix,
-                                                         const float* A, const float* Wc,
-                                                         int kind, int a_per_head, int H, int G,
-                                                         int V) {
-  const int bh = blockIdx.y;
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= G * V) return;
-  const int g = idx / V, v = idx % V;
-  const float* zb = z + (int64_t)bh * G * V;
-  float acc = 0.f;
-  if (kind == 0) {
-    acc = zb[idx];
-  } else if (kind == 1) {
-    const float* Ah = A + (a_per_head ? (int64_t)(bh % H) * G * G : 0) + (int64_t)g * G;
-    for (int k = 0; k < G; ++k) acc += Ah[k] * zb[(int64_t)k * V + v];
-  } else {
-    for (int k = 0; k < V; ++k) acc += zb[(int64_t)g * V + k] * Wc[(int64_t)k * V + v];
+struct GemmDesc {
+  // element (m, k) of A for output o and summand s: A[(o % a_mod) * a_o + s * a_s + m * a_rs + k * a_cs]
+  const float* A;
+  int64_t a_rs, a_cs, a_o, a_s;
+  int a_mod;
+  const float* B;  // element (k, n): B[o * b_o + s * b_s + k * b_rs + n * b_cs]
+  int64_t b_rs, b_cs, b_o, b_s;
+  float* C;  // element (m, n): C[o * c_o + m * c_rs + n]
+  int64_t c_rs, c_o;
+  int M, N, K, nsum;
+  float alpha;
+};
+
+constexpr int kGemmWaves = 4;
+
+__global__ __launch_bounds__(64 * kGemmWaves) void k_tile_gemm(GemmDesc d) {
+  typedef float f4 __attribute__((ext_vector_type(4)));
+  const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
+  const int t = blockIdx.x * kGemmWaves + (threadIdx.x >> 6);
+  const int tn = d.N >> 4;
+  if (t >= (d.M >> 4) * tn) return;  // whole wavefronts only
+  const int m0 = (t / tn) << 4, n0 = (t % tn) << 4;
+  const int o = blockIdx.y;
+  const float* Ao = d.A + (int64_t)(o % d.a_mod) * d.a_o + (int64_t)(m0 + i) * d.a_rs;
+  const float* Bo = d.B + (int64_t)o * d.b_o + (int64_t)(n0 + i) * d.b_cs;
+  f4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int sidx = 0; sidx < d.nsum; ++sidx) {
+    const float* As = Ao + (int64_t)sidx * d.a_s;
+    const float* Bs = Bo + (int64_t)sidx * d.b_s;
+    int k = 0;
+    for (; k + 32 <= d.K; k += 32) {  // eight products' operands loaded before their MFMAs
+      float av[8], bv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        av[u] = As[(int64_t)(k + 4 * u + j) * d.a_cs];
+        bv[u] = Bs[(int64_t)(k + 4 * u + j) * d.b_rs];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u], acc, 0, 0, 0);
+    }
+    for (; k < d.K; k += 4)
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(As[(int64_t)(k + j) * d.a_cs],
+                                                 Bs[(int64_t)(k + j) * d.b_rs], acc, 0, 0, 0);
   }
-  zmix[(int64_t)bh * G * V + idx] = acc;
+  float* Co = d.C + (int64_t)o * d.c_o + n0 + i;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) Co[(int64_t)(m0 + 4 * j + r) * d.c_rs] = d.alpha * acc[r];
 }
 
-// dz = Mix^T(dzmix) for the linear kinds (one thread per output).
-__global__ __launch_bounds__(kThreads) void k_mix_dz_linear(const float* dzm, float* dz,
-                                                            const float* A, const float* Wc,
-                                                            int kind, int a_per_head, int H,
-                                                            int G, int V) {
-  const int bh = blockIdx.y;
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= G * V) return;
-  const int g = idx / V, v = idx % V;
-  const float* db = dzm + (int64_t)bh * G * V;
-  float acc = 0.f;
-  if (kind == 0) {
-    acc = db[idx];
-  } else if (kind == 1) {
-    const float* Ah = A + (a_per_head ? (int64_t)(bh % H) * G * G : 0);
-    for (int k = 0; k < G; ++k) acc += Ah[(int64_t)k * G + g] * db[(int64_t)k * V + v];
-  } else {
-    for (int k = 0; k < V; ++k) acc += db[(int64_t)g * V + k] * Wc[(int64_t)v * V + k];
-  }
-  dz[(int64_t)bh * G * V + idx] = acc;
+static hipError_t run_gemm(const GemmDesc& d, int nout, hipStream_t st) {
+  const int tiles = (d.M / 16) * (d.N / 16);
+  hipLaunchKernelGGL(k_tile_gemm, dim3((tiles + kGemmWaves - 1) / kGemmWaves, nout),
+                     dim3(64 * kGemmWaves), 0, st, d);
+  return hipGetLastError();
 }
 
-// Per-(b, h) mix-parameter partial for the linear kinds (one thread per output):
-// LINEAR_G: dA_bh[g][k] = sum_v dzmix[g][v] z[k][v]; LINEAR_C: dWc_bh[c][v] = sum_g z[g][c] dzmix[g][v].
-__global__ __launch_bounds__(kThreads) void k_mix_param_linear(const float* z, const float* dzm,
-                                                               float* partM, int kind, int G,
-                                                               int V) {
-  const int bh = blockIdx.y;
-  const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-  const float* zb = z + (int64_t)bh * G * V;
-  const float* db = dzm + (int64_t)bh * G * V;
-  if (kind == 1) {
-    if (idx >= G * G) return;
-    const int g = idx / G, k = idx % G;
-    float acc = 0.f;
-    for (int v = 0; v < V; ++v) acc += db[(int64_t)g * V + v] * zb[(int64_t)k * V + v];
-    partM[(int64_t)bh * G * G + idx] = acc;
-  } else {
-    if (idx >= V * V) return;
-    const int cc = idx / V, v = idx % V;
-    float acc = 0.f;
-    for (int g = 0; g < G; ++g) acc += zb[(int64_t)g * V + cc] * db[(int64_t)g * V + v];
-    partM[(int64_t)bh * V * V + idx] = acc;
-  }
-}
-
-// Token gradients and the shifts the backward pass B uses, one workgroup per (b, h):
-// dU = dz / (s + eps), ds = -sum_v dz z / (s + eps), and the mass-weighted slot means
+// Token gradients and the shifts the backward pass B uses, one 1024-thread workgroup per
+// (b, h): dU = dz / (s + eps), ds = -sum_v dz z / (s + eps), and the mass-weighted slot means
 // cen = [sum_g m_g zmix[g][:], sum_g m_g dU[g][:], sum_g m_g ds[g]] with m_g = s_g / sum s.
+// Each of the 2V + 1 mean columns is summed by 16 threads over interleaved slots, then
+// combined over those threads in a fixed order.
 __device__ void token_grads(const float* zb, const float* sb, const float* zmb, const float* dzb,
                             float* dUb, float* dsb, float* cenb, int G, int V, float eps) {
   for (int idx = threadIdx.x; idx < G * V; idx += blockDim.x) {
@@ -301,6 +295,7 @@ __device__ void token_grads(const float* zb, const float* sb, const float* zmb, 
     for (int v = 0; v < V; ++v) acc += dzb[(int64_t)g * V + v] * zb[(int64_t)g * V + v];
     dsb[g] = -acc / (sb[g] + eps);
   }
+  __threadfence_block();
   __syncthreads();
   __shared__ float tot_s;
   if (threadIdx.x < 64) {
@@ -311,23 +306,34 @@ __device__ void token_grads(const float* zb, const float* sb, const float* zmb, 
   }
   __syncthreads();
   const float inv = tot_s > 0.f ? 1.0f / tot_s : 0.f;
-  for (int c = threadIdx.x; c < 2 * V + 1; c += blockDim.x) {
+  const int ncol = 2 * V + 1;
+  for (int base = 0; base < ncol * 16; base += blockDim.x) {
+    const int idx = base + threadIdx.x;
+    const int c = idx >> 4, part = idx & 15;
     float acc = 0.f;
-    if (c < V) {
-      for (int g = 0; g < G; ++g) acc += sb[g] * zmb[(int64_t)g * V + c];
-    } else if (c < 2 * V) {
-      for (int g = 0; g < G; ++g) acc += sb[g] * dUb[(int64_t)g * V + (c - V)];
-    } else {
-      for (int g = 0; g < G; ++g) acc += sb[g] * dsb[g];
+    if (c < ncol) {
+      if (c < V) {
+        for (int g = part; g < G; g += 16) acc += sb[g] * zmb[(int64_t)g * V + c];
+      } else if (c < 2 * V) {
+        for (int g = part; g < G; g += 16) acc += sb[g] * dUb[(int64_t)g * V + (c - V)];
+      } else {
+        for (int g = part; g < G; g += 16) acc += sb[g] * dsb[g];
+      }
     }
-    cenb[c] = acc * inv;
+    // fixed-order sum over the 16 threads of a column (aligned groups of 16 lanes)
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 16);
+    if (c < ncol && part == 0) cenb[c] = acc * inv;
   }
 }
 
-__global__ __launch_bounds__(kThreads) void k_token_grads(const float* z, const float* s,
-                                                          const float* zmix, const float* dz,
-                                                          float* dU, float* ds, float* cen,
-                                                          int G, int V, float eps) {
+constexpr int kTokGradThreads = 1024;
+
+__global__ __launch_bounds__(kTokGradThreads) void k_token_grads(const float* z, const float* s,
+                                                                 const float* zmix,
+                                                                 const float* dz, float* dU,
+                                                                 float* ds, float* cen, int G,
+                                                                 int V, float eps) {
   const int bh = blockIdx.x;
   const int64_t o = (int64_t)bh * G * V;
   token_grads(z + o, s + (int64_t)bh * G, zmix + o, dz + o, dU + o, ds + (int64_t)bh * G,
@@ -376,251 +382,6 @@ __device__ void attn_softmax_rows(float* S, float* P, int G) {
       if (P != S) P[(int64_t)g * G + u] = p;
     }
   }
-}
-
-// All-LDS variant for G V <= 2048, G <= 64, V <= 64: z, the three projections, q, k, v and
-// the G x G scores all live in dynamically sized LDS, so no phase waits on global memory.
-// Rows are padded by one float (VP = V + 1, GP = G + 1) so that lanes walking different rows
-// of the same column hit different LDS banks.
-constexpr int kAttnSmallGV = 2048;
-
-inline int attn_small_fwd_floats(int G, int V) {
-  const int VP = V + 1, GP = G + 1;
-  return 4 * G * VP + 3 * V * VP + G * GP;
-}
-inline int attn_small_bwd_floats(int G, int V) {
-  const int VP = V + 1, GP = G + 1;
-  return 11 * G * VP + 3 * V * VP + 2 * G * GP + 3 * G;
-}
-
-// Ws: the three projections, [3][V][VP] (padded rows).
-__device__ void attn_project_lds(const float* zs, const float* Ws, float* q, float* k, float* v,
-                                 int G, int V) {
-  const int GV = G * V, VP = V + 1;
-  for (int idx = threadIdx.x; idx < 3 * GV; idx += blockDim.x) {
-    const int which = idx / GV, r = idx % GV;
-    const int g = r / V, c = r % V;
-    const float* W = Ws + which * V * VP;
-    float acc = 0.f;
-#pragma unroll 8
-    for (int e = 0; e < V; ++e) acc += zs[g * VP + e] * W[e * VP + c];
-    (which == 0 ? q : (which == 1 ? k : v))[g * VP + c] = acc;
-  }
-}
-
-__global__ __launch_bounds__(kAttnThreads) void k_attn_fwd_small(const float* z, float* zmix,
-                                                                 float* P, const float* Wq,
-                                                                 const float* Wk,
-                                                                 const float* Wv, float scale,
-                                                                 int G, int V) {
-  extern __shared__ float lds[];
-  const int GV = G * V, VV = V * V, VP = V + 1, GP = G + 1;
-  float* zs = lds;              // [G][VP]
-  float* Ws = zs + G * VP;      // [3][V][VP]
-  float* q = Ws + 3 * V * VP;   // [G][VP]
-  float* k = q + G * VP;
-  float* v = k + G * VP;
-  float* S = v + G * VP;        // [G][GP]
-  const int bh = blockIdx.x;
-  for (int idx = threadIdx.x; idx < GV; idx += blockDim.x)
-    zs[(idx / V) * VP + idx % V] = z[(int64_t)bh * GV + idx];
-  for (int idx = threadIdx.x; idx < VV; idx += blockDim.x) {
-    const int o = (idx / V) * VP + idx % V;
-    Ws[o] = Wq[idx];
-    Ws[V * VP + o] = Wk[idx];
-    Ws[2 * V * VP + o] = Wv[idx];
-  }
-  __syncthreads();
-  attn_project_lds(zs, Ws, q, k, v, G, V);
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < G * G; idx += blockDim.x) {
-    const int g = idx / G, u = idx % G;
-    float acc = 0.f;
-#pragma unroll 8
-    for (int c = 0; c < V; ++c) acc += q[g * VP + c] * k[u * VP + c];
-    S[g * GP + u] = scale * acc;
-  }
-  __syncthreads();
-  {  // row softmax, one wavefront per row; P is written unpadded
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    float* Pb = P + (int64_t)bh * G * G;
-    for (int g = wave; g < G; g += nw) {
-      float m = -INFINITY;
-      for (int u = lane; u < G; u += 64) m = fmaxf(m, S[g * GP + u]);
-      m = wave_max(m);
-      float l = 0.f;
-      for (int u = lane; u < G; u += 64) {
-        const float e = expf(S[g * GP + u] - m);
-        S[g * GP + u] = e;
-        l += e;
-      }
-      l = wave_sum(l);
-      const float inv = 1.0f / l;
-      for (int u = lane; u < G; u += 64) {
-        const float p = S[g * GP + u] * inv;
-        S[g * GP + u] = p;
-        Pb[(int64_t)g * G + u] = p;
-      }
-    }
-  }
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < GV; idx += blockDim.x) {
-    const int g = idx / V, c = idx % V;
-    float acc = 0.f;
-#pragma unroll 8
-    for (int u = 0; u < G; ++u) acc += S[g * GP + u] * v[u * VP + c];
-    zmix[(int64_t)bh * GV + idx] = acc;
-  }
-}
-
-// token_grads with every operand in LDS (zs, zms, dzs, dUs: [G][VP]; ss, dsl: [G]).
-__device__ void token_grads_lds(const float* zs, const float* ss, const float* zms,
-                                const float* dzs, float* dUs, float* dsl, float* dUb,
-                                float* dsb, float* cenb, int G, int V, float eps) {
-  const int VP = V + 1;
-  for (int idx = threadIdx.x; idx < G * V; idx += blockDim.x) {
-    const int g = idx / V, c = idx % V;
-    const float u = dzs[g * VP + c] / (ss[g] + eps);
-    dUs[g * VP + c] = u;
-    dUb[idx] = u;
-  }
-  for (int g = threadIdx.x; g < G; g += blockDim.x) {
-    float acc = 0.f;
-#pragma unroll 8
-    for (int c = 0; c < V; ++c) acc += dzs[g * VP + c] * zs[g * VP + c];
-    const float d = -acc / (ss[g] + eps);
-    dsl[g] = d;
-    dsb[g] = d;
-  }
-  __syncthreads();
-  float tot = 0.f;
-  for (int g = 0; g < G; ++g) tot += ss[g];
-  const float inv = tot > 0.f ? 1.0f / tot : 0.f;
-  for (int c = threadIdx.x; c < 2 * V + 1; c += blockDim.x) {
-    float acc = 0.f;
-    if (c < V) {
-#pragma unroll 8
-      for (int g = 0; g < G; ++g) acc += ss[g] * zms[g * VP + c];
-    } else if (c < 2 * V) {
-#pragma unroll 8
-      for (int g = 0; g < G; ++g) acc += ss[g] * dUs[g * VP + (c - V)];
-    } else {
-      for (int g = 0; g < G; ++g) acc += ss[g] * dsl[g];
-    }
-    cenb[c] = acc * inv;
-  }
-}
-
-__global__ __launch_bounds__(kAttnThreads) void k_attn_bwd_small(
-    const float* z, const float* s, const float* zmix, const float* P, const float* dzm,
-    float* dz, float* dU, float* ds, float* cen, float* partM, const float* Wq,
-    const float* Wk, const float* Wv, float scale, int G, int V, float eps) {
-  extern __shared__ float lds[];
-  const int GV = G * V, VV = V * V, GG = G * G, VP = V + 1, GP = G + 1;
-  float* zs = lds;              // [G][VP] each, unless noted
-  float* Ws = zs + G * VP;      // [3][V][VP]
-  float* q = Ws + 3 * V * VP;
-  float* k = q + G * VP;
-  float* v = k + G * VP;
-  float* gz = v + G * VP;
-  float* dq = gz + G * VP;
-  float* dk = dq + G * VP;
-  float* dv = dk + G * VP;
-  float* Ps = dv + G * VP;      // [G][GP]
-  float* dS = Ps + G * GP;      // [G][GP]
-  float* rs = dS + G * GP;      // [G]
-  float* dzs = rs + G;          // dz, then the token gradients
-  float* zms = dzs + G * VP;    // zmix
-  float* dUs = zms + G * VP;
-  float* ss = dUs + G * VP;     // [G]
-  float* dsl = ss + G;          // [G]
-  const int bh = blockIdx.x;
-  for (int idx = threadIdx.x; idx < GV; idx += blockDim.x) {
-    const int o = (idx / V) * VP + idx % V;
-    zs[o] = z[(int64_t)bh * GV + idx];
-    gz[o] = dzm[(int64_t)bh * GV + idx];
-  }
-  for (int idx = threadIdx.x; idx < VV; idx += blockDim.x) {
-    const int o = (idx / V) * VP + idx % V;
-    Ws[o] = Wq[idx];
-    Ws[V * VP + o] = Wk[idx];
-    Ws[2 * V * VP + o] = Wv[idx];
-  }
-  for (int idx = threadIdx.x; idx < GG; idx += blockDim.x)
-    Ps[(idx / G) * GP + idx % G] = P[(int64_t)bh * GG + idx];
-  __syncthreads();
-  attn_project_lds(zs, Ws, q, k, v, G, V);
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < GG; idx += blockDim.x) {   // dP
-    const int g = idx / G, u = idx % G;
-    float acc = 0.f;
-#pragma unroll 8
-    for (int c = 0; c < V; ++c) acc += gz[g * VP + c] * v[u * VP + c];
-    dS[g * GP + u] = acc;
-  }
-  __syncthreads();
-  {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-    for (int g = wave; g < G; g += nw) {
-      float acc = 0.f;
-      for (int u = lane; u < G; u += 64) acc += dS[g * GP + u] * Ps[g * GP + u];
-      acc = wave_sum(acc);
-      if (lane == 0) rs[g] = acc;
-    }
-  }
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < GG; idx += blockDim.x) {
-    const int o = (idx / G) * GP + idx % G;
-    dS[o] = Ps[o] * (dS[o] - rs[idx / G]);
-  }
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < 3 * GV; idx += blockDim.x) {
-    const int which = idx / GV, r = idx % GV;
-    const int a = r / V, c = r % V;
-    float acc = 0.f;
-    if (which == 0) {        // dq[a] = scale sum_u dS[a][u] k[u]
-#pragma unroll 8
-      for (int u = 0; u < G; ++u) acc += dS[a * GP + u] * k[u * VP + c];
-      dq[a * VP + c] = scale * acc;
-    } else if (which == 1) { // dk[a] = scale sum_g dS[g][a] q[g]
-#pragma unroll 8
-      for (int g = 0; g < G; ++g) acc += dS[g * GP + a] * q[g * VP + c];
-      dk[a * VP + c] = scale * acc;
-    } else {                 // dv[a] = sum_g P[g][a] dzmix[g]
-#pragma unroll 8
-      for (int g = 0; g < G; ++g) acc += Ps[g * GP + a] * gz[g * VP + c];
-      dv[a * VP + c] = acc;
-    }
-  }
-  __syncthreads();
-  float* dzb = dz + (int64_t)bh * GV;
-  for (int idx = threadIdx.x; idx < GV; idx += blockDim.x) {
-    const int g = idx / V, e = idx % V;
-    float acc = 0.f;
-#pragma unroll 8
-    for (int c = 0; c < V; ++c)
-      acc += dq[g * VP + c] * Ws[e * VP + c] + dk[g * VP + c] * Ws[V * VP + e * VP + c] +
-             dv[g * VP + c] * Ws[2 * V * VP + e * VP + c];
-    dzb[idx] = acc;
-    dzs[g * VP + e] = acc;
-  }
-  float* pm = partM + (int64_t)bh * 3 * VV;
-  for (int idx = threadIdx.x; idx < 3 * VV; idx += blockDim.x) {
-    const int which = idx / VV, r = idx % VV;
-    const int e = r / V, c = r % V;
-    const float* d = which == 0 ? dq : (which == 1 ? dk : dv);
-    float acc = 0.f;
-#pragma unroll 8
-    for (int g = 0; g < G; ++g) acc += zs[g * VP + e] * d[g * VP + c];
-    pm[idx] = acc;
-  }
-  if (s == nullptr) return;
-  for (int idx = threadIdx.x; idx < GV; idx += blockDim.x)
-    zms[(idx / V) * VP + idx % V] = zmix[(int64_t)bh * GV + idx];
-  for (int g = threadIdx.x; g < G; g += blockDim.x) ss[g] = s[(int64_t)bh * G + g];
-  __syncthreads();
-  token_grads_lds(zs, ss, zms, dzs, dUs, dsl, dU + (int64_t)bh * GV, ds + (int64_t)bh * G,
-                  cen + (int64_t)bh * (2 * V + 1), G, V, eps);
 }
 
 __global__ __launch_bounds__(kThreads) void k_attn_fwd(const float* z, float* zmix, float* P,
@@ -742,16 +503,7 @@ inline unsigned blocks(int64_t n, int per) { return (unsigned)((n + per - 1) / p
 inline int64_t mix_partial_len(const Geom& g, int kind) {
   return kind == 1 ? (int64_t)g.G * g.G : (kind == 2 ? (int64_t)g.V * g.V : 3LL * g.V * g.V);
 }
-inline bool attn_small(const Geom& g) {
-  return g.G * g.V <= kAttnSmallGV && g.G <= 64 && g.V <= 64;
-}
-// Dynamic LDS above 64 KB has to be allowed per kernel once.
-template <typename K>
-hipError_t allow_lds(K kernel, size_t bytes) {
-  if (bytes <= 65536) return hipSuccess;
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-}
+
 
 }  // namespace
 
@@ -770,11 +522,18 @@ hipError_t launch_reduce_rows(const Geom& g, const float* part, float* out, int 
   return hipGetLastError();
 }
 
+// Whether the mix-parameter gradient goes through per-(b, h) partials (the LDS kernels and
+// attention) or is written directly (the batched products of the linear maps).
+static bool mix_params_in_partials(const Geom& g, int kind) {
+  return tok_fused(g, kind) || kind == 3;
+}
+
 hipError_t launch_reduce_params(const Geom& g, const float* part, float* dWs, float* dbias,
                                 float* dtau, int chunks, int nblk, const MixArgs* m,
                                 const float* partM, float* dmix, hipStream_t st) {
   const int64_t ncol = (int64_t)g.D * g.G + g.G;
-  const bool with_mix = m != nullptr && dmix != nullptr && m->kind != 0;
+  const bool with_mix =
+      m != nullptr && dmix != nullptr && m->kind != 0 && mix_params_in_partials(g, m->kind);
   const int64_t mix_len = with_mix ? mix_partial_len(g, m->kind) : 0;
   const bool mix_per_head = with_mix && m->kind == 1 && m->a_per_head;
   const unsigned nb = blocks(ncol, kColsWide) + 1 + (with_mix ? blocks(mix_len, kColsWide) : 0);
@@ -785,27 +544,33 @@ hipError_t launch_reduce_params(const Geom& g, const float* part, float* dWs, fl
   return hipGetLastError();
 }
 
+// Linear maps of one (b, h) per output: zmix = A z (fixed matrix) or z W_c (channel map).
+static GemmDesc mix_fwd_desc(const Geom& g, const MixArgs& m, const float* z, float* zmix) {
+  const int64_t GV = (int64_t)g.G * g.V;
+  GemmDesc d{};
+  if (m.kind == 1) {  // (G x G) x (G x V)
+    d = GemmDesc{m.A, g.G, 1, (int64_t)g.G * g.G, 0, m.a_per_head ? g.H : 1,
+                 z, g.V, 1, GV, 0, zmix, g.V, GV, g.G, g.V, g.G, 1, 1.0f};
+  } else {            // (G x V) x (V x V)
+    d = GemmDesc{z, g.V, 1, GV, 0, 1 << 30, m.Wc, g.V, 1, 0, 0, zmix, g.V, GV, g.G, g.V, g.V, 1, 1.0f};
+  }
+  return d;
+}
+
 hipError_t launch_mix(const Geom& g, const MixArgs& m, const float* z, float* zmix,
                       float* attn, hipStream_t st) {
   const int BH = g.BH();
   if (tok_fused(g, m.kind)) return launch_tok_fwd(g, m, z, zmix, attn, st);
   if (m.kind == 3) {
-    if (attn_small(g)) {
-      const size_t lds = sizeof(float) * (size_t)attn_small_fwd_floats(g.G, g.V);
-      hipError_t e = allow_lds(k_attn_fwd_small, lds);
-      if (e != hipSuccess) return e;
-      hipLaunchKernelGGL(k_attn_fwd_small, dim3(BH), dim3(kAttnThreads), lds, st, z, zmix, attn,
-                         m.Wq, m.Wk, m.Wv, m.scale, g.G, g.V);
-    } else {
-      hipLaunchKernelGGL(k_attn_fwd, dim3(BH), dim3(kThreads), 0, st, z, zmix, attn, m.Wq,
-                         m.Wk, m.Wv, m.scale, g.G, g.V);
-    }
-  } else {
-    dim3 grid(blocks((int64_t)g.G * g.V, kThreads), BH);
-    hipLaunchKernelGGL(k_mix_linear, grid, dim3(kThreads), 0, st, z, zmix, m.A, m.Wc, m.kind,
-                       m.a_per_head ? 1 : 0, g.H, g.G, g.V);
+    hipLaunchKernelGGL(k_attn_fwd, dim3(BH), dim3(kThreads), 0, st, z, zmix, attn, m.Wq,
+                       m.Wk, m.Wv, m.scale, g.G, g.V);
+    return hipGetLastError();
   }
-  return hipGetLastError();
+  if (m.kind == 0) {
+    return hipMemcpyAsync(zmix, z, sizeof(float) * (size_t)BH * g.G * g.V,
+                          hipMemcpyDeviceToDevice, st);
+  }
+  return run_gemm(mix_fwd_desc(g, m, z, zmix), BH, st);
 }
 
 hipError_t launch_mix_bwd(const Geom& g, const MixArgs& m, const float* z, const float* s,
@@ -813,37 +578,50 @@ hipError_t launch_mix_bwd(const Geom& g, const MixArgs& m, const float* z, const
                           float* dU, float* ds, float* cen, float* scr, float* partM,
                           float* dmix, bool reduce_params, hipStream_t st) {
   const int BH = g.BH();
-  hipError_t e;
+  const int64_t GV = (int64_t)g.G * g.V;
+  hipError_t e = hipSuccess;
   if (tok_fused(g, m.kind)) {
     e = launch_tok_bwd(g, m, z, s, zmix, attn, dzm, dz, dU, ds, cen, partM, st);
   } else if (m.kind == 3) {
-    if (attn_small(g)) {
-      const size_t lds = sizeof(float) * (size_t)attn_small_bwd_floats(g.G, g.V);
-      hipError_t e = allow_lds(k_attn_bwd_small, lds);
-      if (e != hipSuccess) return e;
-      hipLaunchKernelGGL(k_attn_bwd_small, dim3(BH), dim3(kAttnThreads), lds, st, z, s, zmix, attn,
-                         dzm, dz, dU, ds, cen, partM, m.Wq, m.Wk, m.Wv, m.scale, g.G, g.V, g.eps);
-    } else {
-      hipLaunchKernelGGL(k_attn_bwd, dim3(BH), dim3(kThreads), 0, st, z, s, zmix, attn, dzm, dz,
-                         dU, ds, cen, scr, partM, m.Wq, m.Wk, m.Wv, m.scale, g.G, g.V, g.eps);
-    }
+    hipLaunchKernelGGL(k_attn_bwd, dim3(BH), dim3(kThreads), 0, st, z, s, zmix, attn, dzm, dz,
+                       dU, ds, cen, scr, partM, m.Wq, m.Wk, m.Wv, m.scale, g.G, g.V, g.eps);
+    e = hipGetLastError();
   } else {
-    dim3 grid(blocks((int64_t)g.G * g.V, kThreads), BH);
-    hipLaunchKernelGGL(k_mix_dz_linear, grid, dim3(kThreads), 0, st, dzm, dz, m.A, m.Wc, m.kind,
-                       m.a_per_head ? 1 : 0, g.H, g.G, g.V);
-    if (dmix != nullptr && m.kind != 0) {
-      const int64_t len = m.kind == 1 ? (int64_t)g.G * g.G : (int64_t)g.V * g.V;
-      dim3 pg(blocks(len, kThreads), BH);
-      hipLaunchKernelGGL(k_mix_param_linear, pg, dim3(kThreads), 0, st, z, dzm, partM, m.kind,
-                         g.G, g.V);
+    if (m.kind == 0) {
+      e = hipMemcpyAsync(dz, dzm, sizeof(float) * (size_t)BH * GV, hipMemcpyDeviceToDevice, st);
+    } else if (m.kind == 1) {  // dz = A^T dzmix
+      e = run_gemm(GemmDesc{m.A, 1, g.G, (int64_t)g.G * g.G, 0, m.a_per_head ? g.H : 1, dzm,
+                            g.V, 1, GV, 0, dz, g.V, GV, g.G, g.V, g.G, 1, 1.0f},
+                   BH, st);
+    } else {                   // dz = dzmix W_c^T
+      e = run_gemm(GemmDesc{dzm, g.V, 1, GV, 0, 1 << 30, m.Wc, 1, g.V, 0, 0, dz, g.V, GV, g.G,
+                            g.V, g.V, 1, 1.0f},
+                   BH, st);
     }
-    if (s != nullptr)
-      hipLaunchKernelGGL(k_token_grads, dim3(BH), dim3(kThreads), 0, st, z, s, zmix, dz, dU, ds,
-                         cen, g.G, g.V, g.eps);
+    if (e == hipSuccess && dmix != nullptr && m.kind == 1) {
+      // dA = sum over (b, h) of dzmix z^T, or over b for each head's own A
+      if (m.a_per_head)
+        e = run_gemm(GemmDesc{dzm, g.V, 1, GV, (int64_t)g.H * GV, 1 << 30, z, 1, g.V, GV,
+                              (int64_t)g.H * GV, dmix, g.G, (int64_t)g.G * g.G, g.G, g.G, g.V,
+                              (int)g.B, 1.0f},
+                     g.H, st);
+      else
+        e = run_gemm(GemmDesc{dzm, g.V, 1, 0, GV, 1, z, 1, g.V, 0, GV, dmix, g.G, 0, g.G, g.G,
+                              g.V, BH, 1.0f},
+                     1, st);
+    }
+    if (e == hipSuccess && dmix != nullptr && m.kind == 2)  // dW_c = sum over (b, h) of z^T dzmix
+      e = run_gemm(GemmDesc{z, 1, g.V, 0, GV, 1, dzm, g.V, 1, 0, GV, dmix, g.V, 0, g.V, g.V,
+                            g.G, BH, 1.0f},
+                   1, st);
+    if (e == hipSuccess && s != nullptr) {
+      hipLaunchKernelGGL(k_token_grads, dim3(BH), dim3(kTokGradThreads), 0, st, z, s, zmix, dz,
+                         dU, ds, cen, g.G, g.V, g.eps);
+      e = hipGetLastError();
+    }
   }
-  if (!tok_fused(g, m.kind)) e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (reduce_params && dmix != nullptr && m.kind != 0) {
+  if (reduce_params && dmix != nullptr && m.kind != 0 && mix_params_in_partials(g, m.kind)) {
     const int64_t len = mix_partial_len(g, m.kind);
     const bool per_head = m.kind == 1 && m.a_per_head;
     dim3 grid(blocks(len, kColsWide), per_head ? g.H : 1);
