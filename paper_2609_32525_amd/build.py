@@ -15,6 +15,13 @@ SOURCES = [os.path.join(HERE, "csrc", f) for f in (
     "fs_pass_point.hip",
     "fs_kernels.hip", "fs_tokens.hip", "fs_tokmix.hip", "fs_api.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+# Per-source flags: MFMA results in VGPRs rather than accumulation registers measured faster
+# for the slice and deslice passes (less accumulator traffic around the softmax) and slower
+# for backward pass B (higher register pressure), so it is applied per translation unit.
+SOURCE_FLAGS = {
+    "fs_pass_slice.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "fs_pass_deslice.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
 
 # -packed-fp32-ops: no v_pk_{add,mul,fma}_f32 in the generated code.
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -39,7 +46,8 @@ def build(verbose: bool = False, extra=None) -> str:
     for src in SOURCES:
         obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
         objs.append(obj)
-        cmds.append([HIPCC] + cflags + ["-c", src, "-o", obj])
+        cmds.append([HIPCC] + cflags + SOURCE_FLAGS.get(os.path.basename(src), [])
+                    + ["-c", src, "-o", obj])
     with ThreadPoolExecutor(max_workers=min(len(cmds), os.cpu_count() or 1)) as ex:
         errs = list(ex.map(_run, cmds))
     tmp = LIB + ".tmp"

@@ -74,10 +74,11 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
         w[gb][pb] = acc;
       }
     f4 o[VB][2];
+    const TileB<BF, GB, 2> wt = tile_b<BF, GB, 2>(w);
 #pragma unroll
     for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
-      for (int pb = 0; pb < 2; ++pb) o[vb][pb] = mm_gop_tile<BF, GB, VB>(zop, vb, w, pb, zero4());
+      for (int pb = 0; pb < 2; ++pb) o[vb][pb] = mm_gop_b<BF, GB, VB, 2>(zop, vb, wt, pb, zero4());
 
     if constexpr (NS > 1) {
       if (ws > 0) {

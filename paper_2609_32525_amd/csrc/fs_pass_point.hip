@@ -141,26 +141,43 @@ __device__ __forceinline__ void stage_put(const Stage<N>& s, uint4* dst) {
   }
 }
 
-// Contraction over a half block's 32 slots with the B operand (a T-layout tile) rounded in two
-// bf16 parts for bf16 storage: acc += M^T (hi + lo).
+// A T-layout tile over a half block's 32 slots as the B operand of contractions over slots,
+// rounded in two bf16 parts for bf16 storage (hi + lo), converted once per tile.
+template <bool BF, int GBH>
+struct SplitB {
+  const f4 (*t)[2];
+  bf8 hi[GBH / 2][2], lo[GBH / 2][2];
+};
+template <bool BF, int GBH>
+__device__ __forceinline__ SplitB<BF, GBH> split_b(const f4 (*t)[2]) {
+  SplitB<BF, GBH> o;
+  o.t = t;
+  if constexpr (BF) {
+#pragma unroll
+    for (int q = 0; q < GBH / 2; ++q)
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float v = t[2 * q + e / 4][pb][e % 4];
+          const __bf16 h = (__bf16)v;
+          o.hi[q][pb][e] = h;
+          o.lo[q][pb][e] = (__bf16)(v - (float)h);
+        }
+  }
+  return o;
+}
+// acc += M^T (hi + lo): the contraction over the half block with the split operand.
 template <bool BF, int GBH, int CB>
-__device__ __forceinline__ f4 mm_gop_split(const GOp<BF, GBH, CB>& o, int cb, const f4 (*t)[2],
-                                           int pb, f4 acc) {
+__device__ __forceinline__ f4 mm_split_b(const GOp<BF, GBH, CB>& o, int cb, const SplitB<BF, GBH>& s,
+                                         int pb, f4 acc) {
   if constexpr (!BF) {
-    return mm_gop_tile<false, GBH, CB, 2>(o, cb, t, pb, acc);
+    return mm_gop_tile<false, GBH, CB, 2>(o, cb, s.t, pb, acc);
   } else {
 #pragma unroll
     for (int q = 0; q < GBH / 2; ++q) {
-      bf8 hi, lo;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float v = t[2 * q + e / 4][pb][e % 4];
-        const __bf16 h = (__bf16)v;
-        hi[e] = h;
-        lo[e] = (__bf16)(v - (float)h);
-      }
-      acc = mfma_bf16(o.v[q][cb], hi, acc);
-      acc = mfma_bf16(o.v[q][cb], lo, acc);
+      acc = mfma_bf16(o.v[q][cb], s.hi[q][pb], acc);
+      acc = mfma_bf16(o.v[q][cb], s.lo[q][pb], acc);
     }
     return acc;
   }
@@ -300,15 +317,17 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2)))
           UOp ug, wg;
           lds_get(ug, hb + IM::kW + 2 * IM::kZ, lane);
           lds_get(wg, hb + IM::kW + 2 * IM::kZ + IM::kU, lane);
+          const TileB<BF, GBH, 2> wt = tile_b<BF, GBH, 2>(w);
+          const SplitB<BF, GBH> ws = split_b<BF, GBH>(w), dws = split_b<BF, GBH>(dw);
 #pragma unroll
           for (int pb = 0; pb < 2; ++pb) {
 #pragma unroll
             for (int vb = 0; vb < VB; ++vb)
-              gf[vb][pb] = mm_gop_tile<BF, GBH, VB, 2>(ug, vb, w, pb, gf[vb][pb]);
+              gf[vb][pb] = mm_gop_b<BF, GBH, VB, 2>(ug, vb, wt, pb, gf[vb][pb]);
 #pragma unroll
             for (int d = 0; d < DB; ++d) {
-              P[d][pb] = mm_gop_split<BF, GBH, DB>(wg, d, dw, pb, P[d][pb]);
-              Q[d][pb] = mm_gop_split<BF, GBH, DB>(wg, d, w, pb, Q[d][pb]);
+              P[d][pb] = mm_split_b<BF, GBH, DB>(wg, d, dws, pb, P[d][pb]);
+              Q[d][pb] = mm_split_b<BF, GBH, DB>(wg, d, ws, pb, Q[d][pb]);
             }
           }
         }

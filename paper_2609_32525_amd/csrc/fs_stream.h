@@ -413,6 +413,50 @@ __device__ __forceinline__ f4 mm_gop_tile(const GOp<BF, GB, CB>& o, int cb, cons
   return acc;
 }
 
+// A T-layout tile as the B operand of contractions over slots, converted once and reused for
+// every output column block: fp32 keeps the tile itself; bf16 packs slot pairs q of column
+// block pb into bf8 (element e = row 16 (e / 4) + 4 j + (e % 4) of the pair).
+template <bool BF, int GB, int PB>
+struct TileB;
+template <int GB, int PB>
+struct TileB<false, GB, PB> {
+  const f4 (*t)[PB];
+};
+template <int GB, int PB>
+struct TileB<true, GB, PB> {
+  bf8 v[GB / 2][PB];
+};
+template <bool BF, int GB, int PB>
+__device__ __forceinline__ TileB<BF, GB, PB> tile_b(const f4 (*t)[PB]) {
+  TileB<BF, GB, PB> o;
+  if constexpr (!BF) {
+    o.t = t;
+  } else {
+#pragma unroll
+    for (int q = 0; q < GB / 2; ++q)
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o.v[q][pb][e] = (__bf16)t[2 * q + e / 4][pb][e % 4];
+  }
+  return o;
+}
+// out[cb] (+)= M^T-contraction with a converted tile (same result as mm_gop_tile).
+template <bool BF, int GB, int CB, int PB>
+__device__ __forceinline__ f4 mm_gop_b(const GOp<BF, GB, CB>& o, int cb, const TileB<BF, GB, PB>& tb,
+                                       int pb, f4 acc) {
+  if constexpr (!BF) {
+#pragma unroll
+    for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc = mfma_f32(o.v[gb][r][cb], tb.t[gb][pb][r], acc);
+  } else {
+#pragma unroll
+    for (int q = 0; q < GB / 2; ++q) acc = mfma_bf16(o.v[q][cb], tb.v[q][pb], acc);
+  }
+  return acc;
+}
+
 // Operand rows of a point-major matrix P (row stride rs) for a contraction over the 32 points
 // of a tile: lane (j, i) holds P(p, 16 cb + i) for the points of its k-set.
 //   fp32: point 16 pb + 4 j + r for MFMA (pb, r);  bf16: point 16 (e / 4) + 4 j + (e % 4).
