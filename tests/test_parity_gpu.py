@@ -97,6 +97,11 @@ SMALL = [
           ws_mode="std3", N=800, H=2),
     small("bf16_D32_G1024_lin", "bf16", 32, 1024, O.MIX_LINEAR_G, tau_mode="uniform",
           ws_mode="std3", N=700, H=2, B=1),
+    # large token sets with every mix kind, and dh = 64 beyond G = 128
+    small("f32_D32_G512_linc", "f32", 32, 512, O.MIX_LINEAR_C, N=600, H=2),
+    small("f32_D16_G1024_id", "f32", 16, 1024, O.MIX_IDENTITY, N=500, H=2, B=1),
+    small("bf16_D64_G256_lin", "bf16", 64, 256, O.MIX_LINEAR_G, N=600, H=2),
+    small("bf16_D32_G256_attn", "bf16", 32, 256, O.MIX_ATTN, N=600, H=2),
 ]
 
 
@@ -262,3 +267,81 @@ def test_parity_full_size(name):
     print("  errors:", {k: f"{e:.2e}" for k, e in errs.items()}, flush=True)
     bad = {k: e for k, e in errs.items() if not e <= tol}
     assert not bad, f"{name}: above {tol:g}: {bad}"
+
+
+# ---- the standalone token-mix entry points (fs_mix, fs_mix_bwd) -----------------------------
+MIX_CASES = [
+    ("identity", O.MIX_IDENTITY, 32, False), ("identity", O.MIX_IDENTITY, 1024, False),
+    ("fixed", O.MIX_LINEAR_G, 32, False), ("fixed", O.MIX_LINEAR_G, 512, False),
+    ("fixed_per_head", O.MIX_LINEAR_G, 64, True), ("fixed_per_head", O.MIX_LINEAR_G, 256, True),
+    ("channel", O.MIX_LINEAR_C, 32, False), ("channel", O.MIX_LINEAR_C, 512, False),
+    ("attention", O.MIX_ATTN, 32, False), ("attention", O.MIX_ATTN, 128, False),
+]
+
+
+@pytest.mark.parametrize("label,kind,G,per_head", MIX_CASES,
+                         ids=[f"{c[0]}_G{c[2]}" for c in MIX_CASES])
+def test_mix_entry_points(label, kind, G, per_head):
+    """fs_mix and fs_mix_bwd on their own (both the single-workgroup LDS kernels and the
+    batched products for large token sets) against the oracle's mix steps, per (b, h); the
+    parameter gradients are summed over samples and heads (over samples per head for a
+    per-head matrix)."""
+    import torch
+    import paper_2609_32525_amd as fs
+    B, H, V = 2, 3, 32
+    w = W.Workload(f"mix_{label}", 300 + kind, "f32", B, 64, H, V, V, G, kind, a_per_head=per_head)
+    inp = W.make_inputs(w, with_grad=False)
+    z = W.random_like(w, 1, (B, H, G, V))
+    dzm = W.random_like(w, 2, (B, H, G, V))
+    announce(f"mix {label} G={G}")
+    dev = torch.device("cuda:0")
+    up = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+    prob = fs.Problem.make(B, 64, H, V, V, G, fs.F32, 1e-5)
+    prm = {k: up(inp[k]) for k in ("A", "Wc", "Wq", "Wk", "Wv") if inp.get(k) is not None}
+    md = fs.MixDesc.make(kind, A=prm.get("A"), Wc=prm.get("Wc"), Wq=prm.get("Wq"),
+                         Wk=prm.get("Wk"), Wv=prm.get("Wv"), scale=float(inp["scale"]),
+                         a_per_head=1 if per_head else 0)
+    zt, dzt = up(z), up(dzm)
+    zmix = torch.empty_like(zt)
+    attn = torch.empty((B, H, G, G), device=dev) if kind == O.MIX_ATTN else None
+    fs.mix(prob, md, zt, zmix, attn)
+    dz = torch.empty_like(zt)
+    npar = {O.MIX_IDENTITY: 0, O.MIX_LINEAR_G: (H if per_head else 1) * G * G,
+            O.MIX_LINEAR_C: V * V, O.MIX_ATTN: 3 * V * V}[kind]
+    dmix = torch.empty(max(npar, 1), device=dev)
+    ws = torch.empty(fs.workspace_bytes(prob, True), device=dev, dtype=torch.uint8)
+    fs.mix_bwd(prob, md, zt, attn, dzt, dz, dmix if npar else None, ws)
+    torch.cuda.synchronize()
+    got_zm, got_dz = zmix.double().cpu().numpy(), dz.double().cpu().numpy()
+    ref_zm, ref_dz, ref_P = np.zeros_like(got_zm), np.zeros_like(got_dz), []
+    ref_par = {}
+    prm_np = {k: inp[k] for k in ("A", "Wc", "Wq", "Wk", "Wv", "scale")}
+    for b in range(B):
+        for h in range(H):
+            p = O._head_params(kind, prm_np, h)
+            zbh = z[b, h].astype(np.float64)
+            zm, P = O.mix_forward(kind, zbh, p)
+            ref_zm[b, h] = zm
+            d, dp = O.mix_backward(kind, zbh, P, dzm[b, h].astype(np.float64), p)
+            ref_dz[b, h] = d
+            if P is not None:
+                ref_P.append(P)
+            for k, v in dp.items():
+                if k == "dA" and per_head:
+                    ref_par.setdefault(k, np.zeros((H, G, G)))[h] += v
+                else:
+                    ref_par[k] = ref_par.get(k, 0) + v
+    errs = {"zmix": rel(got_zm, ref_zm), "dz": rel(got_dz, ref_dz)}
+    if kind == O.MIX_ATTN:
+        errs["P"] = rel(attn.double().cpu().numpy().reshape(-1, G, G), np.stack(ref_P))
+    if npar:
+        d = dmix.double().cpu().numpy()
+        if kind == O.MIX_ATTN:
+            for n, k in enumerate(("dWq", "dWk", "dWv")):
+                errs[k] = rel(d[n * V * V:(n + 1) * V * V].reshape(V, V), ref_par[k])
+        else:
+            k = "dA" if kind == O.MIX_LINEAR_G else "dWc"
+            errs[k] = rel(d.reshape(ref_par[k].shape), ref_par[k])
+    print("  errors:", {k: f"{e:.2e}" for k, e in errs.items()}, flush=True)
+    bad = {k: e for k, e in errs.items() if not e <= 1e-5}
+    assert not bad, bad
