@@ -36,13 +36,22 @@ __device__ __forceinline__ Mat mat(const float* p, int rs, int cs) { return Mat{
 
 // One 16 x 16 tile of C = A B over k in [0, K), K a multiple of 4. Lane (j, i) feeds
 // A(m0 + i, k + j) and B(k + j, n0 + i); the result acc[r] is C(m0 + 4 j + r, n0 + i).
+// Two accumulators take alternate k steps, halving the chain of dependent MFMAs.
 __device__ __forceinline__ f4 mm16(const Mat& A, const Mat& B, int m0, int n0, int K, int i,
                                    int j, f4 acc) {
-#pragma unroll 4
-  for (int k = 0; k < K; k += 4)
+  f4 acc2{0.f, 0.f, 0.f, 0.f};
+  int k = 0;
+#pragma unroll 2
+  for (; k + 8 <= K; k += 8) {
     acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.at(m0 + i, k + j), B.at(k + j, n0 + i), acc,
                                                0, 0, 0);
-  return acc;
+    acc2 = __builtin_amdgcn_mfma_f32_16x16x4f32(A.at(m0 + i, k + 4 + j), B.at(k + 4 + j, n0 + i),
+                                                acc2, 0, 0, 0);
+  }
+  if (k < K)
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(A.at(m0 + i, k + j), B.at(k + j, n0 + i), acc,
+                                               0, 0, 0);
+  return acc + acc2;
 }
 
 struct Job {
@@ -367,9 +376,12 @@ __global__ __launch_bounds__(kTokThreads) void k_tok_bwd(
         f4 acc{0.f, 0.f, 0.f, 0.f};
         if (t < tz) {
           const int m0 = (t / (V >> 4)) << 4, n0 = (t % (V >> 4)) << 4;
-          acc = mm16(mat(dq, VP, 1), mat(W, 1, VP), m0, n0, V, i, j, acc);
-          acc = mm16(mat(dk, VP, 1), mat(W + V * VP, 1, VP), m0, n0, V, i, j, acc);
-          acc = mm16(mat(dv, VP, 1), mat(W + 2 * V * VP, 1, VP), m0, n0, V, i, j, acc);
+          // three independent chains, added at the end
+          acc = mm16(mat(dq, VP, 1), mat(W, 1, VP), m0, n0, V, i, j, acc) +
+                mm16(mat(dk, VP, 1), mat(W + V * VP, 1, VP), m0, n0, V, i, j,
+                     f4{0.f, 0.f, 0.f, 0.f}) +
+                mm16(mat(dv, VP, 1), mat(W + 2 * V * VP, 1, VP), m0, n0, V, i, j,
+                     f4{0.f, 0.f, 0.f, 0.f});
 #pragma unroll
           for (int r = 0; r < 4; ++r) to_dz(m0 + 4 * j + r, n0 + i, acc[r]);
         } else {
@@ -393,6 +405,7 @@ __global__ __launch_bounds__(kTokThreads) void k_tok_bwd(
     dUs[g * VP + c] = u;
     dUb[idx] = u;
   }
+  __shared__ float tot_s;
   {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
     for (int g = wave; g < G; g += nw) {
@@ -404,23 +417,35 @@ __global__ __launch_bounds__(kTokThreads) void k_tok_bwd(
         ds[(int64_t)bh * G + g] = d;
       }
     }
+    if (wave == nw - 1) {  // total slot mass, fixed order
+      float t = 0.f;
+      for (int g = lane; g < G; g += 64) t += ss[g];
+      t = wave_sum64(t);
+      if (lane == 0) tot_s = t;
+    }
   }
   __syncthreads();
-  // shifts: cen = [sum_g m_g zmix[g][:], sum_g m_g dU[g][:], sum_g m_g ds[g]], m_g = s_g / sum s
-  float tot = 0.f;
-  for (int g = 0; g < G; ++g) tot += ss[g];
-  const float inv = tot > 0.f ? 1.0f / tot : 0.f;
+  // shifts: cen = [sum_g m_g zmix[g][:], sum_g m_g dU[g][:], sum_g m_g ds[g]], m_g = s_g / sum s;
+  // each column is summed by 16 threads over interleaved slots, then over those threads
+  const float inv = tot_s > 0.f ? 1.0f / tot_s : 0.f;
   float* cb = cen + (int64_t)bh * (2 * V + 1);
-  for (int c = threadIdx.x; c < 2 * V + 1; c += blockDim.x) {
+  const int ncol = 2 * V + 1;
+  for (int base = 0; base < ncol * 16; base += blockDim.x) {
+    const int idx = base + threadIdx.x;
+    const int c = idx >> 4, part = idx & 15;
     float acc = 0.f;
-    if (c < V) {
-      for (int g = 0; g < G; ++g) acc += ss[g] * zms[g * VP + c];
-    } else if (c < 2 * V) {
-      for (int g = 0; g < G; ++g) acc += ss[g] * dUs[g * VP + (c - V)];
-    } else {
-      for (int g = 0; g < G; ++g) acc += ss[g] * dsl[g];
+    if (c < ncol) {
+      if (c < V) {
+        for (int g = part; g < G; g += 16) acc += ss[g] * zms[g * VP + c];
+      } else if (c < 2 * V) {
+        for (int g = part; g < G; g += 16) acc += ss[g] * dUs[g * VP + (c - V)];
+      } else {
+        for (int g = part; g < G; g += 16) acc += ss[g] * dsl[g];
+      }
     }
-    cb[c] = acc * inv;
+#pragma unroll
+    for (int off = 8; off >= 1; off >>= 1) acc += __shfl_xor(acc, off, 16);
+    if (c < ncol && part == 0) cb[c] = acc * inv;
   }
 }
 
