@@ -34,6 +34,9 @@ bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 #ifndef FS_TARGET_DESLICE
 #define FS_TARGET_DESLICE 512
 #endif
+#ifndef FS_TARGET_LONG
+#define FS_TARGET_LONG 1024
+#endif
 
 constexpr int kMaxAttnG = 256;
 constexpr int kMaxAttnGV = 8192;
@@ -87,6 +90,12 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
   // passes that write partials give every chunk at least 4 tiles per point group, so the
   // partials stay small next to the points they summarise
   chunks = std::min<int64_t>(chunks, partials ? std::max<int64_t>(1, ntiles / 4) : ntiles);
+  // long streams take twice as many workgroups where every chunk still keeps 16 tiles: the
+  // shorter per-workgroup runs shrink the tail of the last wave of workgroups
+  if (c.NS < 8 && FS_TARGET_LONG > target) {
+    const int64_t more = std::min<int64_t>((FS_TARGET_LONG + units - 1) / units, ntiles / 16);
+    chunks = std::max<int64_t>(chunks, more);
+  }
   // the kernels address a chunk's rows with 32-bit byte offsets (raw buffer loads)
   const int64_t row_bytes = (int64_t)g.H * g.D * (g.bf16 ? 2 : 4);
   const int64_t max_tiles = std::max<int64_t>(1, (((int64_t)1 << 31) - 1) / (row_bytes * step) - 1);
