@@ -4,7 +4,9 @@
 One step = fs_slice_fwd, fs_mix, fs_deslice_fwd and fs_slice_deslice_bwd (which includes the
 mix backward) over one batch of seeded synthetic inputs already resident in device memory.
 The default workload is the car-surface-scale layer (fp32, B=1, N=32768 points, H=8 heads,
-dh=32, G=32 slices, single-head token self-attention). Prints ONE JSON line.
+dh=32, G=32 slices, single-head token self-attention). Prints ONE JSON line. A forward-only
+workload (``--workload infer``: bf16, N = 2^24) times fs_slice_fwd, fs_mix and fs_deslice_fwd
+with no saved normaliser instead.
 
 Besides the step time it reports, for the dominant kernel (backward pass B), the roofline
 point from algorithmic bytes or MFMA flops per launch over its average duration measured with
@@ -25,6 +27,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = ("points/sec fused slice+deslice fwd+bwd; % HBM BW (small G) / % MFMA (large G)")
+METRIC_FWD = "points/sec fused slice+deslice forward (inference, no saved normaliser)"
 HBM_PEAK = 8.0e12
 MFMA_PEAK = {"f32": 157.3e12, "bf16": 2.5e15}
 PASS_NAMES = ("slice", "deslice", "bwd_a", "bwd_b")
@@ -36,15 +39,17 @@ MIX_NAMES = {0: "identity", 1: "fixed GxG matrix", 2: "per-token channel map",
 def pass_work(w, pass_name):
     """Algorithmic HBM bytes and MFMA flops of one streaming pass per (point, head).
 
-    bytes: the pass's point-tensor reads and writes in the storage dtype plus the 4-byte lse;
+    bytes: the pass's point-tensor reads and writes in the storage dtype plus the 4-byte lse
+    (none in the forward-only path, which neither writes nor reads it);
     flops: its dense contractions (logits 2DG, each token contraction 2GV or 2DG).
     """
     elt = 2 if w.dtype == "bf16" else 4
     D, V, G = w.D, w.V, w.G
+    lse = 0 if w.forward_only else 4
     if pass_name == "slice":      # read x, fx; write lse; logits + U
-        return (D + V) * elt + 4, 2 * D * G + 2 * G * V
+        return (D + V) * elt + lse, 2 * D * G + 2 * G * V
     if pass_name == "deslice":    # read x, lse; write out; logits + w zmix
-        return (D + V) * elt + 4, 2 * D * G + 2 * G * V
+        return (D + V) * elt + lse, 2 * D * G + 2 * G * V
     if pass_name == "bwd_a":      # read x, dout, lse; logits + w^T dout
         return (D + V) * elt + 4, 2 * D * G + 2 * G * V
     # bwd_b: read x, fx, dout, lse; write dx, dfx; logits, dw (2 GV), dfx, dx, dW_s
@@ -66,7 +71,8 @@ def measured_traffic(workload, kernel):
 
 
 def cpu_baseline(w, budget_s=10.0):
-    """The fp64 oracle (unchanged) on the same workload, timed on the host cores."""
+    """The fp64 oracle (unchanged) on the same workload, timed on the host cores. A workload
+    built from a repeated block is sampled on one block (its points per second)."""
     try:
         libc = ctypes.CDLL("libc.so.6")
         libc.mallopt(-4, 0)
@@ -79,17 +85,20 @@ def cpu_baseline(w, budget_s=10.0):
     import workloads
     with threadpool_limits(threads):
         used = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-        inp = workloads.make_inputs(w)
+        inp = workloads.make_inputs(w, with_grad=not w.forward_only)
         runs, t_total = 0, 0.0
         while runs == 0 or (t_total < budget_s and runs < 500):
             t0 = time.perf_counter()
-            oracle.run_inputs(inp, w.mix, w.eps)
+            oracle.run_inputs(inp, w.mix, w.eps, backward_too=not w.forward_only)
             t_total += time.perf_counter() - t0
             runs += 1
-    pts = w.B * w.N * runs
+    n = w.block_N or w.N
+    pts = w.B * n * runs
+    what = "whole workload" if not w.block_N else "one seeded block"
     return {"value": pts / t_total, "unit": "points/s", "cores": used, "kind": "oracle",
-            "sample": f"whole workload (B={w.B}, N={w.N}, all {w.H} heads), forward + "
-                      f"backward in fp64, {runs} run(s), {t_total:.1f} s",
+            "sample": f"{what} (B={w.B}, N={n}, all {w.H} heads), "
+                      f"{'forward' if w.forward_only else 'forward + backward'} in fp64, "
+                      f"{runs} run(s), {t_total:.1f} s",
             "cpu": platform.processor() or platform.machine()}
 
 
@@ -128,8 +137,11 @@ def main():
         del src, dst
 
     w = workloads.WORKLOADS[args.workload]
-    inp = workloads.make_inputs(w)
-    pb = PathBuffers(inp, w.mix, w.dtype, w.eps)
+    fwd_only = w.forward_only
+    inp = workloads.make_inputs(w, with_grad=not fwd_only)
+    pb = PathBuffers(inp, w.mix, w.dtype, w.eps, with_backward=not fwd_only, repeat=w.repeat,
+                     keep_lse=not fwd_only)
+    del inp
     dev = pb.dev
     stream = torch.cuda.current_stream(dev)
 
@@ -172,21 +184,22 @@ def main():
 
     # per-kernel durations: events recorded around each streaming kernel's launch, on its
     # stream, over the same number of eager steps
+    npass = 2 if fwd_only else 4
     ev = {p: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.steps)] for p in range(4)}
-    for p in range(4):      # torch creates the underlying hipEvent_t on first record
+              for _ in range(args.steps)] for p in range(npass)}
+    for p in range(npass):  # torch creates the underlying hipEvent_t on first record
         for a, b in ev[p]:
             a.record(stream)
             b.record(stream)
     torch.cuda.synchronize(dev)
     for k in range(args.steps):
-        for p in range(4):
+        for p in range(npass):
             fs.set_pass_events(p, ev[p][k][0], ev[p][k][1])
         pb.step()
     fs.set_pass_events(-1)
     torch.cuda.synchronize(dev)
     pass_us = {PASS_NAMES[p]: 1e3 * float(np.mean([a.elapsed_time(b) for a, b in ev[p]]))
-               for p in range(4)}
+               for p in range(npass)}
 
     units = w.B * w.N * w.H   # (point, head) pairs per launch
     dom = max(pass_us, key=pass_us.get)
@@ -206,10 +219,14 @@ def main():
     roof["per_launch"] = {"units": units, "algorithmic_bytes": byt * units,
                           "algorithmic_flops": flp * units, "avg_duration_us": pass_us[dom]}
 
-    # whole step against the path's own ceilings (4 passes)
+    # whole step against the path's own ceilings (4 passes; 2 in the forward-only path)
     elt = 2 if w.dtype == "bf16" else 4
-    step_bytes = ((5 * w.D + 6 * w.V) * elt + 12) * units
-    step_flops = 12 * w.G * (w.D + w.V) * units
+    if fwd_only:
+        step_bytes = (2 * w.D + 2 * w.V) * elt * units
+        step_flops = 4 * w.G * (w.D + w.V) * units
+    else:
+        step_bytes = ((5 * w.D + 6 * w.V) * elt + 12) * units
+        step_flops = 12 * w.G * (w.D + w.V) * units
     t_step = ms_step * 1e-3
     step_roof = {"hbm_frac": step_bytes / t_step / HBM_PEAK,
                  "mfma_frac": step_flops / t_step / MFMA_PEAK[w.dtype],
@@ -218,7 +235,7 @@ def main():
 
     value = w.B * w.N / t_step
     out = {
-        "metric": METRIC, "value": value, "unit": "points/s", "n_gpus": 1,
+        "metric": METRIC_FWD if fwd_only else METRIC, "value": value, "unit": "points/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": w.dtype, "data": "synthetic",
@@ -229,6 +246,10 @@ def main():
         "passes_us": pass_us,
         "wall_s_timed": wall,
     }
+    if fwd_only:
+        out["config"]["forward_only"] = True
+    if w.block_N:
+        out["config"]["points"] = f"{w.repeat} copies of one seeded {w.block_N}-point block"
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out), flush=True)

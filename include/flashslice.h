@@ -130,10 +130,23 @@ int fs_mix_bwd(const fs_problem* prob, const fs_mix_desc* mix, const float* z,
                void* ws, size_t ws_bytes, void* hip_stream);
 
 /* Deslice (paper: Sec. 2, u_i = sum_g w_ig z'_g; App. F.1): recompute the weights from x and
- * lse (required) and write out (B,N,H,V) = w zmix in the storage dtype.                     */
+ * write out (B,N,H,V) = w zmix in the storage dtype. lse (B,H,N) is the base-2 normaliser
+ * saved by fs_slice_fwd; nullable: the kernel then recomputes each point's normaliser from its
+ * logits (as fs_deslice_stats_fwd without the lse output).                                 */
 int fs_deslice_fwd(const fs_problem* prob, const void* x, const float* Ws, const float* bias,
                    const float* tau, const float* zmix, const float* lse, void* out,
                    void* hip_stream);
+
+/* Deslice with no saved normaliser, for a forward that runs no slice pass before it (forward
+ * only inference; Sec. 2 and App. F.1, the per-point softmax over the G slots of Eq. (1)).
+ * The maximum and the sum over the slots are formed per point inside the deslice kernel, the
+ * weights normalised with them, and out (B,N,H,V) written as in fs_deslice_fwd.
+ * lse_out (B,H,N) fp32, nullable: receives the base-2 normaliser of every point, the same
+ * quantity fs_slice_fwd writes, for a later fs_slice_deslice_bwd. It must not overlap any
+ * input or out (FS_ERR_ALIAS).                                                              */
+int fs_deslice_stats_fwd(const fs_problem* prob, const void* x, const float* Ws,
+                         const float* bias, const float* tau, const float* zmix, float* lse_out,
+                         void* out, void* hip_stream);
 
 /* Backward of slice -> mix -> deslice for the upstream gradient dout (B,N,H,V).
  * Inputs are the forward's inputs and saved z, s, zmix, attn_probs (ATTN only), lse.

@@ -218,6 +218,41 @@ def forward(x, fx, Ws, b, tau, kind, prm: Optional[Dict] = None, eps=1e-5,
     return res
 
 
+def forward_repeated(x, fx, Ws, b, tau, kind, prm: Optional[Dict], eps, repeat, points,
+                     pairs=None) -> Dict[str, np.ndarray]:
+    """Forward over the point set made of ``repeat`` back-to-back copies of the given block of
+    points (full N = repeat * block), evaluated from the block alone: each copy contributes
+    the same terms to s = sum_n w[n, :] and U = w^T F, so both are ``repeat`` times the
+    block's sums, and a point's weights, lse and output depend only on its own row.
+
+    points: full-size point indices (copy k of block point n is point k * block + n).
+    Returns z, s, zmix (B, H, G[, V]), P, and lse (B, H, len(points)), out (B, len(points),
+    H, V) at those points; entries of pairs not listed stay zero.
+    """
+    prm = prm or {}
+    B, Nb, H, D = x.shape
+    V = fx.shape[3]
+    G = np.asarray(Ws).shape[-1]
+    idx = np.asarray(points, dtype=np.int64) % Nb
+    res = {k: np.zeros(sh) for k, sh in dict(
+        z=(B, H, G, V), s=(B, H, G), zmix=(B, H, G, V), lse=(B, H, len(idx)),
+        out=(B, len(idx), H, V)).items()}
+    res["P"] = np.zeros((B, H, G, G)) if kind == MIX_ATTN else None
+    for bb, h in _pairs(B, H, pairs):
+        X = np.asarray(x[bb, :, h, :], dtype=f64)
+        F = np.asarray(fx[bb, :, h, :], dtype=f64)
+        Wsh, bh = _ws_b(Ws, b, h)
+        w, lse = slot_softmax(logits(X, Wsh, bh, f64(tau[h])))
+        s, U, z = slice_tokens(f64(repeat) * w, F, f64(eps))
+        zm, P = mix_forward(kind, z, _head_params(kind, prm, h))
+        res["z"][bb, h], res["s"][bb, h], res["zmix"][bb, h] = z, s, zm
+        if P is not None:
+            res["P"][bb, h] = P
+        res["lse"][bb, h] = lse[idx]
+        res["out"][bb, :, h, :] = deslice(w[idx], zm)
+    return res
+
+
 def backward(x, fx, Ws, b, tau, kind, prm: Optional[Dict], dout, eps=1e-5,
              fwd: Optional[Dict] = None, pairs=None, dtype=f64) -> Dict[str, np.ndarray]:
     """Backward of the path for the upstream gradient dout (B, N, H, V) (over all samples and

@@ -16,7 +16,7 @@ from typing import Optional
 __all__ = [
     "F32", "BF16", "MIX_IDENTITY", "MIX_LINEAR_G", "MIX_LINEAR_C", "MIX_ATTN",
     "FsError", "Problem", "MixDesc", "lib", "lib_path", "workspace_bytes", "slice_fwd", "mix",
-    "mix_bwd", "deslice_fwd", "slice_deslice_bwd", "status_string", "last_hip_error",
+    "mix_bwd", "deslice_fwd", "deslice_stats_fwd", "slice_deslice_bwd", "status_string", "last_hip_error",
     "set_pass_events", "EXPORTED", "PASS_SLICE", "PASS_DESLICE", "PASS_BWD_A", "PASS_BWD_B",
 ]
 
@@ -24,7 +24,7 @@ F32, BF16 = 0, 1
 MIX_IDENTITY, MIX_LINEAR_G, MIX_LINEAR_C, MIX_ATTN = 0, 1, 2, 3
 
 EXPORTED = ("fs_workspace_bytes", "fs_slice_fwd", "fs_mix", "fs_mix_bwd", "fs_deslice_fwd",
-            "fs_slice_deslice_bwd", "fs_set_pass_events", "fs_status_string",
+            "fs_deslice_stats_fwd", "fs_slice_deslice_bwd", "fs_set_pass_events", "fs_status_string",
             "fs_last_hip_error")
 
 PASS_SLICE, PASS_DESLICE, PASS_BWD_A, PASS_BWD_B = 0, 1, 2, 3
@@ -89,6 +89,7 @@ def lib() -> ctypes.CDLL:
         L.fs_mix.argtypes = [prob, mixp, P, P, P, P]
         L.fs_mix_bwd.argtypes = [prob, mixp, P, P, P, P, P, P, S, P]
         L.fs_deslice_fwd.argtypes = [prob, P, P, P, P, P, P, P, P]
+        L.fs_deslice_stats_fwd.argtypes = [prob, P, P, P, P, P, P, P, P]
         L.fs_slice_deslice_bwd.argtypes = [prob, mixp] + [P] * 19 + [S, P]
         L.fs_status_string.argtypes = [ctypes.c_int]
         L.fs_status_string.restype = ctypes.c_char_p
@@ -177,6 +178,13 @@ def deslice_fwd(prob, x, Ws, b, tau, zmix, lse, out, stream=None) -> None:
     _check(lib().fs_deslice_fwd(ctypes.byref(prob), _ptr(x), _ptr(Ws), _ptr(b), _ptr(tau),
                                 _ptr(zmix), _ptr(lse), _ptr(out), _stream(stream)),
            "fs_deslice_fwd")
+
+
+def deslice_stats_fwd(prob, x, Ws, b, tau, zmix, lse_out, out, stream=None) -> None:
+    _check(lib().fs_deslice_stats_fwd(ctypes.byref(prob), _ptr(x), _ptr(Ws), _ptr(b),
+                                      _ptr(tau), _ptr(zmix), _ptr(lse_out), _ptr(out),
+                                      _stream(stream)),
+           "fs_deslice_stats_fwd")
 
 
 def slice_deslice_bwd(prob, mixdesc, x, fx, Ws, b, tau, z, s, zmix, attn, lse, dout, dx, dfx,

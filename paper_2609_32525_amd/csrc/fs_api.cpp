@@ -401,11 +401,27 @@ int fs_deslice_fwd(const fs_problem* prob, const void* x, const float* Ws, const
   if (st != FS_OK) return st;
   const Sizes zs = sizes(g);
   const Buf in[] = {{x, zs.x, true},     {Ws, zs.Ws, true},     {bias, zs.b, true},
-                    {tau, zs.tau, true}, {zmix, zs.tok, true},  {lse, zs.lse, true}};
+                    {tau, zs.tau, true}, {zmix, zs.tok, true},  {lse, zs.lse, false}};
   const Buf outb[] = {{out, zs.fx, true}};
   st = check_bufs(in, 6, outb, 1);
   if (st != FS_OK) return st;
-  return hip_status(fs::launch_deslice(g, x, Ws, bias, tau, zmix, lse, out,
+  return hip_status(fs::launch_deslice(g, x, Ws, bias, tau, zmix, lse, nullptr, out,
+                                       static_cast<hipStream_t>(hip_stream)));
+}
+
+int fs_deslice_stats_fwd(const fs_problem* prob, const void* x, const float* Ws,
+                         const float* bias, const float* tau, const float* zmix, float* lse_out,
+                         void* out, void* hip_stream) {
+  Geom g;
+  int st = check_problem(prob, &g);
+  if (st != FS_OK) return st;
+  const Sizes zs = sizes(g);
+  const Buf in[] = {{x, zs.x, true},     {Ws, zs.Ws, true},   {bias, zs.b, true},
+                    {tau, zs.tau, true}, {zmix, zs.tok, true}};
+  const Buf outb[] = {{out, zs.fx, true}, {lse_out, zs.lse, false}};
+  st = check_bufs(in, 5, outb, 2);
+  if (st != FS_OK) return st;
+  return hip_status(fs::launch_deslice(g, x, Ws, bias, tau, zmix, nullptr, lse_out, out,
                                        static_cast<hipStream_t>(hip_stream)));
 }
 

@@ -137,8 +137,8 @@ hipError_t launch_slice(const Geom& g, const void* x, const void* fx, const floa
                         const float* bias, const float* tau, float* z, float* s, float* lse,
                         char* ws, hipStream_t st);
 hipError_t launch_deslice(const Geom& g, const void* x, const float* Ws, const float* bias,
-                          const float* tau, const float* zmix, const float* lse, void* out,
-                          hipStream_t st);
+                          const float* tau, const float* zmix, const float* lse, float* lse_out,
+                          void* out, hipStream_t st);
 hipError_t launch_mix(const Geom& g, const MixArgs& m, const float* z, float* zmix,
                       float* attn, hipStream_t st);
 // dz = Mix^T(dzm); with s given also dU = dz / (s + eps), ds and the slot-mean shifts cen

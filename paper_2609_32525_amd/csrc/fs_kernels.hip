@@ -81,15 +81,16 @@ hipError_t launch_slice(const Geom& g, const void* x, const void* fx, const floa
 }
 
 hipError_t launch_deslice(const Geom& g, const void* x, const float* Ws, const float* bias,
-                          const float* tau, const float* zmix, const float* lse, void* out,
-                          hipStream_t st) {
+                          const float* tau, const float* zmix, const float* lse, float* lse_out,
+                          void* out, hipStream_t st) {
   PassArgs a = base_args(g, PASS_DESLICE);
   a.x = x;
   a.Ws = Ws;
   a.bias = bias;
   a.tau = tau;
   a.zmix = zmix;
-  a.lse_in = lse;
+  a.lse_in = lse;      // null: the deslice computes the softmax statistics itself
+  a.lse_out = lse_out;  // with lse null only; nullable
   a.out = out;
   return timed(PASS_DESLICE, st, [&] { return run_pass_deslice(g, a, st); });
 }

@@ -1,4 +1,5 @@
-// Streaming pass: deslice (logits, w = exp2(a - lse), out = w zmix).
+// Streaming pass: deslice (logits, w = exp2(a - lse), out = w zmix), and the deslice that
+// computes the per-point softmax statistics itself (no lse input; optionally writes lse).
 // Kernel design and MFMA lane layouts are described at the top of fs_stream.h.
 
 #include "fs_stream.h"
@@ -7,9 +8,10 @@ namespace fs {
 namespace {
 
 // =======================================================================================
-// Deslice pass
+// Deslice pass. ST: the normaliser of every point is computed here from the logits (max and
+// sum over the slot groups, combined across the NS slot waves through LDS) instead of read.
 // =======================================================================================
-template <bool BF, int D, int GS, int NS, int NP>
+template <bool BF, int D, int GS, int NS, int NP, bool ST>
 __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_DESLICE))) void k_deslice(
     PassArgs a) {
   constexpr int GB = GS / 16, VB = D / 16;
@@ -21,7 +23,8 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   const int64_t rs = (int64_t)a.H * D;
   const T* xb = (const T*)a.x + c.off;
   T* ob = (T*)a.out + c.off;
-  const float* lse = a.lse_in + (int64_t)c.bh * a.N;
+  const float* lse = (ST ? a.lse_out : a.lse_in) + (int64_t)c.bh * a.N;
+  const bool want_lse = !ST || a.lse_out != nullptr;
 
   SlotOp<BF, D, GB> wop;
   load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, c.sc, i, j);
@@ -34,6 +37,9 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   load_gop<BF, GB, VB, false>(zop, a.zmix + (int64_t)c.bh * a.G * D, D, c.g0, 1.0f, i, j);
 
   __shared__ f4 ox[NS > 1 ? NP : 1][NS > 1 ? NS : 1][VB][2][64];
+  constexpr int SX = ST && NS > 1;
+  __shared__ float st_m[SX ? 2 : 1][SX ? NP : 1][SX ? NS : 1][32];
+  __shared__ float st_l[SX ? 2 : 1][SX ? NP : 1][SX ? NS : 1][32];
 
   const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
@@ -42,7 +48,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   const int rsb = (int)(rs * sizeof(T));
   const auto rx = rows_rsrc(xb + pbeg * rs, npts, (int)rs, D);
   const auto ro = rows_rsrc(ob + pbeg * rs, npts, (int)rs, D);
-  const auto rl = rows_rsrc(lse + pbeg, npts, 1, 1);
+  const auto rl = rows_rsrc(want_lse ? lse + pbeg : a.Ws, npts, 1, 1);
   const int wpu = __builtin_amdgcn_readfirstlane(wp);
 
   struct Tile {
@@ -54,14 +60,16 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) {
       load_row_buf<BF, D>(tt.xo[pb], rx, i * rsb, (tb + 16 * pb) * rsb, j);
-      const float l = bld32(rl, 4 * i, 4 * (tb + 16 * pb));
-      tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
+      if constexpr (!ST) {
+        const float l = bld32(rl, 4 * i, 4 * (tb + 16 * pb));
+        tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
+      }
     }
   };
   pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_DESLICE), Tile>(ntile, load_tile, [&](Tile& cur, int t) {
     const int tb = (t * NP + wpu) * 32;
     const RowOp<BF, D>* xo = cur.xo;
-    const float* lse2 = cur.lse2;
+    [[maybe_unused]] const float* lse2 = cur.lse2;
     f4 w[GB][2];
 #pragma unroll
     for (int gb = 0; gb < GB; ++gb)
@@ -69,10 +77,77 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
       for (int pb = 0; pb < 2; ++pb) {
         f4 acc = f4{bT[gb][0], bT[gb][1], bT[gb][2], bT[gb][3]};
         acc = mm_slot_row<BF, D, GB, SPLIT>(wop, gb, xo[pb], acc);
+        if constexpr (!ST) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) acc[r] = __builtin_amdgcn_exp2f(acc[r] - lse2[pb]);
+          for (int r = 0; r < 4; ++r) acc[r] = __builtin_amdgcn_exp2f(acc[r] - lse2[pb]);
+        }
         w[gb][pb] = acc;
       }
+    if constexpr (ST) {
+      // T-layout: lane (i, j) holds slots 4 j + r of point 16 pb + i; reduce over gb and r in
+      // the lane, over j across the four 16-lane rows, then over the slot waves
+      float m[2], l[2];
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb) {
+        float mx = w[0][pb][0];
+#pragma unroll
+        for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) mx = vmax(mx, w[gb][pb][r]);
+        mx = vmax(mx, __shfl_xor(mx, 16));
+        m[pb] = vmax(mx, __shfl_xor(mx, 32));
+        float sum = 0.f;
+#pragma unroll
+        for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float e = __builtin_amdgcn_exp2f(w[gb][pb][r] - m[pb]);
+            w[gb][pb][r] = e;
+            sum += e;
+          }
+        l[pb] = col4_sum(sum);
+      }
+      float f[2], ls2[2];
+      if constexpr (NS == 1) {
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) {
+          f[pb] = __builtin_amdgcn_rcpf(l[pb]);
+          ls2[pb] = m[pb] + __log2f(l[pb]);
+        }
+      } else {
+        const int par = t & 1;
+        if (j == 0) {
+#pragma unroll
+          for (int pb = 0; pb < 2; ++pb) {
+            st_m[par][wp][ws][16 * pb + i] = m[pb];
+            st_l[par][wp][ws][16 * pb + i] = l[pb];
+          }
+        }
+        __syncthreads();
+        // lane p < 32 combines the slot waves' statistics of point p; every lane then fetches
+        // the combined values of its own points
+        float Mp = st_m[par][wp][0][lane & 31];
+#pragma unroll
+        for (int s = 1; s < NS; ++s) Mp = vmax(Mp, st_m[par][wp][s][lane & 31]);
+        float Lp = 0.f;
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+          Lp += st_l[par][wp][s][lane & 31] * __builtin_amdgcn_exp2f(st_m[par][wp][s][lane & 31] - Mp);
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) {
+          const float M = __shfl(Mp, 16 * pb + i);
+          const float L = __shfl(Lp, 16 * pb + i);
+          f[pb] = __builtin_amdgcn_exp2f(m[pb] - M) * __builtin_amdgcn_rcpf(L);
+          ls2[pb] = M + __log2f(L);
+        }
+      }
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb) {
+#pragma unroll
+        for (int gb = 0; gb < GB; ++gb) w[gb][pb] *= f[pb];
+        if (want_lse && ws == 0 && j == 0) bst32(rl, ls2[pb], 4 * (16 * pb + i), 4 * tb);
+      }
+    }
     f4 o[VB][2];
     const TileB<BF, GB, 2> wt = tile_b<BF, GB, 2>(w);
 #pragma unroll
@@ -107,19 +182,23 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   });
 }
 
-template <bool BF, int D, int GS, int NS, int NP, int PB>
-struct Run_k_deslice {
-  static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
-    dim3 grid(cfg.chunks * BH * cfg.nblk);
-    hipLaunchKernelGGL((k_deslice<BF, D, GS, NS, NP>), grid, dim3(64 * NS * NP), 0, st, a);
-    return hipGetLastError();
-  }
+template <bool ST>
+struct Run_k_deslice_ {
+  template <bool BF, int D, int GS, int NS, int NP, int PB>
+  struct R {
+    static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
+      dim3 grid(cfg.chunks * BH * cfg.nblk);
+      hipLaunchKernelGGL((k_deslice<BF, D, GS, NS, NP, ST>), grid, dim3(64 * NS * NP), 0, st, a);
+      return hipGetLastError();
+    }
+  };
 };
 
 }  // namespace
 
 hipError_t run_pass_deslice(const Geom& g, const PassArgs& a, hipStream_t st) {
-  return run_pass_tilings<PASS_DESLICE, Run_k_deslice>(g, a, st);
+  if (a.lse_in == nullptr) return run_pass_tilings<PASS_DESLICE, Run_k_deslice_<true>::R>(g, a, st);
+  return run_pass_tilings<PASS_DESLICE, Run_k_deslice_<false>::R>(g, a, st);
 }
 
 }  // namespace fs

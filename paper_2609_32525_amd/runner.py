@@ -18,18 +18,26 @@ class PathBuffers:
 
     inp: dict of fp32 numpy arrays holding the exact stored values (x, fx, Ws, b, tau, the
     mix parameters, scale, dout), as produced by the seeded input generators.
+    repeat: the device copies of x and fx (and dout) hold ``repeat`` back-to-back copies of the
+    given points along N.
+    keep_lse: False runs the forward with no saved normaliser (the slice writes no lse and
+    the deslice recomputes it); only with with_backward=False.
     """
 
     def __init__(self, inp: Dict, kind: int, dtype: str = "f32", eps: float = 1e-5,
-                 device: str = "cuda:0", with_backward: bool = True):
+                 device: str = "cuda:0", with_backward: bool = True, repeat: int = 1,
+                 keep_lse: bool = True):
         import torch
         self.torch = torch
         self.dev = torch.device(device)
         self.kind = kind
         sdt = torch.bfloat16 if dtype == "bf16" else torch.float32
         self.sdt = sdt
+        if with_backward and not keep_lse:
+            raise ValueError("the backward needs the saved lse")
         x = inp["x"]
         B, N, H, D = x.shape
+        N *= repeat
         V = inp["fx"].shape[3]
         Ws = np.asarray(inp["Ws"])
         G = Ws.shape[-1]
@@ -40,8 +48,12 @@ class PathBuffers:
         def up(a, dt=torch.float32):
             return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(self.dev).to(dt)
 
-        self.x = up(x, sdt)
-        self.fx = up(inp["fx"], sdt)
+        def up_points(a):
+            t = up(a, sdt)
+            return t.repeat(1, repeat, 1, 1) if repeat > 1 else t
+
+        self.x = up_points(x)
+        self.fx = up_points(inp["fx"])
         self.Ws = up(Ws)
         self.b = up(inp["b"])
         self.tau = up(inp["tau"])
@@ -60,13 +72,13 @@ class PathBuffers:
         self.s = torch.empty((B, H, G), **f32)
         self.zmix = torch.empty((B, H, G, V), **f32)
         self.attn = torch.empty((B, H, G, G), **f32) if kind == MIX_ATTN else None
-        self.lse = torch.empty((B, H, N), **f32)
+        self.lse = torch.empty((B, H, N), **f32) if keep_lse else None
         self.out = torch.empty((B, N, H, V), device=self.dev, dtype=sdt)
         self.ws_f = torch.empty(max(1, workspace_bytes(self.prob, False)), device=self.dev,
                                 dtype=torch.uint8)
         self.with_backward = with_backward
         if with_backward:
-            self.dout = up(inp["dout"], sdt)
+            self.dout = up_points(inp["dout"])
             self.dx = torch.empty((B, N, H, D), device=self.dev, dtype=sdt)
             self.dfx = torch.empty((B, N, H, V), device=self.dev, dtype=sdt)
             self.dWs = torch.empty_like(self.Ws)

@@ -205,3 +205,30 @@ def test_backward_validation():
     # the mix backward alone
     assert L.fs_mix_bwd(ctypes.byref(p), ctypes.byref(lin), f(), None, f(), f(), f(), f(), 0,
                         None) == WS
+
+
+def test_deslice_validation():
+    # every call below fails validation before any launch
+    f = Fake()
+    L = fs.lib()
+    p = prob()
+
+    def call(fn, **over):
+        a = {k: f() for k in ("x", "Ws", "b", "tau", "zmix", "lse", "out")}
+        a.update(over)
+        return getattr(L, fn)(ctypes.byref(p), a["x"], a["Ws"], a["b"], a["tau"], a["zmix"],
+                              a["lse"], a["out"], None)
+
+    for fn in ("fs_deslice_fwd", "fs_deslice_stats_fwd"):
+        assert call(fn, x=None) == NULL
+        assert call(fn, out=None) == NULL
+        assert call(fn, zmix=f(8)) == ALIGN
+        x = f()
+        assert call(fn, x=x, out=x + 256) == ALIAS
+        # lse is optional for both: a NULL lse still reaches the later checks
+        assert call(fn, lse=None, out=None) == NULL
+    lse = f()
+    assert call("fs_deslice_stats_fwd", lse=lse, out=lse + 512) == ALIAS   # two outputs overlap
+    zm = f()
+    assert call("fs_deslice_stats_fwd", zmix=zm, lse=zm) == ALIAS           # lse output on an input
+    assert call("fs_deslice_stats_fwd", lse=f(4)) == ALIGN

@@ -328,10 +328,29 @@ def check_temperature_identity(o):
     assert np.abs(lhs).max() > 1e-4
 
 
+def check_repeated_block(o):
+    """forward_repeated (the full-size forward of a point set built from repeated copies of
+    one block, evaluated from the block) against the plain forward on the explicitly tiled
+    point set, at every point, for every mix."""
+    for kind in MIXES:
+        x, fx, Ws, b, tau, rng = _problem(B=2, N=11, H=2, D=4, V=3, G=5, seed=21 + kind)
+        prm = _prm(kind, 5, 3, rng)
+        rep = 3
+        full = o.forward(np.tile(x, (1, rep, 1, 1)), np.tile(fx, (1, rep, 1, 1)), Ws, b, tau,
+                         kind, prm, eps=0.05)
+        pts = np.arange(11 * rep)
+        r = o.forward_repeated(x, fx, Ws, b, tau, kind, prm, 0.05, rep, pts)
+        for k in ("z", "s", "zmix", "lse", "out"):
+            np.testing.assert_allclose(r[k], full[k], rtol=1e-12, atol=1e-13, err_msg=k)
+        if kind == o.MIX_ATTN:
+            np.testing.assert_allclose(r["P"], full["P"], rtol=1e-12, atol=1e-13)
+
+
 ALL_CHECKS = [check_partition_of_unity, check_single_slice_mean, check_identical_points,
               check_constant_tokens, check_zero_logits, check_hard_assignment,
               check_bruteforce, check_invariances, check_mix_closed_forms,
-              check_finite_differences, check_cancellation, check_temperature_identity]
+              check_finite_differences, check_cancellation, check_temperature_identity,
+              check_repeated_block]
 
 
 @pytest.mark.parametrize("check", ALL_CHECKS, ids=lambda c: c.__name__)

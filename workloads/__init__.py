@@ -21,7 +21,15 @@ stressG    bf16    1      262144     8   32  G     per-head tau ~ U[0.3, 1.0]; W
                                                    pre-temperature logit std 3; G in
                                                    {128, 256, 512, 1024}
 stack      f32     4      131072     8   32  64    fixed G x G matrix (one layer's path)
+infer      bf16    1      2^24       8   32  64    fixed G x G matrix; forward only; the
+                                                   points are 16 copies of one seeded
+                                                   2^20-point block
 =========  ======  =====  =========  ==  ==  ====  =====================================
+
+A workload with ``block_N`` set draws only ``block_N`` points; the full point set is that block
+repeated ``N / block_N`` times along N (done by whoever uploads it). The sums over points are
+then exactly ``N / block_N`` times the block's sums, which lets the oracle check the full size
+from the block alone.
 """
 from __future__ import annotations
 
@@ -56,6 +64,12 @@ class Workload:
     ws_mode: str = "xavier"     # "xavier" or "std3" (pre-temperature logit std 3)
     ws_per_head: bool = False
     a_per_head: bool = False
+    block_N: int = 0            # > 0: draw this many points, repeated N / block_N times
+    forward_only: bool = False  # inference: no backward, no saved lse
+
+    @property
+    def repeat(self) -> int:
+        return self.N // self.block_N if self.block_N else 1
 
     def scaled(self, **kw) -> "Workload":
         return dataclasses.replace(self, **kw)
@@ -71,6 +85,8 @@ WORKLOADS: Dict[str, Workload] = {
     "volume": Workload("volume", 2, "bf16", 1, 1 << 20, 8, 32, 32, 64, MIX_LINEAR_G),
     "stack": Workload("stack", 4, "f32", 4, 1 << 17, 8, 32, 32, 64, MIX_LINEAR_G),
 }
+WORKLOADS["infer"] = Workload("infer", 5, "bf16", 1, 1 << 24, 8, 32, 32, 64, MIX_LINEAR_G,
+                             block_N=1 << 20, forward_only=True)
 for _g in (128, 256, 512, 1024):
     WORKLOADS[f"stress{_g}"] = Workload(f"stress{_g}", 3, "bf16", 1, 1 << 18, 8, 32, 32, _g,
                                         MIX_LINEAR_G, tau_mode="uniform", ws_mode="std3")
@@ -113,10 +129,14 @@ def _xavier(rng, shape, fan_in, fan_out) -> np.ndarray:
 def make_inputs(w: Workload, with_grad: bool = True) -> Dict[str, Optional[np.ndarray]]:
     """All inputs of one forward + backward as fp32 numpy arrays (exact stored values).
 
-    Keys: x (B,N,H,D), fx (B,N,H,V), Ws (D,G) or (H,D,G), b (G) or (H,G), tau (H),
+    Keys: x (B,N,H,D), fx (B,N,H,V) (N = block_N when set), Ws (D,G) or (H,D,G), b (G) or (H,G), tau (H),
     A (G,G) or (H,G,G) for the fixed token matrix, Wc (V,V), Wq/Wk/Wv (V,V), scale, dout.
     """
     B, N, H, D, V, G = w.B, w.N, w.H, w.D, w.V, w.G
+    if w.block_N:
+        if N % w.block_N:
+            raise ValueError("N must be a multiple of block_N")
+        N = w.block_N
     x = _store(w, _normal(_rng(w, _K_X), (B, N, H, D)))
     fx = _store(w, _normal(_rng(w, _K_F), (B, N, H, V)))
     ws_shape = (H, D, G) if w.ws_per_head else (D, G)
