@@ -40,8 +40,8 @@
  *   - Results are deterministic: no atomics; every reduction has a fixed order, so repeated
  *     calls give bitwise identical outputs.
  *   - Supported shapes: D == V in {16, 32, 64}; G a power of two in [16, 1024] (fp32
- *     storage) or [32, 1024] (bf16 storage); attention mix for G <= 256 and G * V <= 8192;
- *     B * H <= 65535. Anything else returns FS_ERR_UNSUPPORTED.
+ *     storage) or [32, 1024] (bf16 storage), for every mix kind; B * H <= 65535. Anything
+ *     else returns FS_ERR_UNSUPPORTED.
  *   - Concurrent calls are safe as long as they do not share a workspace.
  */
 #ifndef FLASHSLICE_H
@@ -117,7 +117,7 @@ int fs_slice_fwd(const fs_problem* prob, const void* x, const void* fx, const fl
 
 /* Token mix (paper: Sec. 2; Eq. (1); the attention-free variant). z, zmix: (B,H,G,V).
  * attn_probs: (B,H,G,G) output, required for FS_MIX_ATTN (saved for the backward),
- * ignored otherwise.                                                                        */
+ * ignored otherwise. Needs no workspace for any G (attention up to G = 1024 included).      */
 int fs_mix(const fs_problem* prob, const fs_mix_desc* mix, const float* z, float* zmix,
            float* attn_probs, void* hip_stream);
 

@@ -38,8 +38,6 @@ bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 #define FS_TARGET_LONG 1024
 #endif
 
-constexpr int kMaxAttnG = 256;
-constexpr int kMaxAttnGV = 8192;
 }  // namespace
 
 PassEvents& pass_events() {
@@ -160,7 +158,9 @@ BwdWs bwd_ws_layout(const Geom& g, int kind) {
   if (kind == FS_MIX_ATTN) per_bh = 3 * (size_t)g.V * g.V;
   off += up(sizeof(float) * (size_t)g.BH() * per_bh);
   L.scr = off;
-  off += up(kind == FS_MIX_ATTN ? 3 * tok + sizeof(float) * (size_t)g.BH() * g.G * g.G : 0);
+  off += up(kind == FS_MIX_ATTN
+                ? (attn_rows(g, kind) ? 6 : 3) * tok + sizeof(float) * (size_t)g.BH() * g.G * g.G
+                : 0);
   L.cpt = off;
   off += up(blocked(g) ? 2 * sizeof(float) * (size_t)g.BH() * (size_t)g.N : 0);
   L.img = off;
@@ -215,7 +215,6 @@ int check_mix(const fs_mix_desc* m, const Geom& g) {
   if (m->kind == FS_MIX_ATTN) {
     if (m->Wq == nullptr || m->Wk == nullptr || m->Wv == nullptr) return FS_ERR_NULL;
     if (!std::isfinite(m->scale)) return FS_ERR_ARG;
-    if (g.G > fs::kMaxAttnG || (int64_t)g.G * g.V > fs::kMaxAttnGV) return FS_ERR_UNSUPPORTED;
   }
   return FS_OK;
 }

@@ -152,6 +152,9 @@ hipError_t launch_mix_bwd(const Geom& g, const MixArgs& m, const float* z, const
 // Single-workgroup-per-(b, h) token mix kernels with every operand in LDS (fs_tokmix.hip);
 // tok_fused tells whether they apply to this problem and mix kind.
 bool tok_fused(const Geom& g, int mix_kind);
+// Attention over token sets beyond the single-workgroup LDS kernels: the row-block forward
+// (no workspace) and the backward as batched products.
+bool attn_rows(const Geom& g, int mix_kind);
 hipError_t launch_tok_fwd(const Geom& g, const MixArgs& m, const float* z, float* zmix,
                           float* attn, hipStream_t st);
 hipError_t launch_tok_bwd(const Geom& g, const MixArgs& m, const float* z, const float* s,

@@ -234,6 +234,7 @@ struct GemmDesc {
   int64_t c_rs, c_o;
   int M, N, K, nsum;
   float alpha;
+  int accumulate;  // nonzero: C += alpha * product
 };
 
 constexpr int kGemmWaves = 4;
@@ -248,7 +249,11 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_tile_gemm(GemmDesc d) {
   const int o = blockIdx.y;
   const float* Ao = d.A + (int64_t)(o % d.a_mod) * d.a_o + (int64_t)(m0 + i) * d.a_rs;
   const float* Bo = d.B + (int64_t)o * d.b_o + (int64_t)(n0 + i) * d.b_cs;
-  f4 acc = {0.f, 0.f, 0.f, 0.f};
+  // four independent accumulation chains (k steps round robin), added at the end: shorter
+  // rounding-error walks over long K and overlapping MFMA latencies
+  f4 ch[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) ch[c] = f4{0.f, 0.f, 0.f, 0.f};
   for (int sidx = 0; sidx < d.nsum; ++sidx) {
     const float* As = Ao + (int64_t)sidx * d.a_s;
     const float* Bs = Bo + (int64_t)sidx * d.b_s;
@@ -261,15 +266,21 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_tile_gemm(GemmDesc d) {
         bv[u] = Bs[(int64_t)(k + 4 * u + j) * d.b_rs];
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u], acc, 0, 0, 0);
+      for (int u = 0; u < 8; ++u)
+        ch[u & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u], ch[u & 3], 0, 0, 0);
     }
-    for (; k < d.K; k += 4)
-      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(As[(int64_t)(k + j) * d.a_cs],
-                                                 Bs[(int64_t)(k + j) * d.b_rs], acc, 0, 0, 0);
+    for (int u = 0; k < d.K; k += 4, ++u)
+      ch[u & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(As[(int64_t)(k + j) * d.a_cs],
+                                                       Bs[(int64_t)(k + j) * d.b_rs], ch[u & 3], 0,
+                                                       0, 0);
   }
+  const f4 acc = (ch[0] + ch[1]) + (ch[2] + ch[3]);
   float* Co = d.C + (int64_t)o * d.c_o + n0 + i;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) Co[(int64_t)(m0 + 4 * j + r) * d.c_rs] = d.alpha * acc[r];
+  for (int r = 0; r < 4; ++r) {
+    float* c = Co + (int64_t)(m0 + 4 * j + r) * d.c_rs;
+    *c = d.accumulate ? *c + d.alpha * acc[r] : d.alpha * acc[r];
+  }
 }
 
 static hipError_t run_gemm(const GemmDesc& d, int nout, hipStream_t st) {
@@ -345,7 +356,8 @@ __global__ __launch_bounds__(kTokGradThreads) void k_token_grads(const float* z,
 // z Wv; P = softmax_row(scale q k^T); zmix = P v. One workgroup per (b, h); q, k, v live in
 // LDS; the G x G scores live in LDS up to G = 64, otherwise in the P output buffer.
 // ---------------------------------------------------------------------------------------
-constexpr int kAttnMaxGV = 8192;
+constexpr int kAttnMaxGV = 8192;   // q, k, v of one (b, h) in LDS
+constexpr int kAttnLdsMaxG = 256;
 constexpr int kAttnLdsG = 64;
 
 __device__ void attn_project(const float* zb, const float* Wq, const float* Wk, const float* Wv,
@@ -498,6 +510,185 @@ __global__ __launch_bounds__(kThreads) void k_attn_bwd(
               ds + (int64_t)bh * G, cen + (int64_t)bh * (2 * V + 1), G, V, eps);
 }
 
+// ---------------------------------------------------------------------------------------
+// Attention among large token sets (beyond the LDS kernels' limits), any G multiple of 16.
+// Forward: one wavefront per (b, h, block of 16 token rows) computes those rows with fp32
+// MFMA and needs no workspace. With r = (z Wq) Wk^T for its rows, the scores are
+// S[g][u] = scale r_g . z_u (= scale q_g . k_u). A first sweep over the key tiles forms each
+// row's maximum and sum of exponentials, a second recomputes the scores, writes
+// P = softmax_row(S) and accumulates T = P z, and zmix = T Wv (= P v by associativity, so
+// v is never formed). Operands come from global memory (small, cache resident); LDS only
+// re-lays out 16-row intermediates between products.
+// MFMA 16x16x4 lane layout (lane = i + 16 j): A[m = i][k = j], B[k = j][n = i],
+// C[m = 4 j + r][n = i] in register r.
+// ---------------------------------------------------------------------------------------
+constexpr int kAttnRowWaves = 4;
+
+__device__ __forceinline__ void lane_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+__device__ __forceinline__ float row16_max_x(float v) {
+#pragma unroll
+  for (int off = 8; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 16));
+  return v;
+}
+__device__ __forceinline__ float row16_sum_x(float v) {
+#pragma unroll
+  for (int off = 8; off >= 1; off >>= 1) v += __shfl_xor(v, off, 16);
+  return v;
+}
+
+template <int V>
+__global__ __launch_bounds__(64 * kAttnRowWaves) void k_attn_rows(
+    const float* z, float* zmix, float* P, const float* Wq, const float* Wk, const float* Wv,
+    float scale, int G, int BH) {
+  typedef float f4 __attribute__((ext_vector_type(4)));
+  constexpr int VT = V / 16, VK = V / 4;
+  constexpr float kLog2e = 1.4426950408889634f;
+  __shared__ float stage[kAttnRowWaves][16 * V];
+  __shared__ float ptile[kAttnRowWaves][16 * 16];
+  const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
+  const int wv = threadIdx.x >> 6;
+  const int nrb = G >> 4;
+  const int64_t job = (int64_t)blockIdx.x * kAttnRowWaves + wv;
+  if (job >= (int64_t)BH * nrb) return;  // whole wavefronts; no workgroup barrier follows
+  const int bh = (int)(job / nrb), g0 = (int)(job % nrb) << 4;
+  const float* zb = z + (int64_t)bh * G * V;
+  float* Pb = P + (int64_t)bh * G * G;
+  float* sg = stage[wv];
+  float* pt = ptile[wv];
+  auto mfma = [](float a, float b, f4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  };
+  f4 acc[VT];
+  // q = z[g0 : g0 + 16] Wq
+#pragma unroll
+  for (int nt = 0; nt < VT; ++nt) acc[nt] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k0 = 0; k0 < V; k0 += 4) {
+    const float a = zb[(int64_t)(g0 + i) * V + k0 + j];
+#pragma unroll
+    for (int nt = 0; nt < VT; ++nt) acc[nt] = mfma(a, Wq[(k0 + j) * V + 16 * nt + i], acc[nt]);
+  }
+#pragma unroll
+  for (int nt = 0; nt < VT; ++nt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sg[(4 * j + r) * V + 16 * nt + i] = acc[nt][r];
+  lane_lds_sync();
+  // r = q Wk^T (B[k][n] = Wk[n][k])
+#pragma unroll
+  for (int nt = 0; nt < VT; ++nt) acc[nt] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k0 = 0; k0 < V; k0 += 4) {
+    const float a = sg[i * V + k0 + j];
+#pragma unroll
+    for (int nt = 0; nt < VT; ++nt) acc[nt] = mfma(a, Wk[(16 * nt + i) * V + k0 + j], acc[nt]);
+  }
+  lane_lds_sync();
+#pragma unroll
+  for (int nt = 0; nt < VT; ++nt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sg[(4 * j + r) * V + 16 * nt + i] = acc[nt][r];
+  lane_lds_sync();
+  // score A operand, in base-2 units: ra[kk] = scale log2(e) r[g0 + i][4 kk + j]
+  float ra[VK];
+#pragma unroll
+  for (int kk = 0; kk < VK; ++kk) ra[kk] = (scale * kLog2e) * sg[i * V + 4 * kk + j];
+  // tile ut of the scores: s[r] = S2[g0 + 4 j + r][16 ut + i]
+  auto score = [&](int ut) {
+    f4 sc = {0.f, 0.f, 0.f, 0.f};
+    const float* zu = zb + (int64_t)(16 * ut + i) * V + j;
+#pragma unroll
+    for (int kk = 0; kk < VK; ++kk) sc = mfma(ra[kk], zu[4 * kk], sc);
+    return sc;
+  };
+  // sweep 1: per-lane running max and sum over the lane's own columns, then over the row
+  float mr[4], lr[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    mr[r] = -INFINITY;
+    lr[r] = 0.f;
+  }
+  for (int ut = 0; ut < nrb; ++ut) {
+    const f4 sc = score(ut);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float mn = fmaxf(mr[r], sc[r]);
+      lr[r] = lr[r] * exp2f(mr[r] - mn) + exp2f(sc[r] - mn);
+      mr[r] = mn;
+    }
+  }
+  float M[4], invL[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    M[r] = row16_max_x(mr[r]);
+    invL[r] = 1.0f / row16_sum_x(lr[r] * exp2f(mr[r] - M[r]));
+  }
+  // sweep 2: P and T^T = z^T P^T (C layout: T[ct][r] = T[g0 + i][16 ct + 4 j + r]), in four
+  // accumulation chains (one per k step of a key tile) added at the end
+  f4 Tc[4][VT];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int ct = 0; ct < VT; ++ct) Tc[c][ct] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int ut = 0; ut < nrb; ++ut) {
+    const f4 sc = score(ut);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float p = exp2f(sc[r] - M[r]) * invL[r];
+      Pb[(int64_t)(g0 + 4 * j + r) * G + 16 * ut + i] = p;
+      pt[(4 * j + r) * 16 + i] = p;
+    }
+    lane_lds_sync();
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const float b = pt[i * 16 + 4 * c + j];   // P[g0 + i][16 ut + 4 c + j]
+      const float* zr = zb + (int64_t)(16 * ut + 4 * c + j) * V + i;
+#pragma unroll
+      for (int ct = 0; ct < VT; ++ct) Tc[c][ct] = mfma(zr[16 * ct], b, Tc[c][ct]);
+    }
+    lane_lds_sync();
+  }
+  f4 T[VT];
+#pragma unroll
+  for (int ct = 0; ct < VT; ++ct) T[ct] = (Tc[0][ct] + Tc[1][ct]) + (Tc[2][ct] + Tc[3][ct]);
+  // zmix = T Wv: A[i][k0 + j] = T[g0 + i][k0 + j] through LDS
+#pragma unroll
+  for (int ct = 0; ct < VT; ++ct)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sg[i * V + 16 * ct + 4 * j + r] = T[ct][r];
+  lane_lds_sync();
+#pragma unroll
+  for (int nt = 0; nt < VT; ++nt) acc[nt] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int k0 = 0; k0 < V; k0 += 4) {
+    const float a = sg[i * V + k0 + j];
+#pragma unroll
+    for (int nt = 0; nt < VT; ++nt) acc[nt] = mfma(a, Wv[(k0 + j) * V + 16 * nt + i], acc[nt]);
+  }
+  float* zo = zmix + ((int64_t)bh * G + g0) * V;
+#pragma unroll
+  for (int nt = 0; nt < VT; ++nt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) zo[(4 * j + r) * V + 16 * nt + i] = acc[nt][r];
+}
+
+// dS = P * (dP - rowsum(dP * P)) in place over dP, one wavefront per row of one (b, h).
+__global__ __launch_bounds__(256) void k_attn_ds(const float* P, float* dS, int64_t rows,
+                                                 int G) {
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const float* p = P + row * G;
+  float* d = dS + row * G;
+  float acc = 0.f;
+  for (int u = lane; u < G; u += 64) acc += d[u] * p[u];
+  acc = wave_sum(acc);
+  for (int u = lane; u < G; u += 64) d[u] = p[u] * (d[u] - acc);
+}
+
 inline unsigned blocks(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 // Floats of one (b, h) mix-parameter partial.
 inline int64_t mix_partial_len(const Geom& g, int kind) {
@@ -506,6 +697,10 @@ inline int64_t mix_partial_len(const Geom& g, int kind) {
 
 
 }  // namespace
+
+bool attn_rows(const Geom& g, int kind) {
+  return kind == 3 && !tok_fused(g, kind) && (g.G > kAttnLdsMaxG || (int64_t)g.G * g.V > kAttnMaxGV);
+}
 
 hipError_t launch_reduce_tokens(const Geom& g, const float* partU, const float* partS,
                                 int chunks, float* z, float* s, hipStream_t st) {
@@ -525,7 +720,7 @@ hipError_t launch_reduce_rows(const Geom& g, const float* part, float* out, int 
 // Whether the mix-parameter gradient goes through per-(b, h) partials (the LDS kernels and
 // attention) or is written directly (the batched products of the linear maps).
 static bool mix_params_in_partials(const Geom& g, int kind) {
-  return tok_fused(g, kind) || kind == 3;
+  return tok_fused(g, kind) || (kind == 3 && !attn_rows(g, kind));
 }
 
 hipError_t launch_reduce_params(const Geom& g, const float* part, float* dWs, float* dbias,
@@ -561,6 +756,22 @@ hipError_t launch_mix(const Geom& g, const MixArgs& m, const float* z, float* zm
                       float* attn, hipStream_t st) {
   const int BH = g.BH();
   if (tok_fused(g, m.kind)) return launch_tok_fwd(g, m, z, zmix, attn, st);
+  if (attn_rows(g, m.kind)) {
+    const int64_t jobs = (int64_t)BH * (g.G / 16);
+    const dim3 grid(blocks(jobs, kAttnRowWaves)), block(64 * kAttnRowWaves);
+    if (g.V == 16)
+      hipLaunchKernelGGL(k_attn_rows<16>, grid, block, 0, st, z, zmix, attn, m.Wq, m.Wk, m.Wv,
+                         m.scale, g.G, BH);
+    else if (g.V == 32)
+      hipLaunchKernelGGL(k_attn_rows<32>, grid, block, 0, st, z, zmix, attn, m.Wq, m.Wk, m.Wv,
+                         m.scale, g.G, BH);
+    else if (g.V == 64)
+      hipLaunchKernelGGL(k_attn_rows<64>, grid, block, 0, st, z, zmix, attn, m.Wq, m.Wk, m.Wv,
+                         m.scale, g.G, BH);
+    else
+      return hipErrorInvalidValue;
+    return hipGetLastError();
+  }
   if (m.kind == 3) {
     hipLaunchKernelGGL(k_attn_fwd, dim3(BH), dim3(kThreads), 0, st, z, zmix, attn, m.Wq,
                        m.Wk, m.Wv, m.scale, g.G, g.V);
@@ -573,6 +784,66 @@ hipError_t launch_mix(const Geom& g, const MixArgs& m, const float* z, float* zm
   return run_gemm(mix_fwd_desc(g, m, z, zmix), BH, st);
 }
 
+// Backward of the large-token-set attention as batched MFMA products (k_tile_gemm) and one
+// row kernel. scr: q, k, v (B H G V each), dS (B H G G), dq, dk, dv (B H G V each).
+//   q, k, v = z W;  dP = dzmix v^T;  dS = P * (dP - rowsum(dP * P));  dv = P^T dzmix;
+//   dq = scale dS k;  dk = scale dS^T q;  dz = dq Wq^T + dk Wk^T + dv Wv^T;
+//   [dWq; dWk; dWv] = sum over (b, h) of z^T [dq; dk; dv].
+static hipError_t attn_rows_bwd(const Geom& g, const MixArgs& m, const float* z, const float* s,
+                                const float* zmix, const float* P, const float* dzm, float* dz,
+                                float* dU, float* ds, float* cen, float* scr, float* dmix,
+                                hipStream_t st) {
+  const int BH = g.BH(), G = g.G, V = g.V;
+  const int64_t GV = (int64_t)G * V, GG = (int64_t)G * G, T = BH * GV;
+  constexpr int kPer = 1 << 30;  // a_mod: A advances with the output index
+  float* q = scr;
+  float* k = q + T;
+  float* v = k + T;
+  float* dS = v + T;
+  float* dq = dS + BH * GG;
+  float* dk = dq + T;
+  float* dv = dk + T;
+  const float* W[3] = {m.Wq, m.Wk, m.Wv};
+  float* qkv[3] = {q, k, v};
+  float* dqkv[3] = {dq, dk, dv};
+  hipError_t e = hipSuccess;
+  for (int w = 0; w < 3 && e == hipSuccess; ++w)  // q, k, v = z W
+    e = run_gemm(GemmDesc{z, V, 1, GV, 0, kPer, W[w], V, 1, 0, 0, qkv[w], V, GV, G, V, V, 1,
+                          1.0f, 0},
+                 BH, st);
+  if (e == hipSuccess)  // dP = dzmix v^T (into dS)
+    e = run_gemm(GemmDesc{dzm, V, 1, GV, 0, kPer, v, 1, V, GV, 0, dS, G, GG, G, G, V, 1, 1.0f, 0},
+                 BH, st);
+  if (e == hipSuccess) {
+    hipLaunchKernelGGL(k_attn_ds, dim3(blocks((int64_t)BH * G, 4)), dim3(256), 0, st, P, dS,
+                       (int64_t)BH * G, G);
+    e = hipGetLastError();
+  }
+  if (e == hipSuccess)  // dv = P^T dzmix
+    e = run_gemm(GemmDesc{P, 1, G, GG, 0, kPer, dzm, V, 1, GV, 0, dv, V, GV, G, V, G, 1, 1.0f, 0},
+                 BH, st);
+  if (e == hipSuccess)  // dq = scale dS k
+    e = run_gemm(GemmDesc{dS, G, 1, GG, 0, kPer, k, V, 1, GV, 0, dq, V, GV, G, V, G, 1, m.scale, 0},
+                 BH, st);
+  if (e == hipSuccess)  // dk = scale dS^T q
+    e = run_gemm(GemmDesc{dS, 1, G, GG, 0, kPer, q, V, 1, GV, 0, dk, V, GV, G, V, G, 1, m.scale, 0},
+                 BH, st);
+  for (int w = 0; w < 3 && e == hipSuccess; ++w)  // dz = sum_w d[w] W[w]^T
+    e = run_gemm(GemmDesc{dqkv[w], V, 1, GV, 0, kPer, W[w], 1, V, 0, 0, dz, V, GV, G, V, V, 1,
+                          1.0f, w > 0 ? 1 : 0},
+                 BH, st);
+  for (int w = 0; w < 3 && e == hipSuccess && dmix != nullptr; ++w)  // dW = sum z^T d[w]
+    e = run_gemm(GemmDesc{z, 1, V, 0, GV, 1, dqkv[w], V, 1, 0, GV, dmix + (int64_t)w * V * V, V, 0,
+                          V, V, G, BH, 1.0f, 0},
+                 1, st);
+  if (e == hipSuccess && s != nullptr) {
+    hipLaunchKernelGGL(k_token_grads, dim3(BH), dim3(kTokGradThreads), 0, st, z, s, zmix, dz, dU,
+                       ds, cen, G, V, g.eps);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
 hipError_t launch_mix_bwd(const Geom& g, const MixArgs& m, const float* z, const float* s,
                           const float* zmix, const float* attn, const float* dzm, float* dz,
                           float* dU, float* ds, float* cen, float* scr, float* partM,
@@ -582,6 +853,8 @@ hipError_t launch_mix_bwd(const Geom& g, const MixArgs& m, const float* z, const
   hipError_t e = hipSuccess;
   if (tok_fused(g, m.kind)) {
     e = launch_tok_bwd(g, m, z, s, zmix, attn, dzm, dz, dU, ds, cen, partM, st);
+  } else if (attn_rows(g, m.kind)) {
+    e = attn_rows_bwd(g, m, z, s, zmix, attn, dzm, dz, dU, ds, cen, scr, dmix, st);
   } else if (m.kind == 3) {
     hipLaunchKernelGGL(k_attn_bwd, dim3(BH), dim3(kThreads), 0, st, z, s, zmix, attn, dzm, dz,
                        dU, ds, cen, scr, partM, m.Wq, m.Wk, m.Wv, m.scale, g.G, g.V, g.eps);

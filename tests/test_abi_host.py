@@ -167,8 +167,8 @@ def test_mix_validation():
     assert L.fs_mix(ctypes.byref(p), None, z, zm, None, None) == NULL
     attn = MixDesc.make(fs.MIX_ATTN, Wq=f(), Wk=f(), Wv=f(), scale=0.1)
     assert L.fs_mix(ctypes.byref(p), ctypes.byref(attn), z, zm, None, None) == NULL  # no P
-    big = prob(G=512)
-    assert L.fs_mix(ctypes.byref(big), ctypes.byref(attn), z, zm, f(), None) == UNSUP
+    big = prob(G=1024, D=64, V=64)   # attention over any supported token set
+    assert L.fs_mix(ctypes.byref(big), ctypes.byref(attn), z, zm, None, None) == NULL
     A = f()
     lin = MixDesc.make(fs.MIX_LINEAR_G, A=A)
     assert L.fs_mix(ctypes.byref(p), ctypes.byref(lin), z, A, None, None) == ALIAS

@@ -102,6 +102,9 @@ SMALL = [
     small("f32_D16_G1024_id", "f32", 16, 1024, O.MIX_IDENTITY, N=500, H=2, B=1),
     small("bf16_D64_G256_lin", "bf16", 64, 256, O.MIX_LINEAR_G, N=600, H=2),
     small("bf16_D32_G256_attn", "bf16", 32, 256, O.MIX_ATTN, N=600, H=2),
+    # attention over large token sets inside the whole path
+    small("f32_D32_G1024_attn", "f32", 32, 1024, O.MIX_ATTN, N=600, H=2, B=1),
+    small("bf16_D64_G512_attn", "bf16", 64, 512, O.MIX_ATTN, N=600, H=2),
 ]
 
 
@@ -276,19 +279,23 @@ MIX_CASES = [
     ("fixed_per_head", O.MIX_LINEAR_G, 64, True), ("fixed_per_head", O.MIX_LINEAR_G, 256, True),
     ("channel", O.MIX_LINEAR_C, 32, False), ("channel", O.MIX_LINEAR_C, 512, False),
     ("attention", O.MIX_ATTN, 32, False), ("attention", O.MIX_ATTN, 128, False),
+    # attention over large token sets (the row-block forward and the batched-product backward)
+    ("attention", O.MIX_ATTN, 512, False), ("attention", O.MIX_ATTN, 1024, False),
+    ("attention_v64", O.MIX_ATTN, 256, False, 64), ("attention_v16", O.MIX_ATTN, 1024, False, 16),
 ]
 
 
-@pytest.mark.parametrize("label,kind,G,per_head", MIX_CASES,
+@pytest.mark.parametrize("label,kind,G,per_head,V", [c if len(c) == 5 else c + (32,)
+                                                     for c in MIX_CASES],
                          ids=[f"{c[0]}_G{c[2]}" for c in MIX_CASES])
-def test_mix_entry_points(label, kind, G, per_head):
+def test_mix_entry_points(label, kind, G, per_head, V):
     """fs_mix and fs_mix_bwd on their own (both the single-workgroup LDS kernels and the
     batched products for large token sets) against the oracle's mix steps, per (b, h); the
     parameter gradients are summed over samples and heads (over samples per head for a
     per-head matrix)."""
     import torch
     import paper_2609_32525_amd as fs
-    B, H, V = 2, 3, 32
+    B, H = 2, 3
     w = W.Workload(f"mix_{label}", 300 + kind, "f32", B, 64, H, V, V, G, kind, a_per_head=per_head)
     inp = W.make_inputs(w, with_grad=False)
     z = W.random_like(w, 1, (B, H, G, V))
