@@ -352,3 +352,45 @@ def test_mix_entry_points(label, kind, G, per_head, V):
     print("  errors:", {k: f"{e:.2e}" for k, e in errs.items()}, flush=True)
     bad = {k: e for k, e in errs.items() if not e <= 1e-5}
     assert not bad, bad
+
+
+# ---- HIP graph replay ------------------------------------------------------------------------
+@pytest.mark.parametrize("name,dtype,D,G,mix", [
+    ("graph_f32_G32_attn", "f32", 32, 32, O.MIX_ATTN),
+    ("graph_bf16_G64_lin", "bf16", 32, 64, O.MIX_LINEAR_G),
+    ("graph_bf16_G256_lin", "bf16", 32, 256, O.MIX_LINEAR_G),
+    ("graph_f32_G1024_attn", "f32", 32, 1024, O.MIX_ATTN),
+])
+def test_graph_replay_matches_eager(name, dtype, D, G, mix):
+    """One forward + backward captured as a HIP graph and replayed several times, with eager
+    launches and synchronisations in between, gives bitwise the eager results every time
+    (the kernels are deterministic, and no call records a memset)."""
+    import torch
+    from paper_2609_32525_amd.runner import PathBuffers
+    w = small(name, dtype, D, G, mix, N=3000 if G <= 256 else 900, B=2, H=2)
+    announce(f"graph {w}")
+    inp = W.make_inputs(w)
+    pb = PathBuffers(inp, w.mix, w.dtype, w.eps)
+    pb.step()
+    eager = pb.results()
+    dev = pb.dev
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(side):
+        pb.step()
+    torch.cuda.current_stream(dev).wait_stream(side)
+    torch.cuda.synchronize(dev)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        pb.step()
+    torch.cuda.synchronize(dev)
+    for rep in range(3):
+        for t in (pb.out, pb.dx, pb.dfx, pb.dWs, pb.z):
+            t.fill_(float("nan"))          # the replay must rewrite every output
+        graph.replay()
+        got = pb.results()
+        for k, v in eager.items():
+            if v is not None:
+                assert np.array_equal(v, got[k]), (rep, k)
+        pb.forward()                        # eager work between replays
+        torch.cuda.synchronize(dev)
