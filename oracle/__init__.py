@@ -311,6 +311,99 @@ def backward(x, fx, Ws, b, tau, kind, prm: Optional[Dict], dout, eps=1e-5,
     return res
 
 
+# ----------------------------------------------------------------------------------------
+# untied variant (Sec. 2 ablation suite): the deslice has its own projection W_d, bias b_d
+# and temperature tau_d, so its weights w_d = softmax_g((X W_d + b_d) / tau_d) differ from
+# the slice weights w
+# ----------------------------------------------------------------------------------------
+def untied_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm: Optional[Dict] = None,
+                   eps=1e-5, pairs=None) -> Dict[str, np.ndarray]:
+    """Slice with (W_s, b, tau), mix, deslice with (W_d, b_d, tau_d). Returns z, s, zmix,
+    P, lse (slice normaliser), lse_d (deslice normaliser) and out."""
+    prm = prm or {}
+    B, N, H, D = x.shape
+    V = fx.shape[3]
+    G = np.asarray(Ws).shape[-1]
+    res = {k: np.zeros(sh) for k, sh in dict(
+        z=(B, H, G, V), s=(B, H, G), zmix=(B, H, G, V), lse=(B, H, N), lse_d=(B, H, N),
+        out=(B, N, H, V)).items()}
+    res["P"] = np.zeros((B, H, G, G)) if kind == MIX_ATTN else None
+    for bb, h in _pairs(B, H, pairs):
+        X = np.asarray(x[bb, :, h, :], dtype=f64)
+        F = np.asarray(fx[bb, :, h, :], dtype=f64)
+        Wsh, bh = _ws_b(Ws, b, h)
+        Wdh, bdh = _ws_b(Wd, bd, h)
+        w, lse = slot_softmax(logits(X, Wsh, bh, f64(tau[h])))
+        s, U, z = slice_tokens(w, F, f64(eps))
+        zm, P = mix_forward(kind, z, _head_params(kind, prm, h))
+        wd, lse_d = slot_softmax(logits(X, Wdh, bdh, f64(taud[h])))
+        res["z"][bb, h], res["s"][bb, h], res["zmix"][bb, h] = z, s, zm
+        res["lse"][bb, h], res["lse_d"][bb, h] = lse, lse_d
+        if P is not None:
+            res["P"][bb, h] = P
+        res["out"][bb, :, h, :] = deslice(wd, zm)
+    return res
+
+
+def untied_backward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm: Optional[Dict], dout,
+                    eps=1e-5, fwd: Optional[Dict] = None, pairs=None) -> Dict[str, np.ndarray]:
+    """Backward of the untied path. The deslice weights receive dw_d = dO z'^T only; the
+    slice weights receive dw = F dU^T + 1 ds^T only; each goes through its own softmax
+    Jacobian and its own projection. Returns dx, dfx, dWs, db, dtau, dWd, dbd, dtaud,
+    dzmix, dz and the mix-parameter gradients."""
+    prm = prm or {}
+    B, N, H, D = x.shape
+    V = fx.shape[3]
+    Ws_arr, b_arr = np.asarray(Ws, dtype=f64), np.asarray(b, dtype=f64)
+    Wd_arr, bd_arr = np.asarray(Wd, dtype=f64), np.asarray(bd, dtype=f64)
+    G = Ws_arr.shape[-1]
+    if fwd is None:
+        fwd = untied_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm, eps, pairs=pairs)
+    res = dict(dx=np.zeros((B, N, H, D)), dfx=np.zeros((B, N, H, V)),
+               dWs=np.zeros_like(Ws_arr), db=np.zeros_like(b_arr), dtau=np.zeros(H),
+               dWd=np.zeros_like(Wd_arr), dbd=np.zeros_like(bd_arr), dtaud=np.zeros(H),
+               dzmix=np.zeros((B, H, G, V)), dz=np.zeros((B, H, G, V)))
+    for bb, h in _pairs(B, H, pairs):
+        X = np.asarray(x[bb, :, h, :], dtype=f64)
+        F = np.asarray(fx[bb, :, h, :], dtype=f64)
+        dO = np.asarray(dout[bb, :, h, :], dtype=f64)
+        Wsh, bh = _ws_b(Ws, b, h)
+        Wdh, bdh = _ws_b(Wd, bd, h)
+        t, td = f64(tau[h]), f64(taud[h])
+        a = logits(X, Wsh, bh, t)
+        w, _ = slot_softmax(a)
+        ad = logits(X, Wdh, bdh, td)
+        wd, _ = slot_softmax(ad)
+        z, s, zm = fwd["z"][bb, h], fwd["s"][bb, h], fwd["zmix"][bb, h]
+        P = fwd["P"][bb, h] if fwd.get("P") is not None else None
+        dzm = wd.T @ dO
+        dz, dprm = mix_backward(kind, z, P, dzm, _head_params(kind, prm, h))
+        dU, ds = token_backward(dz, z, s, f64(eps))
+        da = softmax_backward(w, F @ dU.T + ds[None, :])
+        dad = softmax_backward(wd, dO @ zm.T)
+        dX, dWs, db, dtau = logit_backward(da, X, Wsh, a, t)
+        dXd, dWd, dbd, dtaud = logit_backward(dad, X, Wdh, ad, td)
+        res["dx"][bb, :, h, :] = dX + dXd
+        res["dfx"][bb, :, h, :] = w @ dU
+        res["dzmix"][bb, h], res["dz"][bb, h] = dzm, dz
+        res["dtau"][h] += dtau
+        res["dtaud"][h] += dtaud
+        for key, arr, val in (("dWs", Ws_arr, dWs), ("db", b_arr, db), ("dWd", Wd_arr, dWd),
+                              ("dbd", bd_arr, dbd)):
+            per_head = arr.ndim == (3 if key in ("dWs", "dWd") else 2)
+            if per_head:
+                res[key][h] += val
+            else:
+                res[key] += val
+        for k, v in dprm.items():
+            if k == "dA" and np.asarray(prm["A"]).ndim == 3:
+                res.setdefault(k, np.zeros((H, G, G)))[h] += v
+            else:
+                res.setdefault(k, np.zeros_like(v))
+                res[k] += v
+    return res
+
+
 def run_inputs(inp: Dict, kind: int, eps: float = 1e-5, backward_too: bool = True,
                pairs=None, dtype=f64):
     """Convenience: forward (+ backward) on a ``workloads.make_inputs`` dictionary."""

@@ -19,6 +19,7 @@ namespace {
 thread_local int g_last_hip_error = 0;
 
 constexpr size_t kAlign = 256;
+constexpr int64_t kCUs = 256;  // MI355X compute units
 size_t up(size_t v, size_t a = kAlign) { return (v + a - 1) / a * a; }
 bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 
@@ -33,6 +34,9 @@ bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 #endif
 #ifndef FS_TARGET_DESLICE
 #define FS_TARGET_DESLICE 512
+#endif
+#ifndef FS_MIN_TILES
+#define FS_MIN_TILES 4
 #endif
 #ifndef FS_TARGET_LONG
 #define FS_TARGET_LONG 1024
@@ -87,7 +91,11 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
   int64_t chunks = std::max<int64_t>(1, (target + units - 1) / units);
   // passes that write partials give every chunk at least 4 tiles per point group, so the
   // partials stay small next to the points they summarise
-  chunks = std::min<int64_t>(chunks, partials ? std::max<int64_t>(1, ntiles / 4) : ntiles);
+  chunks = std::min<int64_t>(chunks, partials ? std::max<int64_t>(1, ntiles / FS_MIN_TILES) : ntiles);
+  // but never fewer workgroups than compute units while tiles remain to spread (small N;
+  // two tiles per point group at least where partials are written)
+  chunks = std::max<int64_t>(
+      chunks, std::min<int64_t>(partials ? ntiles / 2 : ntiles, (kCUs + units - 1) / units));
   // long streams take twice as many workgroups where every chunk still keeps 16 tiles: the
   // shorter per-workgroup runs shrink the tail of the last wave of workgroups
   if (c.NS < 8 && FS_TARGET_LONG > target) {

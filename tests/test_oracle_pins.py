@@ -346,11 +346,95 @@ def check_repeated_block(o):
             np.testing.assert_allclose(r["P"], full["P"], rtol=1e-12, atol=1e-13)
 
 
+def _untied_problem(seed, per_head=False, **kw):
+    x, fx, Ws, b, tau, rng = _problem(seed=seed, per_head=per_head, **kw)
+    Wd = rng.standard_normal(Ws.shape)
+    bd = rng.standard_normal(b.shape)
+    taud = rng.uniform(0.4, 1.5, size=tau.shape)
+    return x, fx, Ws, b, tau, Wd, bd, taud, rng
+
+
+def check_untied_finite_differences(o, kinds=tuple(MIXES)):
+    """Untied variant: central differences of L = sum(O * R) in fp64 match every analytic
+    gradient, both projections' included."""
+    eps = 0.3
+    for kind in kinds:
+        x, fx, Ws, b, tau, Wd, bd, taud, rng = _untied_problem(
+            40 + kind, B=2, N=5, H=2, D=3, V=2, G=4)
+        prm = _prm(kind, 4, 2, rng)
+        R = rng.standard_normal((2, 5, 2, 2))
+        fwd = o.untied_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm, eps=eps)
+        g = o.untied_backward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm, R, eps=eps, fwd=fwd)
+        tensors = {"dx": x, "dfx": fx, "dWs": Ws, "db": b, "dtau": tau, "dWd": Wd, "dbd": bd,
+                   "dtaud": taud}
+        for k in ("A", "Wc", "Wq", "Wk", "Wv"):
+            if prm.get(k) is not None:
+                tensors["d" + k] = prm[k]
+        step = 1e-6
+        for gname, arr in tensors.items():
+            num = np.zeros_like(arr)
+            for idx in np.ndindex(arr.shape):
+                old = arr[idx]
+                vals = []
+                for sgn in (1, -1):
+                    arr[idx] = old + sgn * step
+                    vals.append((o.untied_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm,
+                                                  eps=eps)["out"] * R).sum())
+                arr[idx] = old
+                num[idx] = (vals[0] - vals[1]) / (2 * step)
+            scale = max(np.abs(num).max(), 1e-3)
+            err = np.abs(g[gname] - num).max() / scale
+            assert err < 2e-7, (kind, gname, err)
+
+
+def check_untied_reduces_to_tied(o):
+    """With the deslice projection, bias and temperature equal to the slice's, the untied
+    forward is the tied one, and each shared-parameter gradient of the tied path is the sum
+    of its two untied parts (the parameter feeds both weight sets)."""
+    for kind in (o.MIX_LINEAR_G, o.MIX_ATTN):
+        x, fx, Ws, b, tau, rng = _problem(B=2, N=9, H=2, D=3, V=3, G=5, seed=60 + kind)
+        prm = _prm(kind, 5, 3, rng)
+        R = rng.standard_normal(fx.shape)
+        ut = o.untied_forward(x, fx, Ws, b, tau, Ws, b, tau, kind, prm, eps=0.1)
+        t = o.forward(x, fx, Ws, b, tau, kind, prm, eps=0.1)
+        for k in ("z", "s", "zmix", "lse", "out"):
+            np.testing.assert_allclose(ut[k], t[k], rtol=1e-12, atol=1e-14, err_msg=k)
+        np.testing.assert_allclose(ut["lse_d"], t["lse"], rtol=1e-12, atol=1e-14)
+        gu = o.untied_backward(x, fx, Ws, b, tau, Ws, b, tau, kind, prm, R, eps=0.1, fwd=ut)
+        gt = o.backward(x, fx, Ws, b, tau, kind, prm, R, eps=0.1, fwd=t)
+        for k in ("dx", "dfx", "dzmix"):
+            np.testing.assert_allclose(gu[k], gt[k], rtol=1e-11, atol=1e-13, err_msg=k)
+        for k, kd in (("dWs", "dWd"), ("db", "dbd"), ("dtau", "dtaud")):
+            np.testing.assert_allclose(gu[k] + gu[kd], gt[k], rtol=1e-11, atol=1e-13, err_msg=k)
+            # and the split is not trivial: both parts carry gradient
+            assert np.abs(gu[k]).max() > 1e-6 and np.abs(gu[kd]).max() > 1e-6
+
+
+def check_untied_cancellation_and_temperature(o):
+    """Each weight set's logit gradient cancels over the slots (sum_g db = sum_g db_d = 0,
+    likewise the projection rows), and the scale invariance of each logit set gives
+    tau dtau = -(<W, dW> + <b, db>) per head for both (App. F.2)."""
+    x, fx, Ws, b, tau, Wd, bd, taud, rng = _untied_problem(
+        70, per_head=True, B=2, N=20, H=3, D=4, V=3, G=6)
+    prm = _prm(o.MIX_LINEAR_C, 6, 3, rng)
+    R = rng.standard_normal(fx.shape)
+    g = o.untied_backward(x, fx, Ws, b, tau, Wd, bd, taud, o.MIX_LINEAR_C, prm, R, eps=1e-2)
+    for kW, kb, W_, b_, t_, kt in (("dWs", "db", Ws, b, tau, "dtau"),
+                                   ("dWd", "dbd", Wd, bd, taud, "dtaud")):
+        np.testing.assert_allclose(g[kb].sum(axis=-1), 0.0, atol=1e-12 * np.abs(g[kb]).sum())
+        np.testing.assert_allclose(g[kW].sum(axis=-1), 0.0, atol=1e-12 * np.abs(g[kW]).sum())
+        lhs = t_ * g[kt]
+        rhs = -((W_ * g[kW]).sum(axis=(1, 2)) + (b_ * g[kb]).sum(axis=1))
+        np.testing.assert_allclose(lhs, rhs, rtol=1e-10, atol=1e-13)
+        assert np.abs(lhs).max() > 1e-5
+
+
 ALL_CHECKS = [check_partition_of_unity, check_single_slice_mean, check_identical_points,
               check_constant_tokens, check_zero_logits, check_hard_assignment,
               check_bruteforce, check_invariances, check_mix_closed_forms,
               check_finite_differences, check_cancellation, check_temperature_identity,
-              check_repeated_block]
+              check_repeated_block, check_untied_finite_differences,
+              check_untied_reduces_to_tied, check_untied_cancellation_and_temperature]
 
 
 @pytest.mark.parametrize("check", ALL_CHECKS, ids=lambda c: c.__name__)
@@ -370,7 +454,8 @@ def _mutant(**overrides):
     m.__dict__.update({k: v for k, v in O.__dict__.items() if not k.startswith("__")})
     m.__dict__.update(overrides)
     # re-bind the module-level drivers so they call the planted functions
-    for name in ("forward", "backward"):
+    for name in ("forward", "backward", "untied_forward", "untied_backward",
+                 "forward_repeated"):
         f = O.__dict__[name]
         m.__dict__[name] = types.FunctionType(f.__code__, m.__dict__, name, f.__defaults__)
     return m
