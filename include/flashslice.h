@@ -100,10 +100,11 @@ typedef struct {
   float scale;          /* attention logit scale, e.g. 1/sqrt(V)                           */
 } fs_mix_desc;
 
-/* Bytes of device workspace needed by fs_slice_fwd (for_backward = 0), or by fs_mix_bwd and
- * fs_slice_deslice_bwd (for_backward = 1), for this problem. The size never grows with N*G:
- * it holds per-workgroup partial sums (bounded number of workgroups) and token-sized
- * buffers. Returns FS_OK and writes *bytes, or a validation error.                          */
+/* Bytes of device workspace needed by fs_slice_fwd (for_backward = 0), by fs_mix_bwd and
+ * fs_slice_deslice_bwd (for_backward = 1), or by fs_untied_bwd (for_backward = 2), for this
+ * problem. The size never grows with N*G: it holds per-workgroup partial sums (bounded number
+ * of workgroups) and token-sized buffers. Returns FS_OK and writes *bytes, or a validation
+ * error (FS_ERR_ARG for another for_backward).                                             */
 int fs_workspace_bytes(const fs_problem* prob, int for_backward, size_t* bytes);
 
 /* Slice (paper: Sec. 2; App. F.1 single-tile equation): recompute the slice weights per
@@ -160,6 +161,28 @@ int fs_slice_deslice_bwd(const fs_problem* prob, const fs_mix_desc* mix, const v
                          void* dx, void* dfx, float* dWs, float* dbias, float* dtau,
                          float* dmix_params, float* dzmix_out, void* ws, size_t ws_bytes,
                          void* hip_stream);
+
+/* Backward of the untied variant (paper: Sec. 2 ablation suite, the deslice with its own
+ * projection and temperature): the slice uses W_s (D,G), bias (G), tau (H) as everywhere
+ * else, the deslice uses Wd, bd, taud of the same shapes (shared or per head with
+ * ws_per_head), so its weights w_d = softmax_g((x Wd + bd) / taud) differ from the slice
+ * weights w. The forward is fs_slice_fwd (W_s; lse), fs_mix, then fs_deslice_stats_fwd with
+ * (Wd, bd, taud), which writes lse_d. Inputs as in fs_slice_deslice_bwd plus Wd, bd, taud
+ * and lse_d. The deslice weights carry dw_d = dout zmix^T, the slice weights
+ * dw = fx dU^T + 1 ds^T, each through its own softmax Jacobian and projection:
+ * dx (B,N,H,D) = the sum of both projections' contributions; dfx (B,N,H,V) = w dU; dWs,
+ * dbias, dtau from the slice weights and dWd, dbd, dtaud from the deslice weights (App. F.2
+ * for both temperatures); dmix_params and dzmix_out (= w_d^T dout) as in
+ * fs_slice_deslice_bwd. Workspace: fs_workspace_bytes(prob, 2, .). Every output is
+ * overwritten; no output may overlap an input or another output.                          */
+int fs_untied_bwd(const fs_problem* prob, const fs_mix_desc* mix, const void* x, const void* fx,
+                  const float* Ws, const float* bias, const float* tau, const float* Wd,
+                  const float* bd, const float* taud, const float* z, const float* s,
+                  const float* zmix, const float* attn_probs, const float* lse,
+                  const float* lse_d, const void* dout, void* dx, void* dfx, float* dWs,
+                  float* dbias, float* dtau, float* dWd, float* dbd, float* dtaud,
+                  float* dmix_params, float* dzmix_out, void* ws, size_t ws_bytes,
+                  void* hip_stream);
 
 /* Measurement aid: for calls made later on this thread, record the caller's hipEvent_t
  * `before` immediately before, and `after` immediately after, the launch of the streaming

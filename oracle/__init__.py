@@ -317,9 +317,10 @@ def backward(x, fx, Ws, b, tau, kind, prm: Optional[Dict], dout, eps=1e-5,
 # the slice weights w
 # ----------------------------------------------------------------------------------------
 def untied_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm: Optional[Dict] = None,
-                   eps=1e-5, pairs=None) -> Dict[str, np.ndarray]:
+                   eps=1e-5, pairs=None, dtype=f64) -> Dict[str, np.ndarray]:
     """Slice with (W_s, b, tau), mix, deslice with (W_d, b_d, tau_d). Returns z, s, zmix,
-    P, lse (slice normaliser), lse_d (deslice normaliser) and out."""
+    P, lse (slice normaliser), lse_d (deslice normaliser) and out. ``dtype`` as in
+    forward."""
     prm = prm or {}
     B, N, H, D = x.shape
     V = fx.shape[3]
@@ -328,15 +329,16 @@ def untied_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm: Optional[Dict] = 
         z=(B, H, G, V), s=(B, H, G), zmix=(B, H, G, V), lse=(B, H, N), lse_d=(B, H, N),
         out=(B, N, H, V)).items()}
     res["P"] = np.zeros((B, H, G, G)) if kind == MIX_ATTN else None
+    ct = np.dtype(dtype).type
     for bb, h in _pairs(B, H, pairs):
-        X = np.asarray(x[bb, :, h, :], dtype=f64)
-        F = np.asarray(fx[bb, :, h, :], dtype=f64)
-        Wsh, bh = _ws_b(Ws, b, h)
-        Wdh, bdh = _ws_b(Wd, bd, h)
-        w, lse = slot_softmax(logits(X, Wsh, bh, f64(tau[h])))
-        s, U, z = slice_tokens(w, F, f64(eps))
-        zm, P = mix_forward(kind, z, _head_params(kind, prm, h))
-        wd, lse_d = slot_softmax(logits(X, Wdh, bdh, f64(taud[h])))
+        X = np.asarray(x[bb, :, h, :], dtype=ct)
+        F = np.asarray(fx[bb, :, h, :], dtype=ct)
+        Wsh, bh = _ws_b(Ws, b, h, ct)
+        Wdh, bdh = _ws_b(Wd, bd, h, ct)
+        w, lse = slot_softmax(logits(X, Wsh, bh, ct(tau[h])))
+        s, U, z = slice_tokens(w, F, ct(eps))
+        zm, P = mix_forward(kind, z, _head_params(kind, prm, h, ct))
+        wd, lse_d = slot_softmax(logits(X, Wdh, bdh, ct(taud[h])))
         res["z"][bb, h], res["s"][bb, h], res["zmix"][bb, h] = z, s, zm
         res["lse"][bb, h], res["lse_d"][bb, h] = lse, lse_d
         if P is not None:
@@ -346,7 +348,8 @@ def untied_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm: Optional[Dict] = 
 
 
 def untied_backward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm: Optional[Dict], dout,
-                    eps=1e-5, fwd: Optional[Dict] = None, pairs=None) -> Dict[str, np.ndarray]:
+                    eps=1e-5, fwd: Optional[Dict] = None, pairs=None,
+                    dtype=f64) -> Dict[str, np.ndarray]:
     """Backward of the untied path. The deslice weights receive dw_d = dO z'^T only; the
     slice weights receive dw = F dU^T + 1 ds^T only; each goes through its own softmax
     Jacobian and its own projection. Returns dx, dfx, dWs, db, dtau, dWd, dbd, dtaud,
@@ -358,27 +361,30 @@ def untied_backward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm: Optional[Dict], 
     Wd_arr, bd_arr = np.asarray(Wd, dtype=f64), np.asarray(bd, dtype=f64)
     G = Ws_arr.shape[-1]
     if fwd is None:
-        fwd = untied_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm, eps, pairs=pairs)
+        fwd = untied_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm, eps, pairs=pairs,
+                             dtype=dtype)
+    ct = np.dtype(dtype).type
     res = dict(dx=np.zeros((B, N, H, D)), dfx=np.zeros((B, N, H, V)),
                dWs=np.zeros_like(Ws_arr), db=np.zeros_like(b_arr), dtau=np.zeros(H),
                dWd=np.zeros_like(Wd_arr), dbd=np.zeros_like(bd_arr), dtaud=np.zeros(H),
                dzmix=np.zeros((B, H, G, V)), dz=np.zeros((B, H, G, V)))
     for bb, h in _pairs(B, H, pairs):
-        X = np.asarray(x[bb, :, h, :], dtype=f64)
-        F = np.asarray(fx[bb, :, h, :], dtype=f64)
-        dO = np.asarray(dout[bb, :, h, :], dtype=f64)
-        Wsh, bh = _ws_b(Ws, b, h)
-        Wdh, bdh = _ws_b(Wd, bd, h)
-        t, td = f64(tau[h]), f64(taud[h])
+        X = np.asarray(x[bb, :, h, :], dtype=ct)
+        F = np.asarray(fx[bb, :, h, :], dtype=ct)
+        dO = np.asarray(dout[bb, :, h, :], dtype=ct)
+        Wsh, bh = _ws_b(Ws, b, h, ct)
+        Wdh, bdh = _ws_b(Wd, bd, h, ct)
+        t, td = ct(tau[h]), ct(taud[h])
         a = logits(X, Wsh, bh, t)
         w, _ = slot_softmax(a)
         ad = logits(X, Wdh, bdh, td)
         wd, _ = slot_softmax(ad)
-        z, s, zm = fwd["z"][bb, h], fwd["s"][bb, h], fwd["zmix"][bb, h]
-        P = fwd["P"][bb, h] if fwd.get("P") is not None else None
+        z, s, zm = (fwd["z"][bb, h].astype(ct), fwd["s"][bb, h].astype(ct),
+                    fwd["zmix"][bb, h].astype(ct))
+        P = fwd["P"][bb, h].astype(ct) if fwd.get("P") is not None else None
         dzm = wd.T @ dO
-        dz, dprm = mix_backward(kind, z, P, dzm, _head_params(kind, prm, h))
-        dU, ds = token_backward(dz, z, s, f64(eps))
+        dz, dprm = mix_backward(kind, z, P, dzm, _head_params(kind, prm, h, ct))
+        dU, ds = token_backward(dz, z, s, ct(eps))
         da = softmax_backward(w, F @ dU.T + ds[None, :])
         dad = softmax_backward(wd, dO @ zm.T)
         dX, dWs, db, dtau = logit_backward(da, X, Wsh, a, t)

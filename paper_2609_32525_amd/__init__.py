@@ -16,7 +16,7 @@ from typing import Optional
 __all__ = [
     "F32", "BF16", "MIX_IDENTITY", "MIX_LINEAR_G", "MIX_LINEAR_C", "MIX_ATTN",
     "FsError", "Problem", "MixDesc", "lib", "lib_path", "workspace_bytes", "slice_fwd", "mix",
-    "mix_bwd", "deslice_fwd", "deslice_stats_fwd", "slice_deslice_bwd", "status_string", "last_hip_error",
+    "mix_bwd", "deslice_fwd", "deslice_stats_fwd", "slice_deslice_bwd", "untied_bwd", "status_string", "last_hip_error",
     "set_pass_events", "EXPORTED", "PASS_SLICE", "PASS_DESLICE", "PASS_BWD_A", "PASS_BWD_B",
 ]
 
@@ -24,7 +24,7 @@ F32, BF16 = 0, 1
 MIX_IDENTITY, MIX_LINEAR_G, MIX_LINEAR_C, MIX_ATTN = 0, 1, 2, 3
 
 EXPORTED = ("fs_workspace_bytes", "fs_slice_fwd", "fs_mix", "fs_mix_bwd", "fs_deslice_fwd",
-            "fs_deslice_stats_fwd", "fs_slice_deslice_bwd", "fs_set_pass_events", "fs_status_string",
+            "fs_deslice_stats_fwd", "fs_slice_deslice_bwd", "fs_untied_bwd", "fs_set_pass_events", "fs_status_string",
             "fs_last_hip_error")
 
 PASS_SLICE, PASS_DESLICE, PASS_BWD_A, PASS_BWD_B = 0, 1, 2, 3
@@ -91,6 +91,7 @@ def lib() -> ctypes.CDLL:
         L.fs_deslice_fwd.argtypes = [prob, P, P, P, P, P, P, P, P]
         L.fs_deslice_stats_fwd.argtypes = [prob, P, P, P, P, P, P, P, P]
         L.fs_slice_deslice_bwd.argtypes = [prob, mixp] + [P] * 19 + [S, P]
+        L.fs_untied_bwd.argtypes = [prob, mixp] + [P] * 26 + [S, P]
         L.fs_status_string.argtypes = [ctypes.c_int]
         L.fs_status_string.restype = ctypes.c_char_p
         L.fs_last_hip_error.argtypes = []
@@ -148,9 +149,10 @@ def set_pass_events(pass_id: int, before=None, after=None) -> None:
     _check(lib().fs_set_pass_events(pass_id, ev(before), ev(after)), "fs_set_pass_events")
 
 
-def workspace_bytes(prob: Problem, for_backward: bool) -> int:
+def workspace_bytes(prob: Problem, for_backward) -> int:
+    """for_backward: 0 / False forward, 1 / True backward, 2 untied backward."""
     out = ctypes.c_size_t(0)
-    _check(lib().fs_workspace_bytes(ctypes.byref(prob), int(bool(for_backward)),
+    _check(lib().fs_workspace_bytes(ctypes.byref(prob), int(for_backward),
                                     ctypes.byref(out)), "fs_workspace_bytes")
     return out.value
 
@@ -195,3 +197,15 @@ def slice_deslice_bwd(prob, mixdesc, x, fx, Ws, b, tau, z, s, zmix, attn, lse, d
         _ptr(dfx), _ptr(dWs), _ptr(db), _ptr(dtau), _ptr(dmix), _ptr(dzmix_out), _ptr(ws),
         _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
         "fs_slice_deslice_bwd")
+
+
+def untied_bwd(prob, mixdesc, x, fx, Ws, b, tau, Wd, bd, taud, z, s, zmix, attn, lse, lse_d,
+               dout, dx, dfx, dWs, db, dtau, dWd, dbd, dtaud, dmix, dzmix_out, ws,
+               ws_bytes=None, stream=None) -> None:
+    _check(lib().fs_untied_bwd(
+        ctypes.byref(prob), ctypes.byref(mixdesc), _ptr(x), _ptr(fx), _ptr(Ws), _ptr(b),
+        _ptr(tau), _ptr(Wd), _ptr(bd), _ptr(taud), _ptr(z), _ptr(s), _ptr(zmix), _ptr(attn),
+        _ptr(lse), _ptr(lse_d), _ptr(dout), _ptr(dx), _ptr(dfx), _ptr(dWs), _ptr(db),
+        _ptr(dtau), _ptr(dWd), _ptr(dbd), _ptr(dtaud), _ptr(dmix), _ptr(dzmix_out), _ptr(ws),
+        _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
+        "fs_untied_bwd")

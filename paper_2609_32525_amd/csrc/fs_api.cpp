@@ -49,7 +49,7 @@ PassEvents& pass_events() {
   return ev;
 }
 
-bool blocked(const Geom& g) { return g.G > FS_BLOCKED_MIN_G && g.D <= 32; }
+bool blocked(const Geom& g) { return !g.untied && g.G > FS_BLOCKED_MIN_G && g.D <= 32; }
 
 PassCfg pick_cfg(const Geom& g, Pass pass) {
   PassCfg c{};
@@ -173,6 +173,10 @@ BwdWs bwd_ws_layout(const Geom& g, int kind) {
   off += up(blocked(g) ? 2 * sizeof(float) * (size_t)g.BH() * (size_t)g.N : 0);
   L.img = off;
   off += up(blocked(g) ? point_image_bytes(g) : 0);
+  L.partP2 = off;  // the deslice weights' parameter partials (untied variant)
+  off += up(g.untied ? sizeof(float) * (size_t)g.BH() * cb.chunks *
+                           (size_t)param_partial_len(g, cb.nblk)
+                     : 0);
   L.total = off;
   return L;
 }
@@ -322,7 +326,9 @@ int fs_workspace_bytes(const fs_problem* prob, int for_backward, size_t* bytes) 
   int st = check_problem(prob, &g);
   if (st != FS_OK) return st;
   if (bytes == nullptr) return FS_ERR_NULL;
+  if (for_backward < 0 || for_backward > 2) return FS_ERR_ARG;
   if (for_backward) {
+    g.untied = for_backward == 2;
     *bytes = bwd_required(g);
   } else {
     *bytes = fs::fwd_ws_layout(g).total;
@@ -472,6 +478,56 @@ int fs_slice_deslice_bwd(const fs_problem* prob, const fs_mix_desc* mix, const v
                                    mix->kind == FS_MIX_IDENTITY ? nullptr : dmix_params,
                                    dzmix_out, static_cast<char*>(ws),
                                    static_cast<hipStream_t>(hip_stream)));
+}
+
+int fs_untied_bwd(const fs_problem* prob, const fs_mix_desc* mix, const void* x, const void* fx,
+                  const float* Ws, const float* bias, const float* tau, const float* Wd,
+                  const float* bd, const float* taud, const float* z, const float* s,
+                  const float* zmix, const float* attn_probs, const float* lse,
+                  const float* lse_d, const void* dout, void* dx, void* dfx, float* dWs,
+                  float* dbias, float* dtau, float* dWd, float* dbd, float* dtaud,
+                  float* dmix_params, float* dzmix_out, void* ws, size_t ws_bytes,
+                  void* hip_stream) {
+  Geom g;
+  int st = check_problem(prob, &g);
+  if (st != FS_OK) return st;
+  st = check_mix(mix, g);
+  if (st != FS_OK) return st;
+  g.untied = true;
+  const Sizes zs = sizes(g);
+  const bool attn = mix->kind == FS_MIX_ATTN;
+  Buf in[20];
+  int nin = 0;
+  mix_bufs(mix, g, in, &nin);
+  in[nin++] = {x, zs.x, true};
+  in[nin++] = {fx, zs.fx, true};
+  in[nin++] = {Ws, zs.Ws, true};
+  in[nin++] = {bias, zs.b, true};
+  in[nin++] = {tau, zs.tau, true};
+  in[nin++] = {Wd, zs.Ws, true};
+  in[nin++] = {bd, zs.b, true};
+  in[nin++] = {taud, zs.tau, true};
+  in[nin++] = {z, zs.tok, true};
+  in[nin++] = {s, zs.s, true};
+  in[nin++] = {zmix, zs.tok, true};
+  in[nin++] = {attn ? attn_probs : nullptr, attn ? zs.attn : 0, true};
+  in[nin++] = {lse, zs.lse, true};
+  in[nin++] = {lse_d, zs.lse, true};
+  in[nin++] = {dout, zs.fx, true};
+  const size_t np = sizeof(float) * fs::mix_param_count(g, mix->kind, mix->a_per_head != 0);
+  const Buf out[] = {{dx, zs.x, true},       {dfx, zs.fx, true},        {dWs, zs.Ws, true},
+                     {dbias, zs.b, true},    {dtau, zs.tau, true},      {dWd, zs.Ws, true},
+                     {dbd, zs.b, true},      {dtaud, zs.tau, true},     {dmix_params, np, false},
+                     {dzmix_out, zs.tok, false}, {ws, ws_bytes, true}};
+  st = check_bufs(in, nin, out, 11);
+  if (st != FS_OK) return st;
+  if (ws == nullptr || ws_bytes < bwd_required(g)) return FS_ERR_WORKSPACE;
+  const fs::UntiedArgs u{Wd, bd, taud, lse_d, dWd, dbd, dtaud};
+  return hip_status(fs::launch_bwd(g, mix_args(mix), x, fx, Ws, bias, tau, z, s, zmix,
+                                   attn_probs, lse, dout, dx, dfx, dWs, dbias, dtau,
+                                   mix->kind == FS_MIX_IDENTITY ? nullptr : dmix_params,
+                                   dzmix_out, static_cast<char*>(ws),
+                                   static_cast<hipStream_t>(hip_stream), &u));
 }
 
 int fs_set_pass_events(int pass, void* before, void* after) {

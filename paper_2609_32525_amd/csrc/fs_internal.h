@@ -15,6 +15,7 @@ struct Geom {
   bool bf16;
   float eps;
   bool ws_per_head;
+  bool untied = false;  // backward of the untied variant (separate deslice projection)
   int BH() const { return (int)(B * H); }
 };
 
@@ -97,6 +98,9 @@ hipError_t run_pass_slice_blk(const Geom& g, const PassArgs& a, hipStream_t st);
 hipError_t run_pass_point(const Geom& g, const PassArgs& a, hipStream_t st);
 size_t point_image_bytes(const Geom& g);  // workspace of the point-owned pass's operand images
 hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, hipStream_t st);
+// Untied variant, backward pass B in two parts: role 1 the slice weights (writes dx, dfx),
+// role 2 the deslice weights (adds to dx); each writes its own parameter partials.
+hipError_t run_pass_bwd_b_untied(const Geom& g, const PassArgs& a, int role, hipStream_t st);
 
 // Per-thread measurement events recorded around the streaming passes (fs_set_pass_events).
 struct PassEvents {
@@ -110,7 +114,7 @@ struct FwdWs {
   size_t partU, partS, lse, total;  // lse: [BH][N] when the blocked family needs it
 };
 struct BwdWs {
-  size_t partDZ, dzm, dz, dU, ds, cen, partP, partM, scr, cpt, img, total;
+  size_t partDZ, dzm, dz, dU, ds, cen, partP, partM, scr, cpt, img, partP2, total;
 };
 // Floats of one parameter partial of backward pass B: [D G] dW_s, [G] dbias, then one fp64
 // dtau partial per slot block.
@@ -170,10 +174,22 @@ hipError_t launch_reduce_rows(const Geom& g, const float* part, float* out, int 
 hipError_t launch_reduce_params(const Geom& g, const float* part, float* dWs, float* dbias,
                                 float* dtau, int chunks, int nblk, const MixArgs* m,
                                 const float* partM, float* dmix, hipStream_t st);
+// The deslice's own projection, bias, temperature and normaliser, and their gradients.
+struct UntiedArgs {
+  const float* Wd;
+  const float* bd;
+  const float* taud;
+  const float* lse_d;
+  float* dWd;
+  float* dbd;
+  float* dtaud;
+};
+// Backward of the path; with u given, of the untied variant (g.untied set).
 hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void* fx,
                       const float* Ws, const float* bias, const float* tau, const float* z,
                       const float* s, const float* zmix, const float* attn, const float* lse,
                       const void* dout, void* dx, void* dfx, float* dWs, float* dbias,
-                      float* dtau, float* dmix, float* dzm_out, char* ws, hipStream_t st);
+                      float* dtau, float* dmix, float* dzm_out, char* ws, hipStream_t st,
+                      const UntiedArgs* u = nullptr);
 
 }  // namespace fs

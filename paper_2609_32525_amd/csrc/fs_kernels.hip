@@ -99,7 +99,8 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
                       const float* Ws, const float* bias, const float* tau, const float* z,
                       const float* s, const float* zmix, const float* attn, const float* lse,
                       const void* dout, void* dx, void* dfx, float* dWs, float* dbias,
-                      float* dtau, float* dmix, float* dzm_out, char* ws, hipStream_t st) {
+                      float* dtau, float* dmix, float* dzm_out, char* ws, hipStream_t st,
+                      const UntiedArgs* u) {
   const BwdWs L = bwd_ws_layout(g, m.kind);
   float* partDZ = reinterpret_cast<float*>(ws + L.partDZ);
   float* dzm = dzm_out != nullptr ? dzm_out : reinterpret_cast<float*>(ws + L.dzm);
@@ -108,14 +109,14 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
   float* dsv = reinterpret_cast<float*>(ws + L.ds);
   float* partP = reinterpret_cast<float*>(ws + L.partP);
   float* partM = reinterpret_cast<float*>(ws + L.partM);
-  // pass A: dzmix = w^T dout
+  // pass A: dzmix = w^T dout (the deslice weights)
   PassArgs a = base_args(g, PASS_BWD_A);
   a.x = x;
   a.dout = dout;
-  a.Ws = Ws;
-  a.bias = bias;
-  a.tau = tau;
-  a.lse_in = lse;
+  a.Ws = u ? u->Wd : Ws;
+  a.bias = u ? u->bd : bias;
+  a.tau = u ? u->taud : tau;
+  a.lse_in = u ? u->lse_d : lse;
   a.part = partDZ;
   hipError_t e = timed(PASS_BWD_A, st, [&] { return run_pass_bwd_a(g, a, st); });
   if (e != hipSuccess) return e;
@@ -142,6 +143,25 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
   b.cen = cen;
   b.lse_in = lse;
   b.part = partP;
+  if (u != nullptr) {
+    // untied: the slice weights' part writes dx and dfx; the deslice weights' part (own
+    // projection, bias, temperature and normaliser) adds its dx contribution
+    PassArgs b2 = b;
+    b2.Ws = u->Wd;
+    b2.bias = u->bd;
+    b2.tau = u->taud;
+    b2.lse_in = u->lse_d;
+    b2.part = reinterpret_cast<float*>(ws + L.partP2);
+    e = timed(PASS_BWD_B, st, [&] {
+      hipError_t e1 = run_pass_bwd_b_untied(g, b, 1, st);
+      return e1 != hipSuccess ? e1 : run_pass_bwd_b_untied(g, b2, 2, st);
+    });
+    if (e != hipSuccess) return e;
+    e = launch_reduce_params(g, partP, dWs, dbias, dtau, b.chunks, b.nblk, &m, partM, dmix, st);
+    if (e != hipSuccess) return e;
+    return launch_reduce_params(g, b2.part, u->dWd, u->dbd, u->dtaud, b.chunks, b.nblk, nullptr,
+                                nullptr, nullptr, st);
+  }
   if (blocked(g)) {
     // point-owned pass (dx, dfx, per-point c and tb), then the slot-owned parameter pass
     PassArgs pa = base_args(g, PASS_POINT);

@@ -12,14 +12,19 @@ namespace {
 // Backward pass B: point gradients and parameter partials
 // partial layout per workgroup: [D * G] dW_s (row-major (D, G)), [G] dbias, [2] fp64 dtau
 // PB: 16-point blocks per tile (1 or 2; bf16 needs 2: its contraction over points has K=32).
+// ROLE: 0 the tied path (one set of weights feeds the slice and the deslice); in the untied
+// variant, 1 is the slice weights' part (dw = F dU^T + ds; writes dfx and dx) and 2 the
+// deslice weights' part (dw = dO zmix^T; adds its dx contribution to the dx already written).
 // With at most two slot groups, the per-head operands live in LDS as register images shared
 // by the workgroup's wavefronts and are read where they are used, which keeps the register
 // count (and so the number of resident wavefronts) in line with the other passes.
 // =======================================================================================
-template <bool BF, int D, int GS, int NS, int NP, int PB, bool PM>
+template <bool BF, int D, int GS, int NS, int NP, int PB, bool PM, int ROLE>
 __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_BWD_B))) void k_bwd_b(
     PassArgs a) {
   static_assert(PB == 2 || !BF, "bf16 contracts over 32 points");
+  static_assert(!PM || ROLE == 0, "the untied parts are point-and-parameter kernels");
+  constexpr bool USE_DOUT = ROLE != 1, USE_FX = ROLE != 2;
   constexpr int GB = GS / 16, VB = D / 16, DB = D / 16, TP = 16 * PB;
   constexpr bool SPLIT = BF;
   using T = typename Store<BF>::T;
@@ -54,7 +59,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       bT[gb][r] = c.sc * c.bias[c.g0 + 16 * gb + 4 * j + r];
-      dsT[gb][r] = a.ds[(int64_t)c.bh * a.G + c.g0 + 16 * gb + 4 * j + r] - cen[2 * D];
+      dsT[gb][r] = ROLE == 2 ? 0.f : a.ds[(int64_t)c.bh * a.G + c.g0 + 16 * gb + 4 * j + r] - cen[2 * D];
     }
 
   // operands: W_s (logits), zmix and dU (dw, contraction over v), dU (dfx) and W_s / tau (dx)
@@ -142,6 +147,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
     RowOp<BF, D> xo[PB], go[PB], fo[PB];
     float lse2[PB];
     float ct[PM ? PB : 1][2];
+    f4 dx0[ROLE == 2 ? DB : 1][PB];  // the dx already written (untied deslice part)
   };
   auto load_tile = [&](Tile& tt, int t) {
     const int tb = (t * NP + wpu) * TP;
@@ -149,8 +155,15 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
     for (int pb = 0; pb < PB; ++pb) {
       const int so = (tb + 16 * pb) * rsb;
       load_row_buf<BF, D>(tt.xo[pb], rx, i * rsb, so, j);
-      load_row_buf<BF, D>(tt.go[pb], rg, i * rsb, so, j);
-      load_row_buf<BF, D>(tt.fo[pb], rf, i * rsb, so, j);
+      if constexpr (USE_DOUT) load_row_buf<BF, D>(tt.go[pb], rg, i * rsb, so, j);
+      if constexpr (USE_FX) load_row_buf<BF, D>(tt.fo[pb], rf, i * rsb, so, j);
+      if constexpr (ROLE == 2) {
+        if (ws == 0) {
+#pragma unroll
+          for (int cb = 0; cb < DB; ++cb)
+            tt.dx0[cb][pb] = bld_row4<BF>(rdx, i * rsb + (16 * cb + 4 * j) * (int)sizeof(T), so);
+        }
+      }
       const float l = bld32(rl, 4 * i, 4 * (tb + 16 * pb));
       tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
       if constexpr (PM) {
@@ -195,8 +208,8 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
         for (int pb = 0; pb < PB; ++pb) {
           f4 g = f4{dsT[gb][0], dsT[gb][1], dsT[gb][2], dsT[gb][3]};
-          g = mm_slot_row<BF, D, GB, false>(zv, gb, go[pb], g);
-          g = mm_slot_row<BF, D, GB, false>(uv, gb, fo[pb], g);
+          if constexpr (USE_DOUT) g = mm_slot_row<BF, D, GB, false>(zv, gb, go[pb], g);
+          if constexpr (USE_FX) g = mm_slot_row<BF, D, GB, false>(uv, gb, fo[pb], g);
           dw[gb][pb] = g;
         }
     }
@@ -271,7 +284,8 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
       for (int pb = 0; pb < PB; ++pb) {
 #pragma unroll
-        for (int vb = 0; vb < VB; ++vb) gf[vb][pb] = mm_gop_tile<BF, GB, VB, PB>(ug, vb, w, pb, zero4());
+        for (int vb = 0; vb < VB; ++vb)
+          gf[vb][pb] = ROLE == 2 ? zero4() : mm_gop_tile<BF, GB, VB, PB>(ug, vb, w, pb, zero4());
 #pragma unroll
         for (int d = 0; d < DB; ++d) gx_[d][pb] = mm_gop_tile<BF, GB, DB, PB>(wg, d, dw, pb, zero4());
       }
@@ -279,7 +293,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
     if constexpr (NS > 1) {
       __syncthreads();  // every wave has read cx and finished the previous da transposes
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
+      for (int half = ROLE == 2 ? 1 : 0; half < 2; ++half) {
         f4(*src)[PB] = half == 0 ? gf : gx_;
         if (ws > 0) {
 #pragma unroll
@@ -306,8 +320,12 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
         for (int cb = 0; cb < VB; ++cb) {
           const int vo = i * rsb + (16 * cb + 4 * j) * (int)sizeof(T), so = (tp0 + 16 * pb) * rsb;
-          bst_row4<BF>(rdf, gf[cb][pb], vo, so);
-          bst_row4<BF>(rdx, gx_[cb][pb], vo, so);
+          if constexpr (ROLE == 2) {
+            bst_row4<BF>(rdx, gx_[cb][pb] + cur.dx0[cb][pb], vo, so);
+          } else {
+            bst_row4<BF>(rdf, gf[cb][pb], vo, so);
+            bst_row4<BF>(rdx, gx_[cb][pb], vo, so);
+          }
         }
     }
     }
@@ -430,7 +448,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   }
 }
 
-template <bool PM>
+template <bool PM, int ROLE>
 struct Run_k_bwd_b_ {
   template <bool BF, int D, int GS, int NS, int NP, int PB>
   struct R {
@@ -439,7 +457,8 @@ struct Run_k_bwd_b_ {
         return hipErrorInvalidConfiguration;
       } else {
         dim3 grid(cfg.chunks * BH * cfg.nblk);
-        hipLaunchKernelGGL((k_bwd_b<BF, D, GS, NS, NP, PB, PM>), grid, dim3(64 * NS * NP), 0, st, a);
+        hipLaunchKernelGGL((k_bwd_b<BF, D, GS, NS, NP, PB, PM, ROLE>), grid, dim3(64 * NS * NP), 0,
+                           st, a);
         return hipGetLastError();
       }
     }
@@ -449,11 +468,17 @@ struct Run_k_bwd_b_ {
 }  // namespace
 
 hipError_t run_pass_bwd_b(const Geom& g, const PassArgs& a, hipStream_t st) {
-  return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<false>::R>(g, a, st);
+  return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<false, 0>::R>(g, a, st);
 }
 
 hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, hipStream_t st) {
-  return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<true>::R>(g, a, st);
+  return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<true, 0>::R>(g, a, st);
+}
+
+hipError_t run_pass_bwd_b_untied(const Geom& g, const PassArgs& a, int role, hipStream_t st) {
+  if (role == 1) return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<false, 1>::R>(g, a, st);
+  if (role == 2) return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<false, 2>::R>(g, a, st);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace fs

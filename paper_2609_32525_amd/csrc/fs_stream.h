@@ -199,6 +199,17 @@ __device__ __forceinline__ void bst_row4(__amdgpu_buffer_rsrc_t r, f4 v, int vof
   }
 }
 
+// Four values of one row in the storage dtype (the counterpart of bst_row4), as fp32.
+template <bool BF>
+__device__ __forceinline__ f4 bld_row4(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  if constexpr (!BF) {
+    return bld128(r, voff, soff);
+  } else {
+    const uint2 v = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+    return f4{bf_to_f(v.x & 0xFFFFu), bf_to_f(v.x >> 16), bf_to_f(v.y & 0xFFFFu), bf_to_f(v.y >> 16)};
+  }
+}
+
 // Row operand from a buffer: rowoff = byte offset of the lane's row (point 16 pb + i of the
 // tile, scalar part in soff). Same register layout as load_row.
 template <bool BF, int D>

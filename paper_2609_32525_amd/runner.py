@@ -10,7 +10,8 @@ from typing import Dict, Optional
 import numpy as np
 
 from . import (BF16, F32, MIX_ATTN, MIX_IDENTITY, MIX_LINEAR_C, MIX_LINEAR_G, MixDesc, Problem,
-               deslice_fwd, mix, slice_deslice_bwd, slice_fwd, workspace_bytes)
+               deslice_fwd, deslice_stats_fwd, mix, slice_deslice_bwd, slice_fwd, untied_bwd,
+               workspace_bytes)
 
 
 class PathBuffers:
@@ -22,11 +23,13 @@ class PathBuffers:
     given points along N.
     keep_lse: False runs the forward with no saved normaliser (the slice writes no lse and
     the deslice recomputes it); only with with_backward=False.
+    untied: dict with the deslice's own Wd, bd, taud (the untied variant): the deslice runs
+    fs_deslice_stats_fwd with them (saving lse_d) and the backward is fs_untied_bwd.
     """
 
     def __init__(self, inp: Dict, kind: int, dtype: str = "f32", eps: float = 1e-5,
                  device: str = "cuda:0", with_backward: bool = True, repeat: int = 1,
-                 keep_lse: bool = True):
+                 keep_lse: bool = True, untied: Optional[Dict] = None):
         import torch
         self.torch = torch
         self.dev = torch.device(device)
@@ -57,6 +60,9 @@ class PathBuffers:
         self.Ws = up(Ws)
         self.b = up(inp["b"])
         self.tau = up(inp["tau"])
+        self.untied = untied is not None
+        if self.untied:
+            self.Wd, self.bd, self.taud = up(untied["Wd"]), up(untied["bd"]), up(untied["taud"])
         self.params = {}
         for k in ("A", "Wc", "Wq", "Wk", "Wv"):
             if inp.get(k) is not None:
@@ -73,6 +79,7 @@ class PathBuffers:
         self.zmix = torch.empty((B, H, G, V), **f32)
         self.attn = torch.empty((B, H, G, G), **f32) if kind == MIX_ATTN else None
         self.lse = torch.empty((B, H, N), **f32) if keep_lse else None
+        self.lse_d = torch.empty((B, H, N), **f32) if self.untied else None
         self.out = torch.empty((B, N, H, V), device=self.dev, dtype=sdt)
         self.ws_f = torch.empty(max(1, workspace_bytes(self.prob, False)), device=self.dev,
                                 dtype=torch.uint8)
@@ -88,18 +95,33 @@ class PathBuffers:
             nparam = {MIX_IDENTITY: 0, MIX_LINEAR_G: A.numel() if A is not None else 0,
                       MIX_LINEAR_C: V * V, MIX_ATTN: 3 * V * V}[kind]
             self.dmix = torch.empty(max(nparam, 1), **f32) if nparam else None
-            self.ws_b = torch.empty(max(1, workspace_bytes(self.prob, True)), device=self.dev,
-                                    dtype=torch.uint8)
+            self.ws_b = torch.empty(max(1, workspace_bytes(self.prob, 2 if self.untied else 1)),
+                                    device=self.dev, dtype=torch.uint8)
+            if self.untied:
+                self.dWd = torch.empty_like(self.Wd)
+                self.dbd = torch.empty_like(self.bd)
+                self.dtaud = torch.empty_like(self.taud)
 
     # ---- launches ------------------------------------------------------------------------
     def forward(self, stream=None) -> None:
         slice_fwd(self.prob, self.x, self.fx, self.Ws, self.b, self.tau, self.z, self.s,
                   self.lse, self.ws_f, stream=stream)
         mix(self.prob, self.mixdesc, self.z, self.zmix, self.attn, stream=stream)
+        if self.untied:
+            deslice_stats_fwd(self.prob, self.x, self.Wd, self.bd, self.taud, self.zmix,
+                              self.lse_d, self.out, stream=stream)
+            return
         deslice_fwd(self.prob, self.x, self.Ws, self.b, self.tau, self.zmix, self.lse,
                     self.out, stream=stream)
 
     def backward(self, stream=None) -> None:
+        if self.untied:
+            untied_bwd(self.prob, self.mixdesc, self.x, self.fx, self.Ws, self.b, self.tau,
+                       self.Wd, self.bd, self.taud, self.z, self.s, self.zmix, self.attn,
+                       self.lse, self.lse_d, self.dout, self.dx, self.dfx, self.dWs, self.db,
+                       self.dtau, self.dWd, self.dbd, self.dtaud, self.dmix, self.dzmix,
+                       self.ws_b, stream=stream)
+            return
         slice_deslice_bwd(self.prob, self.mixdesc, self.x, self.fx, self.Ws, self.b, self.tau,
                           self.z, self.s, self.zmix, self.attn, self.lse, self.dout, self.dx,
                           self.dfx, self.dWs, self.db, self.dtau, self.dmix, self.dzmix,
@@ -119,9 +141,13 @@ class PathBuffers:
 
         r = dict(z=h(self.z), s=h(self.s), zmix=h(self.zmix), P=h(self.attn), lse=h(self.lse),
                  out=h(self.out))
+        if self.untied:
+            r["lse_d"] = h(self.lse_d)
         if self.with_backward:
             r.update(dx=h(self.dx), dfx=h(self.dfx), dWs=h(self.dWs), db=h(self.db),
                      dtau=h(self.dtau), dzmix=h(self.dzmix))
+            if self.untied:
+                r.update(dWd=h(self.dWd), dbd=h(self.dbd), dtaud=h(self.dtaud))
             if self.dmix is not None:
                 d = h(self.dmix)
                 if self.kind == MIX_LINEAR_G:

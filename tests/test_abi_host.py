@@ -232,3 +232,34 @@ def test_deslice_validation():
     zm = f()
     assert call("fs_deslice_stats_fwd", zmix=zm, lse=zm) == ALIAS           # lse output on an input
     assert call("fs_deslice_stats_fwd", lse=f(4)) == ALIGN
+
+
+def test_untied_validation():
+    # every call below fails validation before any launch
+    f = Fake()
+    L = fs.lib()
+    p = prob()
+    lin = MixDesc.make(fs.MIX_LINEAR_G, A=f())
+    st, need = ws_bytes(p, 2)
+    assert st == OK
+    _, need_tied = ws_bytes(p, 1)
+    assert need > need_tied       # the deslice weights' parameter partials
+    assert ws_bytes(p, 3)[0] == ARG
+
+    def call(**over):
+        names = ("x", "fx", "Ws", "b", "tau", "Wd", "bd", "taud", "z", "s", "zmix", "attn", "lse",
+                 "lse_d", "dout", "dx", "dfx", "dWs", "db", "dtau", "dWd", "dbd", "dtaud", "dmix",
+                 "dzm", "ws")
+        a = {k: f() for k in names}
+        nb = over.pop("ws_bytes", need)
+        a.update(over)
+        return L.fs_untied_bwd(ctypes.byref(p), ctypes.byref(lin), *[a[k] for k in names], nb,
+                               None)
+
+    assert call(ws_bytes=need - 1) == WS
+    assert call(lse_d=None) == NULL
+    assert call(Wd=None) == NULL
+    assert call(dtaud=None) == NULL
+    x = f()
+    assert call(x=x, dWd=x + 64) == ALIAS
+    assert call(taud=f(4)) == ALIGN

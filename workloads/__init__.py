@@ -165,6 +165,23 @@ def make_inputs(w: Workload, with_grad: bool = True) -> Dict[str, Optional[np.nd
     return out
 
 
+_K_WD, _K_BD, _K_TAUD = 20, 21, 22
+
+
+def untied_params(w: Workload) -> Dict[str, np.ndarray]:
+    """The deslice's own projection, bias and temperature for the untied variant: W_d drawn
+    like W_s (own sub-stream), b_d ~ N(0, 0.1^2), tau_d ~ U[0.4, 1.0] per head."""
+    D, G, H = w.D, w.G, w.H
+    ws_shape = (H, D, G) if w.ws_per_head else (D, G)
+    if w.ws_mode == "xavier":
+        Wd = _xavier(_rng(w, _K_WD), ws_shape, D, G)
+    else:
+        Wd = _normal(_rng(w, _K_WD), ws_shape, 3.0 / math.sqrt(D))
+    bd = _normal(_rng(w, _K_BD), (H, G) if w.ws_per_head else (G,), 0.1)
+    taud = _rng(w, _K_TAUD).uniform(0.4, 1.0, size=(H,)).astype(np.float32)
+    return dict(Wd=Wd, bd=bd, taud=taud)
+
+
 def random_like(w: Workload, seed_k: int, shape, std=1.0) -> np.ndarray:
     """Extra seeded N(0, std^2) tensor (for tests that need more random data)."""
     rng = np.random.default_rng([SEED, w.cfg_id, 1000 + seed_k, w.G])
