@@ -19,6 +19,10 @@ What it computes (paper: Sec. 2 "The Transolver layer"; Eq. (1); App. F.1 "Kerne
            variant of Sec. 2), or single-head softmax self-attention among the G tokens
 * deslice  O = w z'                                         (Sec. 2, u_i = sum_g w_ig z'_g)
 
+Two variants of the ablation suite (Sec. 2) are here as well: the untied one (the deslice
+with its own projection, bias and temperature) and LinearNO (untied, with the slice weights
+normalised by a softmax over the points of each slot; App. E).
+
 The backward is derived from these definitions (the paper prints only the temperature
 gradient and the per-point cancellation, App. F.2 "Temperature gradients"):
 
@@ -407,6 +411,118 @@ def untied_backward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm: Optional[Dict], 
             else:
                 res.setdefault(k, np.zeros_like(v))
                 res[k] += v
+    return res
+
+
+# ----------------------------------------------------------------------------------------
+# LinearNO (the Untied-LN variant of Sec. 2 and App. E): the slice weights are normalised by
+# a softmax over the N points of each slot, k[:, g] = softmax_n(a[:, g]), so the tokens are
+# z_g = sum_n k[n, g] F[n] with no division by a weight sum; the deslice has its own
+# projection, bias and temperature with the usual softmax over the slots
+# ----------------------------------------------------------------------------------------
+def point_softmax(a):
+    """Softmax of each slot's logits over the points, with its log-sum-exp per slot
+    (natural log); an empty point set gives no weights and lse = -inf."""
+    if a.shape[0] == 0:
+        return a.copy(), np.full(a.shape[1], -np.inf)
+    m = a.max(axis=0, keepdims=True)
+    e = np.exp(a - m)
+    l = e.sum(axis=0, keepdims=True)
+    return e / l, (m + np.log(l))[0]
+
+
+def point_softmax_backward(k, dk):
+    """da = k * (dk - sum_n k dk), per slot (so sum_n da[:, g] = 0)."""
+    return k * (dk - (k * dk).sum(axis=0, keepdims=True))
+
+
+def linearno_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm: Optional[Dict] = None,
+                     pairs=None, dtype=f64) -> Dict[str, np.ndarray]:
+    """Returns z (B,H,G,V), clse (B,H,G) (the slots' log normalisers over the points,
+    natural log), zmix, P, lse_d (B,H,N) and out."""
+    prm = prm or {}
+    B, N, H, D = x.shape
+    V = fx.shape[3]
+    G = np.asarray(Ws).shape[-1]
+    res = {k: np.zeros(sh) for k, sh in dict(
+        z=(B, H, G, V), clse=(B, H, G), zmix=(B, H, G, V), lse_d=(B, H, N),
+        out=(B, N, H, V)).items()}
+    res["P"] = np.zeros((B, H, G, G)) if kind == MIX_ATTN else None
+    ct = np.dtype(dtype).type
+    for bb, h in _pairs(B, H, pairs):
+        X = np.asarray(x[bb, :, h, :], dtype=ct)
+        F = np.asarray(fx[bb, :, h, :], dtype=ct)
+        Wsh, bh = _ws_b(Ws, b, h, ct)
+        Wdh, bdh = _ws_b(Wd, bd, h, ct)
+        k, clse = point_softmax(logits(X, Wsh, bh, ct(tau[h])))
+        z = k.T @ F
+        zm, P = mix_forward(kind, z, _head_params(kind, prm, h, ct))
+        wd, lse_d = slot_softmax(logits(X, Wdh, bdh, ct(taud[h])))
+        res["z"][bb, h], res["clse"][bb, h], res["zmix"][bb, h] = z, clse, zm
+        res["lse_d"][bb, h] = lse_d
+        if P is not None:
+            res["P"][bb, h] = P
+        res["out"][bb, :, h, :] = deslice(wd, zm)
+    return res
+
+
+def linearno_backward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm: Optional[Dict], dout,
+                      fwd: Optional[Dict] = None, pairs=None,
+                      dtype=f64) -> Dict[str, np.ndarray]:
+    """Backward of LinearNO: the deslice part as in untied_backward; the slice weights get
+    dk = F dz^T through the softmax over the points. Returns dx, dfx, dWs, db, dtau, dWd,
+    dbd, dtaud, dzmix, dz and the mix-parameter gradients."""
+    prm = prm or {}
+    B, N, H, D = x.shape
+    V = fx.shape[3]
+    Ws_arr, b_arr = np.asarray(Ws, dtype=f64), np.asarray(b, dtype=f64)
+    Wd_arr, bd_arr = np.asarray(Wd, dtype=f64), np.asarray(bd, dtype=f64)
+    G = Ws_arr.shape[-1]
+    if fwd is None:
+        fwd = linearno_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm, pairs=pairs,
+                               dtype=dtype)
+    ct = np.dtype(dtype).type
+    res = dict(dx=np.zeros((B, N, H, D)), dfx=np.zeros((B, N, H, V)),
+               dWs=np.zeros_like(Ws_arr), db=np.zeros_like(b_arr), dtau=np.zeros(H),
+               dWd=np.zeros_like(Wd_arr), dbd=np.zeros_like(bd_arr), dtaud=np.zeros(H),
+               dzmix=np.zeros((B, H, G, V)), dz=np.zeros((B, H, G, V)))
+    for bb, h in _pairs(B, H, pairs):
+        X = np.asarray(x[bb, :, h, :], dtype=ct)
+        F = np.asarray(fx[bb, :, h, :], dtype=ct)
+        dO = np.asarray(dout[bb, :, h, :], dtype=ct)
+        Wsh, bh = _ws_b(Ws, b, h, ct)
+        Wdh, bdh = _ws_b(Wd, bd, h, ct)
+        t, td = ct(tau[h]), ct(taud[h])
+        a = logits(X, Wsh, bh, t)
+        k, _ = point_softmax(a)
+        ad = logits(X, Wdh, bdh, td)
+        wd, _ = slot_softmax(ad)
+        z, zm = fwd["z"][bb, h].astype(ct), fwd["zmix"][bb, h].astype(ct)
+        P = fwd["P"][bb, h].astype(ct) if fwd.get("P") is not None else None
+        dzm = wd.T @ dO
+        dz, dprm = mix_backward(kind, z, P, dzm, _head_params(kind, prm, h, ct))
+        da = point_softmax_backward(k, F @ dz.T)
+        dad = softmax_backward(wd, dO @ zm.T)
+        dX, dWs, db, dtau = logit_backward(da, X, Wsh, a, t)
+        dXd, dWd, dbd, dtaud = logit_backward(dad, X, Wdh, ad, td)
+        res["dx"][bb, :, h, :] = dX + dXd
+        res["dfx"][bb, :, h, :] = k @ dz
+        res["dzmix"][bb, h], res["dz"][bb, h] = dzm, dz
+        res["dtau"][h] += dtau
+        res["dtaud"][h] += dtaud
+        for key, arr, val in (("dWs", Ws_arr, dWs), ("db", b_arr, db), ("dWd", Wd_arr, dWd),
+                              ("dbd", bd_arr, dbd)):
+            per_head = arr.ndim == (3 if key in ("dWs", "dWd") else 2)
+            if per_head:
+                res[key][h] += val
+            else:
+                res[key] += val
+        for kk, v in dprm.items():
+            if kk == "dA" and np.asarray(prm["A"]).ndim == 3:
+                res.setdefault(kk, np.zeros((H, G, G)))[h] += v
+            else:
+                res.setdefault(kk, np.zeros_like(v))
+                res[kk] += v
     return res
 
 

@@ -429,12 +429,85 @@ def check_untied_cancellation_and_temperature(o):
         assert np.abs(lhs).max() > 1e-5
 
 
+def check_linearno_finite_differences(o, kinds=(MIXES[1], MIXES[2], MIXES[3])):
+    """LinearNO: central differences of L = sum(O * R) in fp64 match every analytic
+    gradient."""
+    for kind in kinds:
+        x, fx, Ws, b, tau, Wd, bd, taud, rng = _untied_problem(
+            80 + kind, B=2, N=5, H=2, D=3, V=2, G=4)
+        prm = _prm(kind, 4, 2, rng)
+        R = rng.standard_normal((2, 5, 2, 2))
+        fwd = o.linearno_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm)
+        g = o.linearno_backward(x, fx, Ws, b, tau, Wd, bd, taud, kind, prm, R, fwd=fwd)
+        tensors = {"dx": x, "dfx": fx, "dWs": Ws, "db": b, "dtau": tau, "dWd": Wd, "dbd": bd,
+                   "dtaud": taud}
+        for k in ("A", "Wc", "Wq", "Wk", "Wv"):
+            if prm.get(k) is not None:
+                tensors["d" + k] = prm[k]
+        step = 1e-6
+        for gname, arr in tensors.items():
+            num = np.zeros_like(arr)
+            for idx in np.ndindex(arr.shape):
+                old = arr[idx]
+                vals = []
+                for sgn in (1, -1):
+                    arr[idx] = old + sgn * step
+                    vals.append((o.linearno_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind,
+                                                    prm)["out"] * R).sum())
+                arr[idx] = old
+                num[idx] = (vals[0] - vals[1]) / (2 * step)
+            # the slice bias gradient is identically zero here: gate it by rounding noise
+            scale = max(np.abs(num).max(), 1e-2)
+            err = np.abs(g[gname] - num).max() / scale
+            assert err < 2e-7, (kind, gname, err)
+
+
+def check_linearno_closed_forms(o):
+    """LinearNO's slice weights are a partition of unity over the points of each slot: they
+    sum to one per slot, zero logits give every slot the plain mean of F, one dominant point
+    per slot (hard assignment) gives that point's F, and a constant added to one slot's
+    logits changes nothing (so the slice bias gets no gradient)."""
+    x, fx, Ws, b, tau, Wd, bd, taud, rng = _untied_problem(90, B=2, N=12, H=2, D=3, V=2, G=4)
+    kind = o.MIX_IDENTITY
+    a = rng.standard_normal((12, 4)) * 3
+    k, lse = o.point_softmax(a)
+    np.testing.assert_allclose(k.sum(axis=0), 1.0, atol=1e-13)
+    np.testing.assert_allclose(k, np.exp(a - lse[None, :]), rtol=1e-12)
+    r = o.linearno_forward(x, fx, np.zeros_like(Ws), np.zeros_like(b), tau, Wd, bd, taud, kind)
+    np.testing.assert_allclose(r["z"], np.broadcast_to(fx.mean(axis=1)[:, :, None, :],
+                                                       r["z"].shape), rtol=1e-12, atol=1e-14)
+    # hard assignment: slot g's logit is huge only at point g (D = G, X = identity rows)
+    X = np.zeros((1, 12, 1, 4))
+    for g in range(4):
+        X[0, 3 * g, 0, g] = 1.0
+    F = rng.standard_normal((1, 12, 1, 2))
+    r = o.linearno_forward(X, F, 200.0 * np.eye(4), np.zeros(4), np.ones(1), np.eye(4),
+                           np.zeros(4), np.ones(1), kind)
+    np.testing.assert_allclose(r["z"][0, 0], F[0, [0, 3, 6, 9], 0], rtol=1e-10)
+    # per-slot constant shift of the logits: no change, hence db = 0
+    r1 = o.linearno_forward(x, fx, Ws, b, tau, Wd, bd, taud, kind)
+    r2 = o.linearno_forward(x, fx, Ws, b + np.arange(4.0), tau, Wd, bd, taud, kind)
+    np.testing.assert_allclose(r1["out"], r2["out"], rtol=1e-12, atol=1e-14)
+    R = rng.standard_normal(fx.shape)
+    gr = o.linearno_backward(x, fx, Ws, b, tau, Wd, bd, taud, o.MIX_LINEAR_C,
+                             _prm(o.MIX_LINEAR_C, 4, 2, rng), R)
+    assert np.abs(gr["db"]).max() < 1e-12 * max(1.0, np.abs(gr["dWs"]).max())
+    assert np.abs(gr["dWs"]).max() > 1e-4
+    # temperature identity (scale invariance of the slice logits), summed over the heads
+    # that share W_s and b: sum_h tau_h dtau_h = -(<W_s, dW_s> + <b, db>)
+    lhs = (tau * gr["dtau"]).sum()
+    np.testing.assert_allclose(lhs, -((Ws * gr["dWs"]).sum() + (b * gr["db"]).sum()),
+                               rtol=1e-10, atol=1e-13)
+    assert abs(lhs) > 1e-5
+
+
 ALL_CHECKS = [check_partition_of_unity, check_single_slice_mean, check_identical_points,
               check_constant_tokens, check_zero_logits, check_hard_assignment,
               check_bruteforce, check_invariances, check_mix_closed_forms,
               check_finite_differences, check_cancellation, check_temperature_identity,
               check_repeated_block, check_untied_finite_differences,
-              check_untied_reduces_to_tied, check_untied_cancellation_and_temperature]
+              check_untied_reduces_to_tied, check_untied_cancellation_and_temperature,
+              check_linearno_finite_differences, check_linearno_closed_forms]
 
 
 @pytest.mark.parametrize("check", ALL_CHECKS, ids=lambda c: c.__name__)
@@ -455,7 +528,7 @@ def _mutant(**overrides):
     m.__dict__.update(overrides)
     # re-bind the module-level drivers so they call the planted functions
     for name in ("forward", "backward", "untied_forward", "untied_backward",
-                 "forward_repeated"):
+                 "forward_repeated", "linearno_forward", "linearno_backward"):
         f = O.__dict__[name]
         m.__dict__[name] = types.FunctionType(f.__code__, m.__dict__, name, f.__defaults__)
     return m
@@ -522,6 +595,14 @@ def _mut_deslice_unmixed(w, zm):
     return w @ (zm * 0.5 + 0.5 * zm[::-1])   # mixes the wrong tokens
 
 
+def _mut_point_softmax_bwd(k, dk):   # the per-slot correction dropped
+    return k * dk
+
+
+def _mut_point_softmax_slots(a):     # LinearNO weights normalised over the slots instead
+    return O.slot_softmax(a)
+
+
 MUTANTS = {
     "dropped eps": dict(slice_tokens=_mut_no_eps),
     "bias not divided by tau": dict(logits=_mut_bias_outside),
@@ -535,6 +616,8 @@ MUTANTS = {
     "mix backward not transposed": dict(mix_backward=_mut_mixbwd_A),
     "token backward sign": dict(token_backward=_mut_token_bwd_sign),
     "deslice of the wrong tokens": dict(deslice=_mut_deslice_unmixed),
+    "LinearNO slice correction dropped": dict(point_softmax_backward=_mut_point_softmax_bwd),
+    "LinearNO weights over the slots": dict(point_softmax=_mut_point_softmax_slots),
 }
 
 
