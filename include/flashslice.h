@@ -101,10 +101,11 @@ typedef struct {
 } fs_mix_desc;
 
 /* Bytes of device workspace needed by fs_slice_fwd (for_backward = 0), by fs_mix_bwd and
- * fs_slice_deslice_bwd (for_backward = 1), or by fs_untied_bwd (for_backward = 2), for this
- * problem. The size never grows with N*G: it holds per-workgroup partial sums (bounded number
- * of workgroups) and token-sized buffers. Returns FS_OK and writes *bytes, or a validation
- * error (FS_ERR_ARG for another for_backward).                                             */
+ * fs_slice_deslice_bwd (for_backward = 1), by fs_untied_bwd (for_backward = 2), by
+ * fs_linearno_slice_fwd (for_backward = 3) or by fs_linearno_bwd (for_backward = 4), for
+ * this problem. The size never grows with N*G: it holds per-workgroup partial sums (bounded
+ * number of workgroups) and token-sized buffers. Returns FS_OK and writes *bytes, or a
+ * validation error (FS_ERR_ARG for another for_backward).                                  */
 int fs_workspace_bytes(const fs_problem* prob, int for_backward, size_t* bytes);
 
 /* Slice (paper: Sec. 2; App. F.1 single-tile equation): recompute the slice weights per
@@ -183,6 +184,35 @@ int fs_untied_bwd(const fs_problem* prob, const fs_mix_desc* mix, const void* x,
                   float* dbias, float* dtau, float* dWd, float* dbd, float* dtaud,
                   float* dmix_params, float* dzmix_out, void* ws, size_t ws_bytes,
                   void* hip_stream);
+
+/* LinearNO slice (paper: App. E and the Untied-LN row of the Sec. 2 ablation suite): the
+ * slice weights are normalised by a softmax over the N points of each slot,
+ * k[n, g] = exp(a[n, g]) / sum_n' exp(a[n', g]) with a = (x W_s + bias) / tau, and the tokens
+ * are z_g = sum_n k[n, g] fx[n] (B,H,G,V), with no division by a weight sum. One streaming
+ * pass with a running per-slot maximum; no N x G tensor is stored.
+ * clse (B,H,G) fp32, nullable: the base-2 log normaliser of every slot over the points,
+ * log2(sum_n 2^(a[n, g] log2 e)) (-inf for an empty point set, whose tokens are 0), needed by
+ * fs_linearno_bwd. Workspace: fs_workspace_bytes(prob, 3, .).
+ * The rest of the LinearNO forward is fs_mix (its layer uses FS_MIX_LINEAR_C) and
+ * fs_deslice_stats_fwd with the deslice's own Wd, bd, taud (writing lse_d).                */
+int fs_linearno_slice_fwd(const fs_problem* prob, const void* x, const void* fx,
+                          const float* Ws, const float* bias, const float* tau, float* z,
+                          float* clse, void* ws, size_t ws_bytes, void* hip_stream);
+
+/* Backward of LinearNO. Inputs: the forward's inputs, Wd, bd, taud, and saved z, clse, zmix,
+ * attn_probs (ATTN only), lse_d. The deslice weights carry dw_d = dout zmix^T (as in
+ * fs_untied_bwd); the slice weights carry dk = fx dz^T through the softmax over the points,
+ * da = k (dk - sum_n k dk) = k (fx dz^T - 1 (z . dz)^T). Outputs as in fs_untied_bwd: dx (both
+ * projections' contributions), dfx = k dz, dWs, dbias (zero up to rounding: a constant added
+ * to a slot's logits changes nothing), dtau, dWd, dbd, dtaud, dmix_params, dzmix_out.
+ * Workspace: fs_workspace_bytes(prob, 4, .).                                               */
+int fs_linearno_bwd(const fs_problem* prob, const fs_mix_desc* mix, const void* x, const void* fx,
+                    const float* Ws, const float* bias, const float* tau, const float* Wd,
+                    const float* bd, const float* taud, const float* z, const float* clse,
+                    const float* zmix, const float* attn_probs, const float* lse_d,
+                    const void* dout, void* dx, void* dfx, float* dWs, float* dbias,
+                    float* dtau, float* dWd, float* dbd, float* dtaud, float* dmix_params,
+                    float* dzmix_out, void* ws, size_t ws_bytes, void* hip_stream);
 
 /* Measurement aid: for calls made later on this thread, record the caller's hipEvent_t
  * `before` immediately before, and `after` immediately after, the launch of the streaming

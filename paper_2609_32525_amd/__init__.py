@@ -16,7 +16,8 @@ from typing import Optional
 __all__ = [
     "F32", "BF16", "MIX_IDENTITY", "MIX_LINEAR_G", "MIX_LINEAR_C", "MIX_ATTN",
     "FsError", "Problem", "MixDesc", "lib", "lib_path", "workspace_bytes", "slice_fwd", "mix",
-    "mix_bwd", "deslice_fwd", "deslice_stats_fwd", "slice_deslice_bwd", "untied_bwd", "status_string", "last_hip_error",
+    "mix_bwd", "deslice_fwd", "deslice_stats_fwd", "slice_deslice_bwd", "untied_bwd",
+    "linearno_slice_fwd", "linearno_bwd", "status_string", "last_hip_error",
     "set_pass_events", "EXPORTED", "PASS_SLICE", "PASS_DESLICE", "PASS_BWD_A", "PASS_BWD_B",
 ]
 
@@ -24,7 +25,8 @@ F32, BF16 = 0, 1
 MIX_IDENTITY, MIX_LINEAR_G, MIX_LINEAR_C, MIX_ATTN = 0, 1, 2, 3
 
 EXPORTED = ("fs_workspace_bytes", "fs_slice_fwd", "fs_mix", "fs_mix_bwd", "fs_deslice_fwd",
-            "fs_deslice_stats_fwd", "fs_slice_deslice_bwd", "fs_untied_bwd", "fs_set_pass_events", "fs_status_string",
+            "fs_deslice_stats_fwd", "fs_slice_deslice_bwd", "fs_untied_bwd",
+            "fs_linearno_slice_fwd", "fs_linearno_bwd", "fs_set_pass_events", "fs_status_string",
             "fs_last_hip_error")
 
 PASS_SLICE, PASS_DESLICE, PASS_BWD_A, PASS_BWD_B = 0, 1, 2, 3
@@ -92,6 +94,8 @@ def lib() -> ctypes.CDLL:
         L.fs_deslice_stats_fwd.argtypes = [prob, P, P, P, P, P, P, P, P]
         L.fs_slice_deslice_bwd.argtypes = [prob, mixp] + [P] * 19 + [S, P]
         L.fs_untied_bwd.argtypes = [prob, mixp] + [P] * 26 + [S, P]
+        L.fs_linearno_slice_fwd.argtypes = [prob] + [P] * 8 + [S, P]
+        L.fs_linearno_bwd.argtypes = [prob, mixp] + [P] * 25 + [S, P]
         L.fs_status_string.argtypes = [ctypes.c_int]
         L.fs_status_string.restype = ctypes.c_char_p
         L.fs_last_hip_error.argtypes = []
@@ -150,7 +154,8 @@ def set_pass_events(pass_id: int, before=None, after=None) -> None:
 
 
 def workspace_bytes(prob: Problem, for_backward) -> int:
-    """for_backward: 0 / False forward, 1 / True backward, 2 untied backward."""
+    """for_backward: 0 / False forward, 1 / True backward, 2 untied backward, 3 LinearNO
+    slice, 4 LinearNO backward."""
     out = ctypes.c_size_t(0)
     _check(lib().fs_workspace_bytes(ctypes.byref(prob), int(for_backward),
                                     ctypes.byref(out)), "fs_workspace_bytes")
@@ -209,3 +214,23 @@ def untied_bwd(prob, mixdesc, x, fx, Ws, b, tau, Wd, bd, taud, z, s, zmix, attn,
         _ptr(dtau), _ptr(dWd), _ptr(dbd), _ptr(dtaud), _ptr(dmix), _ptr(dzmix_out), _ptr(ws),
         _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
         "fs_untied_bwd")
+
+
+def linearno_slice_fwd(prob, x, fx, Ws, b, tau, z, clse, ws, ws_bytes=None, stream=None) -> None:
+    _check(lib().fs_linearno_slice_fwd(ctypes.byref(prob), _ptr(x), _ptr(fx), _ptr(Ws), _ptr(b),
+                                       _ptr(tau), _ptr(z), _ptr(clse), _ptr(ws),
+                                       _nbytes(ws) if ws_bytes is None else ws_bytes,
+                                       _stream(stream)),
+           "fs_linearno_slice_fwd")
+
+
+def linearno_bwd(prob, mixdesc, x, fx, Ws, b, tau, Wd, bd, taud, z, clse, zmix, attn, lse_d,
+                 dout, dx, dfx, dWs, db, dtau, dWd, dbd, dtaud, dmix, dzmix_out, ws,
+                 ws_bytes=None, stream=None) -> None:
+    _check(lib().fs_linearno_bwd(
+        ctypes.byref(prob), ctypes.byref(mixdesc), _ptr(x), _ptr(fx), _ptr(Ws), _ptr(b),
+        _ptr(tau), _ptr(Wd), _ptr(bd), _ptr(taud), _ptr(z), _ptr(clse), _ptr(zmix), _ptr(attn),
+        _ptr(lse_d), _ptr(dout), _ptr(dx), _ptr(dfx), _ptr(dWs), _ptr(db), _ptr(dtau), _ptr(dWd),
+        _ptr(dbd), _ptr(dtaud), _ptr(dmix), _ptr(dzmix_out), _ptr(ws),
+        _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
+        "fs_linearno_bwd")

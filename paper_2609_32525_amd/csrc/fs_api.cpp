@@ -139,6 +139,19 @@ FwdWs fwd_ws_layout(const Geom& g) {
   return L;
 }
 
+FwdWs linearno_fwd_ws_layout(const Geom& g) {
+  const PassCfg c = pick_cfg(g, PASS_SLICE);
+  FwdWs L{};
+  size_t off = 0;
+  L.partU = off;
+  off += up(sizeof(float) * (size_t)g.BH() * c.chunks * g.G * g.V);
+  L.partS = off;
+  off += up(sizeof(float) * (size_t)g.BH() * c.chunks * 2 * g.G);
+  L.lse = off;
+  L.total = off;
+  return L;
+}
+
 BwdWs bwd_ws_layout(const Geom& g, int kind) {
   const PassCfg ca = pick_cfg(g, PASS_BWD_A);
   const PassCfg cb = pick_cfg(g, PASS_BWD_B);
@@ -177,6 +190,8 @@ BwdWs bwd_ws_layout(const Geom& g, int kind) {
   off += up(g.untied ? sizeof(float) * (size_t)g.BH() * cb.chunks *
                            (size_t)param_partial_len(g, cb.nblk)
                      : 0);
+  L.ones = off;    // LinearNO: unit weight sums for the token gradients
+  off += up(g.linearno ? sizeof(float) * (size_t)g.BH() * g.G : 0);
   L.total = off;
   return L;
 }
@@ -326,14 +341,24 @@ int fs_workspace_bytes(const fs_problem* prob, int for_backward, size_t* bytes) 
   int st = check_problem(prob, &g);
   if (st != FS_OK) return st;
   if (bytes == nullptr) return FS_ERR_NULL;
-  if (for_backward < 0 || for_backward > 2) return FS_ERR_ARG;
-  if (for_backward) {
-    g.untied = for_backward == 2;
-    *bytes = bwd_required(g);
-  } else {
-    *bytes = fs::fwd_ws_layout(g).total;
+  switch (for_backward) {
+    case 0:
+      *bytes = fs::fwd_ws_layout(g).total;
+      return FS_OK;
+    case 1:
+    case 2:
+    case 4:
+      g.untied = for_backward != 1;
+      g.linearno = for_backward == 4;
+      *bytes = bwd_required(g);
+      return FS_OK;
+    case 3:
+      g.untied = g.linearno = true;
+      *bytes = fs::linearno_fwd_ws_layout(g).total;
+      return FS_OK;
+    default:
+      return FS_ERR_ARG;
   }
-  return FS_OK;
 }
 
 int fs_slice_fwd(const fs_problem* prob, const void* x, const void* fx, const float* Ws,
@@ -478,6 +503,73 @@ int fs_slice_deslice_bwd(const fs_problem* prob, const fs_mix_desc* mix, const v
                                    mix->kind == FS_MIX_IDENTITY ? nullptr : dmix_params,
                                    dzmix_out, static_cast<char*>(ws),
                                    static_cast<hipStream_t>(hip_stream)));
+}
+
+int fs_linearno_slice_fwd(const fs_problem* prob, const void* x, const void* fx,
+                          const float* Ws, const float* bias, const float* tau, float* z,
+                          float* clse, void* ws, size_t ws_bytes, void* hip_stream) {
+  Geom g;
+  int st = check_problem(prob, &g);
+  if (st != FS_OK) return st;
+  g.untied = g.linearno = true;
+  const Sizes zs = sizes(g);
+  const Buf in[] = {{x, zs.x, true}, {fx, zs.fx, true}, {Ws, zs.Ws, true}, {bias, zs.b, true},
+                    {tau, zs.tau, true}};
+  const Buf out[] = {{z, zs.tok, true}, {clse, zs.s, false}, {ws, ws_bytes, true}};
+  st = check_bufs(in, 5, out, 3);
+  if (st != FS_OK) return st;
+  if (ws == nullptr || ws_bytes < fs::linearno_fwd_ws_layout(g).total) return FS_ERR_WORKSPACE;
+  return hip_status(fs::launch_linearno_slice(g, x, fx, Ws, bias, tau, z, clse,
+                                              static_cast<char*>(ws),
+                                              static_cast<hipStream_t>(hip_stream)));
+}
+
+int fs_linearno_bwd(const fs_problem* prob, const fs_mix_desc* mix, const void* x, const void* fx,
+                    const float* Ws, const float* bias, const float* tau, const float* Wd,
+                    const float* bd, const float* taud, const float* z, const float* clse,
+                    const float* zmix, const float* attn_probs, const float* lse_d,
+                    const void* dout, void* dx, void* dfx, float* dWs, float* dbias,
+                    float* dtau, float* dWd, float* dbd, float* dtaud, float* dmix_params,
+                    float* dzmix_out, void* ws, size_t ws_bytes, void* hip_stream) {
+  Geom g;
+  int st = check_problem(prob, &g);
+  if (st != FS_OK) return st;
+  st = check_mix(mix, g);
+  if (st != FS_OK) return st;
+  g.untied = g.linearno = true;
+  const Sizes zs = sizes(g);
+  const bool attn = mix->kind == FS_MIX_ATTN;
+  Buf in[20];
+  int nin = 0;
+  mix_bufs(mix, g, in, &nin);
+  in[nin++] = {x, zs.x, true};
+  in[nin++] = {fx, zs.fx, true};
+  in[nin++] = {Ws, zs.Ws, true};
+  in[nin++] = {bias, zs.b, true};
+  in[nin++] = {tau, zs.tau, true};
+  in[nin++] = {Wd, zs.Ws, true};
+  in[nin++] = {bd, zs.b, true};
+  in[nin++] = {taud, zs.tau, true};
+  in[nin++] = {z, zs.tok, true};
+  in[nin++] = {clse, zs.s, true};
+  in[nin++] = {zmix, zs.tok, true};
+  in[nin++] = {attn ? attn_probs : nullptr, attn ? zs.attn : 0, true};
+  in[nin++] = {lse_d, zs.lse, true};
+  in[nin++] = {dout, zs.fx, true};
+  const size_t np = sizeof(float) * fs::mix_param_count(g, mix->kind, mix->a_per_head != 0);
+  const Buf out[] = {{dx, zs.x, true},       {dfx, zs.fx, true},        {dWs, zs.Ws, true},
+                     {dbias, zs.b, true},    {dtau, zs.tau, true},      {dWd, zs.Ws, true},
+                     {dbd, zs.b, true},      {dtaud, zs.tau, true},     {dmix_params, np, false},
+                     {dzmix_out, zs.tok, false}, {ws, ws_bytes, true}};
+  st = check_bufs(in, nin, out, 11);
+  if (st != FS_OK) return st;
+  if (ws == nullptr || ws_bytes < bwd_required(g)) return FS_ERR_WORKSPACE;
+  const fs::UntiedArgs u{Wd, bd, taud, lse_d, dWd, dbd, dtaud};
+  return hip_status(fs::launch_bwd(g, mix_args(mix), x, fx, Ws, bias, tau, z, nullptr, zmix,
+                                   attn_probs, nullptr, dout, dx, dfx, dWs, dbias, dtau,
+                                   mix->kind == FS_MIX_IDENTITY ? nullptr : dmix_params,
+                                   dzmix_out, static_cast<char*>(ws),
+                                   static_cast<hipStream_t>(hip_stream), &u, clse));
 }
 
 int fs_untied_bwd(const fs_problem* prob, const fs_mix_desc* mix, const void* x, const void* fx,

@@ -15,7 +15,8 @@ struct Geom {
   bool bf16;
   float eps;
   bool ws_per_head;
-  bool untied = false;  // backward of the untied variant (separate deslice projection)
+  bool untied = false;    // backward of the untied variant (separate deslice projection)
+  bool linearno = false;  // LinearNO: untied, slice weights normalised over the points
   int BH() const { return (int)(B * H); }
 };
 
@@ -72,6 +73,7 @@ struct PassArgs {
   const float* ds;    // bwd_b
   const float* cen;   // bwd_b: per (b,h) [V] slot-mean of zmix, [V] of dU, [1] of ds
   const float* lse_in;
+  const float* clse;  // LinearNO: per-slot base-2 normaliser over the points, [BH][G]
   float* lse_out;
   float* part;   // slice: U partials; bwd_a: dzmix partials; bwd_b: parameter partials
   float* part2;  // slice: s partials
@@ -101,6 +103,16 @@ hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, hipStream_t st)
 // Untied variant, backward pass B in two parts: role 1 the slice weights (writes dx, dfx),
 // role 2 the deslice weights (adds to dx); each writes its own parameter partials.
 hipError_t run_pass_bwd_b_untied(const Geom& g, const PassArgs& a, int role, hipStream_t st);
+// LinearNO slice: per-(sample, head, chunk) partials U [G][V] and [G] maxima + [G] sums of
+// 2^(a - max) over the chunk's points, merged by launch_reduce_col into z and clse.
+hipError_t run_pass_slice_col(const Geom& g, const PassArgs& a, hipStream_t st);
+hipError_t launch_reduce_col(const Geom& g, const float* partU, const float* partML, int chunks,
+                             float* z, float* clse, hipStream_t st);
+hipError_t launch_linearno_slice(const Geom& g, const void* x, const void* fx, const float* Ws,
+                                 const float* bias, const float* tau, float* z, float* clse,
+                                 char* ws, hipStream_t st);
+// Fills n floats with v (workspace constants; a kernel, so it may be captured in a graph).
+hipError_t launch_fill(float* p, float v, int64_t n, hipStream_t st);
 
 // Per-thread measurement events recorded around the streaming passes (fs_set_pass_events).
 struct PassEvents {
@@ -114,7 +126,7 @@ struct FwdWs {
   size_t partU, partS, lse, total;  // lse: [BH][N] when the blocked family needs it
 };
 struct BwdWs {
-  size_t partDZ, dzm, dz, dU, ds, cen, partP, partM, scr, cpt, img, partP2, total;
+  size_t partDZ, dzm, dz, dU, ds, cen, partP, partM, scr, cpt, img, partP2, ones, total;
 };
 // Floats of one parameter partial of backward pass B: [D G] dW_s, [G] dbias, then one fp64
 // dtau partial per slot block.
@@ -122,6 +134,8 @@ inline int64_t param_partial_len(const Geom& g, int nblk) {
   return (int64_t)g.D * g.G + g.G + 2LL * nblk;
 }
 FwdWs fwd_ws_layout(const Geom& g);
+// LinearNO slice: partU as in the forward, partS holding 2 G floats per chunk.
+FwdWs linearno_fwd_ws_layout(const Geom& g);
 BwdWs bwd_ws_layout(const Geom& g, int mix_kind);
 size_t mix_param_count(const Geom& g, int mix_kind, bool a_per_head);
 
@@ -184,12 +198,13 @@ struct UntiedArgs {
   float* dbd;
   float* dtaud;
 };
-// Backward of the path; with u given, of the untied variant (g.untied set).
+// Backward of the path; with u given, of the untied variant (g.untied set); with clse also
+// given, of LinearNO (g.linearno set; s is unused).
 hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void* fx,
                       const float* Ws, const float* bias, const float* tau, const float* z,
                       const float* s, const float* zmix, const float* attn, const float* lse,
                       const void* dout, void* dx, void* dfx, float* dWs, float* dbias,
                       float* dtau, float* dmix, float* dzm_out, char* ws, hipStream_t st,
-                      const UntiedArgs* u = nullptr);
+                      const UntiedArgs* u = nullptr, const float* clse = nullptr);
 
 }  // namespace fs

@@ -80,6 +80,25 @@ hipError_t launch_slice(const Geom& g, const void* x, const void* fx, const floa
   return launch_reduce_tokens(g, partU, partS, a.chunks, z, s, st);
 }
 
+hipError_t launch_linearno_slice(const Geom& g, const void* x, const void* fx, const float* Ws,
+                                 const float* bias, const float* tau, float* z, float* clse,
+                                 char* ws, hipStream_t st) {
+  const FwdWs L = linearno_fwd_ws_layout(g);
+  float* partU = reinterpret_cast<float*>(ws + L.partU);
+  float* partML = reinterpret_cast<float*>(ws + L.partS);
+  PassArgs a = base_args(g, PASS_SLICE);
+  a.x = x;
+  a.fx = fx;
+  a.Ws = Ws;
+  a.bias = bias;
+  a.tau = tau;
+  a.part = partU;
+  a.part2 = partML;
+  hipError_t e = timed(PASS_SLICE, st, [&] { return run_pass_slice_col(g, a, st); });
+  if (e != hipSuccess) return e;
+  return launch_reduce_col(g, partU, partML, a.chunks, z, clse, st);
+}
+
 hipError_t launch_deslice(const Geom& g, const void* x, const float* Ws, const float* bias,
                           const float* tau, const float* zmix, const float* lse, float* lse_out,
                           void* out, hipStream_t st) {
@@ -100,7 +119,7 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
                       const float* s, const float* zmix, const float* attn, const float* lse,
                       const void* dout, void* dx, void* dfx, float* dWs, float* dbias,
                       float* dtau, float* dmix, float* dzm_out, char* ws, hipStream_t st,
-                      const UntiedArgs* u) {
+                      const UntiedArgs* u, const float* clse) {
   const BwdWs L = bwd_ws_layout(g, m.kind);
   float* partDZ = reinterpret_cast<float*>(ws + L.partDZ);
   float* dzm = dzm_out != nullptr ? dzm_out : reinterpret_cast<float*>(ws + L.dzm);
@@ -124,8 +143,20 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
   if (e != hipSuccess) return e;
   // mix backward: dz, dU, ds, the slot-mean shifts (+ parameter gradients)
   float* cen = reinterpret_cast<float*>(ws + L.cen);
-  e = launch_mix_bwd(g, m, z, s, zmix, attn, dzm, dz, dU, dsv, cen,
-                     reinterpret_cast<float*>(ws + L.scr), partM, dmix, false, st);
+  if (clse != nullptr) {
+    // LinearNO: the tokens carry no weight-sum normalisation, so dU = dz and
+    // ds = -sum_v dz z (the token gradients with unit weight sums and no eps)
+    float* ones = reinterpret_cast<float*>(ws + L.ones);
+    e = launch_fill(ones, 1.0f, (int64_t)g.BH() * g.G, st);
+    if (e != hipSuccess) return e;
+    Geom g1 = g;
+    g1.eps = 0.f;
+    e = launch_mix_bwd(g1, m, z, ones, zmix, attn, dzm, dz, dU, dsv, cen,
+                       reinterpret_cast<float*>(ws + L.scr), partM, dmix, false, st);
+  } else {
+    e = launch_mix_bwd(g, m, z, s, zmix, attn, dzm, dz, dU, dsv, cen,
+                       reinterpret_cast<float*>(ws + L.scr), partM, dmix, false, st);
+  }
   if (e != hipSuccess) return e;
   // pass B
   PassArgs b = base_args(g, PASS_BWD_B);
@@ -152,8 +183,9 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
     b2.tau = u->taud;
     b2.lse_in = u->lse_d;
     b2.part = reinterpret_cast<float*>(ws + L.partP2);
+    b.clse = clse;
     e = timed(PASS_BWD_B, st, [&] {
-      hipError_t e1 = run_pass_bwd_b_untied(g, b, 1, st);
+      hipError_t e1 = run_pass_bwd_b_untied(g, b, clse != nullptr ? 3 : 1, st);
       return e1 != hipSuccess ? e1 : run_pass_bwd_b_untied(g, b2, 2, st);
     });
     if (e != hipSuccess) return e;

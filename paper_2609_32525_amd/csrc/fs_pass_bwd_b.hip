@@ -14,7 +14,10 @@ namespace {
 // PB: 16-point blocks per tile (1 or 2; bf16 needs 2: its contraction over points has K=32).
 // ROLE: 0 the tied path (one set of weights feeds the slice and the deslice); in the untied
 // variant, 1 is the slice weights' part (dw = F dU^T + ds; writes dfx and dx) and 2 the
-// deslice weights' part (dw = dO zmix^T; adds its dx contribution to the dx already written).
+// deslice weights' part (dw = dO zmix^T; adds its dx contribution to the dx already written);
+// 3 is LinearNO's slice part: weights k = 2^(a - clse_g) normalised over the points of each
+// slot, dw = F dz^T + ds with ds_g = -z_g . dz_g, and da = k dw (the per-slot correction is
+// ds itself, so there is no per-point one; nor are the slot-mean shifts valid).
 // With at most two slot groups, the per-head operands live in LDS as register images shared
 // by the workgroup's wavefronts and are read where they are used, which keeps the register
 // count (and so the number of resident wavefronts) in line with the other passes.
@@ -24,7 +27,8 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
     PassArgs a) {
   static_assert(PB == 2 || !BF, "bf16 contracts over 32 points");
   static_assert(!PM || ROLE == 0, "the untied parts are point-and-parameter kernels");
-  constexpr bool USE_DOUT = ROLE != 1, USE_FX = ROLE != 2;
+  constexpr bool USE_DOUT = ROLE == 0 || ROLE == 2, USE_FX = ROLE != 2;
+  constexpr bool COLN = ROLE == 3;  // weights normalised over the points of each slot
   constexpr int GB = GS / 16, VB = D / 16, DB = D / 16, TP = 16 * PB;
   constexpr bool SPLIT = BF;
   using T = typename Store<BF>::T;
@@ -58,8 +62,9 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   for (int gb = 0; gb < GB; ++gb)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      bT[gb][r] = c.sc * c.bias[c.g0 + 16 * gb + 4 * j + r];
-      dsT[gb][r] = ROLE == 2 ? 0.f : a.ds[(int64_t)c.bh * a.G + c.g0 + 16 * gb + 4 * j + r] - cen[2 * D];
+      const int slot = c.g0 + 16 * gb + 4 * j + r;
+      bT[gb][r] = c.sc * c.bias[slot] - (COLN ? a.clse[(int64_t)c.bh * a.G + slot] : 0.f);
+      dsT[gb][r] = ROLE == 2 ? 0.f : a.ds[(int64_t)c.bh * a.G + slot] - (COLN ? 0.f : cen[2 * D]);
     }
 
   // operands: W_s (logits), zmix and dU (dw, contraction over v), dU (dfx) and W_s / tau (dx)
@@ -75,7 +80,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
     if (!OPL || wp == 0) {
       load_slotop<BF, D, GB, true, SPLIT>(t0, c.W, a.G, c.g0, c.sc, i, j);
       load_slotop<BF, D, GB, false, false>(t1, zm, D, c.g0, 1.0f, i, j, cen);
-      load_slotop<BF, D, GB, false, false>(t2, dU, D, c.g0, 1.0f, i, j, cen + D);
+      load_slotop<BF, D, GB, false, false>(t2, dU, D, c.g0, 1.0f, i, j, COLN ? nullptr : cen + D);
       load_gop<BF, GB, VB, false>(t3, dU, D, c.g0, 1.0f, i, j);
       load_gop<BF, GB, DB, true>(t4, c.W, a.G, c.g0, inv_tau, i, j);
     }
@@ -164,7 +169,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
             tt.dx0[cb][pb] = bld_row4<BF>(rdx, i * rsb + (16 * cb + 4 * j) * (int)sizeof(T), so);
         }
       }
-      const float l = bld32(rl, 4 * i, 4 * (tb + 16 * pb));
+      const float l = COLN ? 0.f : bld32(rl, 4 * i, 4 * (tb + 16 * pb));
       tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
       if constexpr (PM) {
         tt.ct[pb][0] = bld32(rc, 8 * i, 8 * (tb + 16 * pb));
@@ -216,7 +221,13 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
     // per point (column of the tile): c = sum_g w dw, the softmax correction, and
     // tb = sum_g w t, the weighted mean of the shifted base-2 logits t = a2 - lse2
     float cc[PB], tb[PB];
-    if constexpr (PM) {
+    if constexpr (COLN) {
+#pragma unroll
+      for (int pb = 0; pb < PB; ++pb) {
+        cc[pb] = 0.f;
+        tb[pb] = 0.f;
+      }
+    } else if constexpr (PM) {
 #pragma unroll
       for (int pb = 0; pb < PB; ++pb) {
         cc[pb] = cur.ct[pb][0];
@@ -478,6 +489,7 @@ hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, hipStream_t st)
 hipError_t run_pass_bwd_b_untied(const Geom& g, const PassArgs& a, int role, hipStream_t st) {
   if (role == 1) return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<false, 1>::R>(g, a, st);
   if (role == 2) return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<false, 2>::R>(g, a, st);
+  if (role == 3) return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<false, 3>::R>(g, a, st);
   return hipErrorInvalidValue;
 }
 

@@ -10,8 +10,8 @@ from typing import Dict, Optional
 import numpy as np
 
 from . import (BF16, F32, MIX_ATTN, MIX_IDENTITY, MIX_LINEAR_C, MIX_LINEAR_G, MixDesc, Problem,
-               deslice_fwd, deslice_stats_fwd, mix, slice_deslice_bwd, slice_fwd, untied_bwd,
-               workspace_bytes)
+               deslice_fwd, deslice_stats_fwd, linearno_bwd, linearno_slice_fwd, mix,
+               slice_deslice_bwd, slice_fwd, untied_bwd, workspace_bytes)
 
 
 class PathBuffers:
@@ -25,11 +25,13 @@ class PathBuffers:
     the deslice recomputes it); only with with_backward=False.
     untied: dict with the deslice's own Wd, bd, taud (the untied variant): the deslice runs
     fs_deslice_stats_fwd with them (saving lse_d) and the backward is fs_untied_bwd.
+    linearno: with untied, the LinearNO variant: fs_linearno_slice_fwd (saving clse) and
+    fs_linearno_bwd.
     """
 
     def __init__(self, inp: Dict, kind: int, dtype: str = "f32", eps: float = 1e-5,
                  device: str = "cuda:0", with_backward: bool = True, repeat: int = 1,
-                 keep_lse: bool = True, untied: Optional[Dict] = None):
+                 keep_lse: bool = True, untied: Optional[Dict] = None, linearno: bool = False):
         import torch
         self.torch = torch
         self.dev = torch.device(device)
@@ -61,6 +63,9 @@ class PathBuffers:
         self.b = up(inp["b"])
         self.tau = up(inp["tau"])
         self.untied = untied is not None
+        self.linearno = linearno
+        if linearno and not self.untied:
+            raise ValueError("LinearNO needs the deslice's own parameters")
         if self.untied:
             self.Wd, self.bd, self.taud = up(untied["Wd"]), up(untied["bd"]), up(untied["taud"])
         self.params = {}
@@ -80,9 +85,10 @@ class PathBuffers:
         self.attn = torch.empty((B, H, G, G), **f32) if kind == MIX_ATTN else None
         self.lse = torch.empty((B, H, N), **f32) if keep_lse else None
         self.lse_d = torch.empty((B, H, N), **f32) if self.untied else None
+        self.clse = torch.empty((B, H, G), **f32) if linearno else None
         self.out = torch.empty((B, N, H, V), device=self.dev, dtype=sdt)
-        self.ws_f = torch.empty(max(1, workspace_bytes(self.prob, False)), device=self.dev,
-                                dtype=torch.uint8)
+        self.ws_f = torch.empty(max(1, workspace_bytes(self.prob, 3 if linearno else 0)),
+                                device=self.dev, dtype=torch.uint8)
         self.with_backward = with_backward
         if with_backward:
             self.dout = up_points(inp["dout"])
@@ -95,8 +101,9 @@ class PathBuffers:
             nparam = {MIX_IDENTITY: 0, MIX_LINEAR_G: A.numel() if A is not None else 0,
                       MIX_LINEAR_C: V * V, MIX_ATTN: 3 * V * V}[kind]
             self.dmix = torch.empty(max(nparam, 1), **f32) if nparam else None
-            self.ws_b = torch.empty(max(1, workspace_bytes(self.prob, 2 if self.untied else 1)),
-                                    device=self.dev, dtype=torch.uint8)
+            code = 4 if linearno else (2 if self.untied else 1)
+            self.ws_b = torch.empty(max(1, workspace_bytes(self.prob, code)), device=self.dev,
+                                    dtype=torch.uint8)
             if self.untied:
                 self.dWd = torch.empty_like(self.Wd)
                 self.dbd = torch.empty_like(self.bd)
@@ -104,8 +111,18 @@ class PathBuffers:
 
     # ---- launches ------------------------------------------------------------------------
     def forward(self, stream=None) -> None:
+        if self.linearno:
+            linearno_slice_fwd(self.prob, self.x, self.fx, self.Ws, self.b, self.tau, self.z,
+                               self.clse, self.ws_f, stream=stream)
+        else:
+            self._slice(stream)
+        self._mix_deslice(stream)
+
+    def _slice(self, stream) -> None:
         slice_fwd(self.prob, self.x, self.fx, self.Ws, self.b, self.tau, self.z, self.s,
                   self.lse, self.ws_f, stream=stream)
+
+    def _mix_deslice(self, stream) -> None:
         mix(self.prob, self.mixdesc, self.z, self.zmix, self.attn, stream=stream)
         if self.untied:
             deslice_stats_fwd(self.prob, self.x, self.Wd, self.bd, self.taud, self.zmix,
@@ -115,6 +132,13 @@ class PathBuffers:
                     self.out, stream=stream)
 
     def backward(self, stream=None) -> None:
+        if self.linearno:
+            linearno_bwd(self.prob, self.mixdesc, self.x, self.fx, self.Ws, self.b, self.tau,
+                         self.Wd, self.bd, self.taud, self.z, self.clse, self.zmix, self.attn,
+                         self.lse_d, self.dout, self.dx, self.dfx, self.dWs, self.db, self.dtau,
+                         self.dWd, self.dbd, self.dtaud, self.dmix, self.dzmix, self.ws_b,
+                         stream=stream)
+            return
         if self.untied:
             untied_bwd(self.prob, self.mixdesc, self.x, self.fx, self.Ws, self.b, self.tau,
                        self.Wd, self.bd, self.taud, self.z, self.s, self.zmix, self.attn,
@@ -143,6 +167,8 @@ class PathBuffers:
                  out=h(self.out))
         if self.untied:
             r["lse_d"] = h(self.lse_d)
+        if self.linearno:
+            r["clse"] = h(self.clse)
         if self.with_backward:
             r.update(dx=h(self.dx), dfx=h(self.dfx), dWs=h(self.dWs), db=h(self.db),
                      dtau=h(self.dtau), dzmix=h(self.dzmix))

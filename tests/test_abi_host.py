@@ -244,7 +244,7 @@ def test_untied_validation():
     assert st == OK
     _, need_tied = ws_bytes(p, 1)
     assert need > need_tied       # the deslice weights' parameter partials
-    assert ws_bytes(p, 3)[0] == ARG
+    assert ws_bytes(p, -1)[0] == ARG
 
     def call(**over):
         names = ("x", "fx", "Ws", "b", "tau", "Wd", "bd", "taud", "z", "s", "zmix", "attn", "lse",
@@ -263,3 +263,43 @@ def test_untied_validation():
     x = f()
     assert call(x=x, dWd=x + 64) == ALIAS
     assert call(taud=f(4)) == ALIGN
+
+
+def test_linearno_validation():
+    # every call below fails validation before any launch
+    f = Fake()
+    L = fs.lib()
+    p = prob()
+    st, need_f = ws_bytes(p, 3)
+    assert st == OK and need_f > 0
+    st, need_b = ws_bytes(p, 4)
+    assert st == OK and need_b >= ws_bytes(p, 2)[1]
+    assert ws_bytes(p, 5)[0] == ARG
+
+    def fwd(**over):
+        a = {k: f() for k in ("x", "fx", "Ws", "b", "tau", "z", "clse", "ws")}
+        nb = over.pop("ws_bytes", need_f)
+        a.update(over)
+        return L.fs_linearno_slice_fwd(ctypes.byref(p), a["x"], a["fx"], a["Ws"], a["b"],
+                                       a["tau"], a["z"], a["clse"], a["ws"], nb, None)
+
+    assert fwd(ws_bytes=need_f - 1) == WS
+    assert fwd(x=None) == NULL
+    assert fwd(clse=None, ws_bytes=need_f - 1) == WS     # clse is optional
+    z = f()
+    assert fwd(z=z, clse=z + 16) == ALIAS
+    lin = MixDesc.make(fs.MIX_LINEAR_C, Wc=f())
+    names = ("x", "fx", "Ws", "b", "tau", "Wd", "bd", "taud", "z", "clse", "zmix", "attn", "lse_d",
+             "dout", "dx", "dfx", "dWs", "db", "dtau", "dWd", "dbd", "dtaud", "dmix", "dzm", "ws")
+
+    def bwd(**over):
+        a = {k: f() for k in names}
+        nb = over.pop("ws_bytes", need_b)
+        a.update(over)
+        return L.fs_linearno_bwd(ctypes.byref(p), ctypes.byref(lin), *[a[k] for k in names], nb,
+                                 None)
+
+    assert bwd(ws_bytes=need_b - 1) == WS
+    assert bwd(clse=None) == NULL
+    assert bwd(lse_d=None) == NULL
+    assert bwd(dbd=f(4)) == ALIGN
