@@ -86,10 +86,26 @@ def cpu_baseline(w, budget_s=10.0):
     with threadpool_limits(threads):
         used = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
         inp = workloads.make_inputs(w, with_grad=not w.forward_only)
+        if w.variant != "tied":
+            ut = workloads.untied_params(w)
+            prm = {k: inp.get(k) for k in ("A", "Wc", "Wq", "Wk", "Wv", "scale")}
+            args = (inp["x"], inp["fx"], inp["Ws"], inp["b"], inp["tau"], ut["Wd"], ut["bd"],
+                    ut["taud"], w.mix, prm)
+
+        def run_once():
+            if w.variant == "untied":
+                f = oracle.untied_forward(*args, eps=w.eps)
+                oracle.untied_backward(*args, inp["dout"], eps=w.eps, fwd=f)
+            elif w.variant == "linearno":
+                f = oracle.linearno_forward(*args)
+                oracle.linearno_backward(*args, inp["dout"], fwd=f)
+            else:
+                oracle.run_inputs(inp, w.mix, w.eps, backward_too=not w.forward_only)
+
         runs, t_total = 0, 0.0
         while runs == 0 or (t_total < budget_s and runs < 500):
             t0 = time.perf_counter()
-            oracle.run_inputs(inp, w.mix, w.eps, backward_too=not w.forward_only)
+            run_once()
             t_total += time.perf_counter() - t0
             runs += 1
     n = w.block_N or w.N
@@ -140,7 +156,9 @@ def main():
     fwd_only = w.forward_only
     inp = workloads.make_inputs(w, with_grad=not fwd_only)
     pb = PathBuffers(inp, w.mix, w.dtype, w.eps, with_backward=not fwd_only, repeat=w.repeat,
-                     keep_lse=not fwd_only)
+                     keep_lse=not fwd_only,
+                     untied=workloads.untied_params(w) if w.variant != "tied" else None,
+                     linearno=w.variant == "linearno")
     del inp
     dev = pb.dev
     stream = torch.cuda.current_stream(dev)
@@ -248,6 +266,8 @@ def main():
     }
     if fwd_only:
         out["config"]["forward_only"] = True
+    if w.variant != "tied":
+        out["config"]["variant"] = w.variant
     if w.block_N:
         out["config"]["points"] = f"{w.repeat} copies of one seeded {w.block_N}-point block"
     if not args.no_cpu_baseline:

@@ -178,8 +178,14 @@ __device__ __forceinline__ float bld32(__amdgpu_buffer_rsrc_t r, int voff, int s
 __device__ __forceinline__ unsigned short bld16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
   return __builtin_bit_cast(unsigned short, __builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0));
 }
+// A store of more than 64 bits reads its data registers after it issues; an instruction that
+// overwrites them right behind it corrupted the first dword of some lanes under heavy memory
+// traffic (seen with the accumulator-read that followed a 128-bit store). The no-op below
+// takes the data as an input, so the registers stay live up to it, and it supplies the wait
+// states before anything may reuse them.
 __device__ __forceinline__ void bst128(__amdgpu_buffer_rsrc_t r, f4 v, int voff, int soff) {
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b128(r, 0, 0, 0)), v), r, voff, soff, 0);
+  asm volatile("s_nop 1" ::"v"(v));
 }
 __device__ __forceinline__ void bst64(__amdgpu_buffer_rsrc_t r, uint2 v, int voff, int soff) {
   __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(decltype(__builtin_amdgcn_raw_buffer_load_b64(r, 0, 0, 0)), v), r, voff, soff, 0);

@@ -104,3 +104,42 @@ def test_linearno(w):
             if bad[k] <= gate:
                 del bad[k]
     assert not bad, f"{w.name}: above {tol:g}: {bad}"
+
+
+def test_linearno_full_size_volume():
+    """The LinearNO workload at its full size (bf16, N = 2^20, H = 8, G = 64, channel map), in
+    the launch configuration the benchmark times. The oracle recomputes one (sample, head)
+    pair (every output of it at every point, and that head's two temperature gradients);
+    over all heads every output is finite and the slice bias gradient vanishes."""
+    from paper_2609_32525_amd.runner import PathBuffers
+    w = W.WORKLOADS["volume_linearno"]
+    print(f"\n[case] linearno full size {w}", flush=True)
+    inp = W.make_inputs(w)
+    ut = W.untied_params(w)
+    pb = PathBuffers(inp, w.mix, w.dtype, w.eps, untied=ut, linearno=True)
+    pb.step()
+    got = pb.results()
+    for k in ("z", "clse", "zmix", "out", "dx", "dfx", "dWs", "db", "dtau", "dWd", "dbd",
+              "dtaud"):
+        assert np.isfinite(got[k]).all(), k
+    assert np.linalg.norm(got["db"]) <= 2e-2 * np.linalg.norm(got["dWs"])
+    pairs = [(0, 3)]
+    prm = {k: inp.get(k) for k in ("A", "Wc", "Wq", "Wk", "Wv", "scale")}
+    args = (inp["x"], inp["fx"], inp["Ws"], inp["b"], inp["tau"], ut["Wd"], ut["bd"],
+            ut["taud"], w.mix, prm)
+    print(f"  oracle on pairs {pairs}", flush=True)
+    fwd = O.linearno_forward(*args, pairs=pairs)
+    bwd = O.linearno_backward(*args, inp["dout"], fwd=fwd, pairs=pairs)
+    errs = {}
+    for bb, h in pairs:
+        for k in ("z", "zmix", "dzmix"):
+            errs[f"{k}[{h}]"] = rel(got[k][bb, h], (bwd if k in bwd else fwd)[k][bb, h])
+        errs[f"clse[{h}]"] = rel(got["clse"][bb, h] * LN2, fwd["clse"][bb, h])
+        errs[f"lse_d[{h}]"] = rel(got["lse_d"][bb, h] * LN2, fwd["lse_d"][bb, h])
+        for k in ("out", "dx", "dfx"):
+            errs[f"{k}[{h}]"] = rel(got[k][bb, :, h], (bwd if k in bwd else fwd)[k][bb, :, h])
+        for k in ("dtau", "dtaud"):
+            errs[f"{k}[{h}]"] = abs(got[k][h] - bwd[k][h]) / abs(bwd[k][h])
+    print("  errors:", {k: f"{e:.2e}" for k, e in errs.items()}, flush=True)
+    bad = {k: e for k, e in errs.items() if not e <= TOL[w.dtype]}
+    assert not bad, bad

@@ -229,7 +229,7 @@ def test_no_nxg_allocation():
 # properties that hold at any size check the rest.
 FULL = {"tiny": None, "surface": None, "stack": [(0, 0), (3, 7)], "volume": [(0, 5)],
         "stress128": [(0, 2)], "stress256": [(0, 6)], "stress512": [(0, 1)],
-        "stress1024": [(0, 7)]}
+        "stress1024": [(0, 7)], "attn1024": [(0, 4)]}
 PER_PAIR = ("z", "s", "zmix", "lse", "out", "dx", "dfx", "dzmix")
 
 

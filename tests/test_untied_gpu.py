@@ -94,3 +94,10 @@ def test_untied(w):
             if bad[k] <= gate:
                 del bad[k]
     assert not bad, f"{w.name}: above {tol:g}: {bad}"
+
+
+def test_untied_full_size_surface():
+    """The untied workload at its full size (fp32, N = 32768, H = 8, G = 32, attention mix),
+    in the launch configuration the benchmark times, against the oracle on every head."""
+    w = W.WORKLOADS["surface_untied"]
+    test_untied(w)

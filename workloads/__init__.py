@@ -24,6 +24,13 @@ stack      f32     4      131072     8   32  64    fixed G x G matrix (one layer
 infer      bf16    1      2^24       8   32  64    fixed G x G matrix; forward only; the
                                                    points are 16 copies of one seeded
                                                    2^20-point block
+surface_   f32     1      32768      8   32  32    as surface, untied: the deslice has its
+untied                                             own projection, bias and temperature
+volume_    bf16    1      2^20       8   32  64    LinearNO: untied, slice weights
+linearno                                           softmaxed over the points, per-token
+                                                   channel map
+attn1024   bf16    1      2^18       8   32  1024  single-head token self-attention over
+                                                   1024 tokens; as stress1024 otherwise
 =========  ======  =====  =========  ==  ==  ====  =====================================
 
 A workload with ``block_N`` set draws only ``block_N`` points; the full point set is that block
@@ -66,6 +73,7 @@ class Workload:
     a_per_head: bool = False
     block_N: int = 0            # > 0: draw this many points, repeated N / block_N times
     forward_only: bool = False  # inference: no backward, no saved lse
+    variant: str = "tied"       # "tied", "untied" or "linearno"
 
     @property
     def repeat(self) -> int:
@@ -87,6 +95,12 @@ WORKLOADS: Dict[str, Workload] = {
 }
 WORKLOADS["infer"] = Workload("infer", 5, "bf16", 1, 1 << 24, 8, 32, 32, 64, MIX_LINEAR_G,
                              block_N=1 << 20, forward_only=True)
+WORKLOADS["surface_untied"] = Workload("surface_untied", 6, "f32", 1, 32768, 8, 32, 32, 32,
+                                      MIX_ATTN, variant="untied")
+WORKLOADS["volume_linearno"] = Workload("volume_linearno", 7, "bf16", 1, 1 << 20, 8, 32, 32, 64,
+                                       MIX_LINEAR_C, variant="linearno")
+WORKLOADS["attn1024"] = Workload("attn1024", 8, "bf16", 1, 1 << 18, 8, 32, 32, 1024, MIX_ATTN,
+                                 tau_mode="uniform", ws_mode="std3")
 for _g in (128, 256, 512, 1024):
     WORKLOADS[f"stress{_g}"] = Workload(f"stress{_g}", 3, "bf16", 1, 1 << 18, 8, 32, 32, _g,
                                         MIX_LINEAR_G, tau_mode="uniform", ws_mode="std3")
