@@ -258,16 +258,33 @@ __global__ __launch_bounds__(64 * kGemmWaves) void k_tile_gemm(GemmDesc d) {
     const float* As = Ao + (int64_t)sidx * d.a_s;
     const float* Bs = Bo + (int64_t)sidx * d.b_s;
     int k = 0;
-    for (; k + 32 <= d.K; k += 32) {  // eight products' operands loaded before their MFMAs
+    const int kfull = d.K & ~31;
+    if (kfull > 0) {
+      // eight products' operands per block; the next block's loads are issued before the
+      // current block's MFMAs (the last block reloads itself, so every load is in bounds)
       float av[8], bv[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        av[u] = As[(int64_t)(k + 4 * u + j) * d.a_cs];
-        bv[u] = Bs[(int64_t)(k + 4 * u + j) * d.b_rs];
+        av[u] = As[(int64_t)(4 * u + j) * d.a_cs];
+        bv[u] = Bs[(int64_t)(4 * u + j) * d.b_rs];
       }
+      for (; k < kfull; k += 32) {
+        const int kn = k + 32 < kfull ? k + 32 : k;
+        float an[8], bn[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        ch[u & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u], ch[u & 3], 0, 0, 0);
+        for (int u = 0; u < 8; ++u) {
+          an[u] = As[(int64_t)(kn + 4 * u + j) * d.a_cs];
+          bn[u] = Bs[(int64_t)(kn + 4 * u + j) * d.b_rs];
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          ch[u & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[u], bv[u], ch[u & 3], 0, 0, 0);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          av[u] = an[u];
+          bv[u] = bn[u];
+        }
+      }
     }
     for (int u = 0; k < d.K; k += 4, ++u)
       ch[u & 3] = __builtin_amdgcn_mfma_f32_16x16x4f32(As[(int64_t)(k + j) * d.a_cs],
@@ -784,6 +801,14 @@ hipError_t launch_mix(const Geom& g, const MixArgs& m, const float* z, float* zm
   return run_gemm(mix_fwd_desc(g, m, z, zmix), BH, st);
 }
 
+// out[c] = sum over r of part[r][c] (rows summed in a fixed order), one output row.
+static hipError_t launch_sum_rows(const float* part, float* out, int rows, int64_t len,
+                                  hipStream_t st) {
+  dim3 grid((unsigned)((len + kCols - 1) / kCols), 1);
+  hipLaunchKernelGGL(k_reduce_rows, grid, dim3(kRedThreads), 0, st, part, out, rows, len);
+  return hipGetLastError();
+}
+
 // Backward of the large-token-set attention as batched MFMA products (k_tile_gemm) and one
 // row kernel. scr: q, k, v (B H G V each), dS (B H G G), dq, dk, dv (B H G V each).
 //   q, k, v = z W;  dP = dzmix v^T;  dS = P * (dP - rowsum(dP * P));  dv = P^T dzmix;
@@ -832,10 +857,23 @@ static hipError_t attn_rows_bwd(const Geom& g, const MixArgs& m, const float* z,
     e = run_gemm(GemmDesc{dqkv[w], V, 1, GV, 0, kPer, W[w], 1, V, 0, 0, dz, V, GV, G, V, V, 1,
                           1.0f, w > 0 ? 1 : 0},
                  BH, st);
-  for (int w = 0; w < 3 && e == hipSuccess && dmix != nullptr; ++w)  // dW = sum z^T d[w]
-    e = run_gemm(GemmDesc{z, 1, V, 0, GV, 1, dqkv[w], V, 1, 0, GV, dmix + (int64_t)w * V * V, V, 0,
-                          V, V, G, BH, 1.0f, 0},
-                 1, st);
+  // dW = sum over (b, h, g) of z^T d[w]: the B H G products split over S workgroup-sized K
+  // ranges whose partials (in the dS region, free by now) are then summed in order
+  const int64_t KT = (int64_t)BH * G;
+  int64_t Ks = 16;
+  for (int64_t c : {256, 128, 64, 32})
+    if (KT % c == 0 && KT / c >= 64) {
+      Ks = c;
+      break;
+    }
+  const int S = (int)(KT / Ks);
+  if (dmix != nullptr && (int64_t)S * V * V > BH * GG) return hipErrorInvalidValue;
+  for (int w = 0; w < 3 && e == hipSuccess && dmix != nullptr; ++w) {
+    e = run_gemm(GemmDesc{z, 1, V, Ks * V, 0, kPer, dqkv[w], V, 1, Ks * V, 0, dS, V,
+                          (int64_t)V * V, V, V, (int)Ks, 1, 1.0f, 0},
+                 S, st);
+    if (e == hipSuccess) e = launch_sum_rows(dS, dmix + (int64_t)w * V * V, S, (int64_t)V * V, st);
+  }
   if (e == hipSuccess && s != nullptr) {
     hipLaunchKernelGGL(k_token_grads, dim3(BH), dim3(kTokGradThreads), 0, st, z, s, zmix, dz, dU,
                        ds, cen, G, V, g.eps);
