@@ -77,10 +77,10 @@ def short_name(name: str) -> str:
 def _find(path: str, pattern: str) -> str:
     if os.path.isfile(path):
         return path
-    hits = sorted(glob.glob(os.path.join(path, "**", pattern), recursive=True))
+    hits = glob.glob(os.path.join(path, "**", pattern), recursive=True)
     if not hits:
         raise FileNotFoundError(f"no {pattern} under {path}")
-    return hits[0]
+    return max(hits, key=os.path.getmtime)  # the latest run's file
 
 
 def kernel_stats(path: str) -> List[Tuple[str, int, float, float, float, float]]:
