@@ -177,7 +177,9 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
       }
     }
   };
-  pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_BWD_B), Tile>(ntile, load_tile, [&](Tile& cur, int t) {
+  // fp32 with 64-slot waves has the longest tiles to cover: one more tile in flight there
+  constexpr int PF = NS >= FS_NS_NOPF ? 0 : (!BF && GS == 64 && NS == 1 ? FS_PF_BWD_B + 1 : FS_PF_BWD_B);
+  pipeline<PF, Tile>(ntile, load_tile, [&](Tile& cur, int t) {
     const int tp0 = (t * NP + wpu) * TP;
     const RowOp<BF, D>(&xo)[PB] = cur.xo;
     const RowOp<BF, D>(&go)[PB] = cur.go;
