@@ -74,6 +74,12 @@ struct PassArgs {
   const float* cen;   // bwd_b: per (b,h) [V] slot-mean of zmix, [V] of dU, [1] of ds
   const float* lse_in;
   const float* clse;  // LinearNO: per-slot base-2 normaliser over the points, [BH][G]
+  // the deslice's own weight set (untied, LinearNO) for the one-kernel backward pass B
+  const float* Wd;
+  const float* bd;
+  const float* taud;
+  const float* lse_d;
+  float* part_d;
   float* lse_out;
   float* part;   // slice: U partials; bwd_a: dzmix partials; bwd_b: parameter partials
   float* part2;  // slice: s partials
@@ -103,6 +109,10 @@ hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, hipStream_t st)
 // Untied variant, backward pass B in two parts: role 1 the slice weights (writes dx, dfx),
 // role 2 the deslice weights (adds to dx); each writes its own parameter partials.
 hipError_t run_pass_bwd_b_untied(const Geom& g, const PassArgs& a, int role, hipStream_t st);
+// Both weight sets of the untied variant (or LinearNO, coln) in one backward pass B kernel,
+// when one wavefront covers the tile's slots (fused_untied_bwd_b).
+bool fused_untied_bwd_b(const Geom& g);
+hipError_t run_pass_bwd_b2(const Geom& g, const PassArgs& a, bool coln, hipStream_t st);
 // LinearNO slice: per-(sample, head, chunk) partials U [G][V] and [G] maxima + [G] sums of
 // 2^(a - max) over the chunk's points, merged by launch_reduce_col into z and clse.
 hipError_t run_pass_slice_col(const Geom& g, const PassArgs& a, hipStream_t st);

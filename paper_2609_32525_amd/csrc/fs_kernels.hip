@@ -184,10 +184,20 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
     b2.lse_in = u->lse_d;
     b2.part = reinterpret_cast<float*>(ws + L.partP2);
     b.clse = clse;
-    e = timed(PASS_BWD_B, st, [&] {
-      hipError_t e1 = run_pass_bwd_b_untied(g, b, clse != nullptr ? 3 : 1, st);
-      return e1 != hipSuccess ? e1 : run_pass_bwd_b_untied(g, b2, 2, st);
-    });
+    if (fused_untied_bwd_b(g)) {
+      // both weight sets per tile in one kernel: X read once, dx written once
+      b.Wd = u->Wd;
+      b.bd = u->bd;
+      b.taud = u->taud;
+      b.lse_d = u->lse_d;
+      b.part_d = b2.part;
+      e = timed(PASS_BWD_B, st, [&] { return run_pass_bwd_b2(g, b, clse != nullptr, st); });
+    } else {
+      e = timed(PASS_BWD_B, st, [&] {
+        hipError_t e1 = run_pass_bwd_b_untied(g, b, clse != nullptr ? 3 : 1, st);
+        return e1 != hipSuccess ? e1 : run_pass_bwd_b_untied(g, b2, 2, st);
+      });
+    }
     if (e != hipSuccess) return e;
     e = launch_reduce_params(g, partP, dWs, dbias, dtau, b.chunks, b.nblk, &m, partM, dmix, st);
     if (e != hipSuccess) return e;

@@ -34,7 +34,7 @@ from typing import Dict, List, Tuple
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 KERNEL_SOURCES = ("fs_stream.h", "fs_pass_slice.hip", "fs_pass_deslice.hip", "fs_pass_bwd_a.hip",
-                  "fs_pass_bwd_b.hip", "fs_pass_point.hip", "fs_pass_linearno.hip", "fs_kernels.hip", "fs_tokens.hip", "fs_tokmix.hip",
+                  "fs_pass_bwd_b.hip", "fs_pass_point.hip", "fs_pass_linearno.hip", "fs_pass_bwd_b2.hip", "fs_kernels.hip", "fs_tokens.hip", "fs_tokmix.hip",
                   "fs_api.cpp", "fs_internal.h")
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
 
