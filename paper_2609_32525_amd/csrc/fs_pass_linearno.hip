@@ -6,6 +6,8 @@
 // of a workgroup and then the workgroups (chunks) are merged the same way in a fixed order.
 // Kernel design and MFMA lane layouts are described at the top of fs_stream.h.
 
+#include <type_traits>
+
 #include "fs_stream.h"
 
 namespace fs {
@@ -75,40 +77,55 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice_col(PassArgs a) {
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb)
         w[pb][gb] = mm_row_slot<BF, D, GB, SPLIT>(cur.xo[pb], wop, gb, splat4(bS[gb]));
-    bool valid[2][4];
-#pragma unroll
-    for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) valid[pb][r] = tb + 16 * pb + 4 * j + r < npts;
-#pragma unroll
-    for (int gb = 0; gb < GB; ++gb) {
-      float cm = -INFINITY;
+    // padding rows (past the chunk's points) exist only in its last tile
+    auto update = [&](auto ragged) {
+      bool valid[2][4];
 #pragma unroll
       for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) cm = valid[pb][r] ? vmax(cm, w[pb][gb][r]) : cm;
-      cm = vmax(cm, __shfl_xor(cm, 16));
-      cm = vmax(cm, __shfl_xor(cm, 32));
-      const float mnew = vmax(mrun[gb], cm);
-      const float f = rescale(mrun[gb], mnew);
-      mrun[gb] = mnew;
-      float sum = 0.f;
+        for (int r = 0; r < 4; ++r) valid[pb][r] = !ragged.value || tb + 16 * pb + 4 * j + r < npts;
+      bool moved = false;
+      float fs[GB];
 #pragma unroll
-      for (int pb = 0; pb < 2; ++pb)
+      for (int gb = 0; gb < GB; ++gb) {
+        float cm = -INFINITY;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const float e = valid[pb][r] ? __builtin_amdgcn_exp2f(w[pb][gb][r] - mnew) : 0.f;
-          w[pb][gb][r] = e;
-          sum += e;
-        }
-      lrun[gb] = lrun[gb] * f + sum;
+        for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float fr = __shfl(f, 4 * j + r);  // the factor of slot row 4 j + r
+          for (int r = 0; r < 4; ++r) cm = valid[pb][r] ? vmax(cm, w[pb][gb][r]) : cm;
+        cm = vmax(cm, __shfl_xor(cm, 16));
+        cm = vmax(cm, __shfl_xor(cm, 32));
+        const float mnew = vmax(mrun[gb], cm);
+        fs[gb] = rescale(mrun[gb], mnew);
+        moved = moved || mnew != mrun[gb];
+        mrun[gb] = mnew;
+        float sum = 0.f;
 #pragma unroll
-        for (int vb = 0; vb < VB; ++vb) U[gb][vb][r] *= fr;
+        for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float e = valid[pb][r] ? __builtin_amdgcn_exp2f(w[pb][gb][r] - mnew) : 0.f;
+            w[pb][gb][r] = e;
+            sum += e;
+          }
+        lrun[gb] = lrun[gb] * fs[gb] + sum;
       }
-    }
+      // the numerators follow only where some slot's maximum grew (rare once it settles)
+      if (__any(moved)) {
+#pragma unroll
+        for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const float fr = __shfl(fs[gb], 4 * j + r);  // the factor of slot row 4 j + r
+#pragma unroll
+            for (int vb = 0; vb < VB; ++vb) U[gb][vb][r] *= fr;
+          }
+      }
+    };
+    if (tb + 32 <= npts)
+      update(std::false_type{});
+    else
+      update(std::true_type{});
     mm_points<BF, GB, VB>(U, w, cur.f);
   });
 
