@@ -621,7 +621,7 @@ __device__ __forceinline__ void pipeline(int ntile, Load&& load, Body&& body) {
 
 // Prefetch distance (in tiles) of each streaming pass.
 #ifndef FS_PF_SLICE
-#define FS_PF_SLICE 2
+#define FS_PF_SLICE 1
 #endif
 #ifndef FS_PF_DESLICE
 #define FS_PF_DESLICE 2
