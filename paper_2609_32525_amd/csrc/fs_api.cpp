@@ -35,6 +35,9 @@ bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 #ifndef FS_TARGET_DESLICE
 #define FS_TARGET_DESLICE 512
 #endif
+#ifndef FS_PB_F32
+#define FS_PB_F32 1
+#endif
 #ifndef FS_MIN_TILES
 #define FS_MIN_TILES 4
 #endif
@@ -75,7 +78,7 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
     c.NP = c.NS == 2 ? 2 : 1;
   }
   // fp32 backward pass B works on 16-point tiles (its register footprint is the largest)
-  c.PB = (pass == PASS_BWD_B && !g.bf16 && c.NS == 1) ? 1 : 2;
+  c.PB = (pass == PASS_BWD_B && !g.bf16 && c.NS == 1) ? FS_PB_F32 : 2;
   // Workgroups along the points per (sample, head[, slot block]): enough to fill 256 CUs
   // several times, but few enough that the per-workgroup partials stay small next to the
   // streamed data.
