@@ -153,6 +153,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
     float lse2[PB];
     float ct[PM ? PB : 1][2];
     f4 dx0[ROLE == 2 ? DB : 1][PB];  // the dx already written (untied deslice part)
+    KGather<BF, DB, PB> xk;          // X again, points on the k index, for dW_s
   };
   auto load_tile = [&](Tile& tt, int t) {
     const int tb = (t * NP + wpu) * TP;
@@ -176,6 +177,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
         tt.ct[pb][1] = bld32(rc, 8 * i + 4, 8 * (tb + 16 * pb));
       }
     }
+    gather_k<BF, DB, PB>(tt.xk, rx, rsb, tb, i, j);
   };
   // fp32 with 64-slot waves has the longest tiles to cover: one more tile in flight there
   constexpr int PF = NS >= FS_NS_NOPF ? 0 : (!BF && GS == 64 && NS == 1 ? FS_PF_BWD_B + 1 : FS_PF_BWD_B);
@@ -343,6 +345,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
     }
     }
     // dW_s += X^T da over the tile's points: da goes through LDS to put points on the k index.
+    const KGather<BF, DB, PB>& XK = cur.xk;
     if constexpr (!BF) {
       // myda[p * (GS + 1) + gl]
 #pragma unroll
@@ -359,7 +362,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
           const int pl = 16 * pb + 4 * j + r;
           float xv[DB];
 #pragma unroll
-          for (int d = 0; d < DB; ++d) xv[d] = bld32(rx, 4 * j * rsb + (16 * d + i) * 4, (tp0 + 16 * pb + r) * rsb);
+          for (int d = 0; d < DB; ++d) xv[d] = XK.v[pb][r][d];
 #pragma unroll
           for (int gb = 0; gb < GB; ++gb) {
             const float bv = myda[pl * (GS + 1) + 16 * gb + i];
@@ -377,15 +380,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
           for (int r = 0; r < 4; ++r) t16[(16 * gb + 4 * j + r) * 40 + 16 * pb + i] = f_to_bf(dw[gb][pb][r]);
       wave_lds_sync();
-      bf8 xa[DB];
-#pragma unroll
-      for (int d = 0; d < DB; ++d)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const unsigned short h =
-              bld16(rx, 4 * j * rsb + (16 * d + i) * 2, (tp0 + 16 * (e / 4) + (e % 4)) * rsb);
-          xa[d][e] = __builtin_bit_cast(__bf16, h);
-        }
+      const bf8(&xa)[DB] = XK.v;
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb) {
         const uint2 lo = *reinterpret_cast<const uint2*>(t16 + (16 * gb + i) * 40 + 4 * j);

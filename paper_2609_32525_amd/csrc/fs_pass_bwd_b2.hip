@@ -119,6 +119,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   struct Tile {
     RowOp<BF, D> xo[PB], go[PB], fo[PB];
     float ls[PB], ld[PB];
+    KGather<BF, DB, PB> xk;  // bf16: X again, points on the k index, for dW
   };
   auto load_tile = [&](Tile& tt, int t) {
     const int tb = (t * NP + wpu) * TP;
@@ -134,11 +135,16 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
       const float ld = bld32(rld, 4 * i, 4 * (tb + 16 * pb));
       tt.ld[pb] = ok ? ld : kMasked;
     }
+    // fp32 loads this copy where it is used instead: holding it for a tile's lifetime costs
+    // the fp32 kernels an occupancy step
+    if constexpr (BF) gather_k<BF, DB, PB>(tt.xk, rx, rsb, tb, i, j);
   };
 
   // dW[q] += X^T da over the tile's points (da goes through LDS to put points on the k index)
-  auto acc_dW = [&](f4 (&dWq)[DB][GB], const f4 (&da)[GB][PB], int tp0) {
+  auto acc_dW = [&](f4 (&dWq)[DB][GB], const f4 (&da)[GB][PB], const Tile& cur, int tp0) {
     if constexpr (!BF) {
+      KGather<BF, DB, PB> XK;
+      gather_k<BF, DB, PB>(XK, rx, rsb, tp0, i, j);
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb)
 #pragma unroll
@@ -153,7 +159,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
           const int pl = 16 * pb + 4 * j + r;
           float xv[DB];
 #pragma unroll
-          for (int d = 0; d < DB; ++d) xv[d] = bld32(rx, 4 * j * rsb + (16 * d + i) * 4, (tp0 + 16 * pb + r) * rsb);
+          for (int d = 0; d < DB; ++d) xv[d] = XK.v[pb][r][d];
 #pragma unroll
           for (int gb = 0; gb < GB; ++gb) {
             const float bv = myda[pl * (GS + 1) + 16 * gb + i];
@@ -171,15 +177,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
           for (int r = 0; r < 4; ++r) t16[(16 * gb + 4 * j + r) * 40 + 16 * pb + i] = f_to_bf(da[gb][pb][r]);
       wave_lds_sync();
-      bf8 xa[DB];
-#pragma unroll
-      for (int d = 0; d < DB; ++d)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const unsigned short h =
-              bld16(rx, 4 * j * rsb + (16 * d + i) * 2, (tp0 + 16 * (e / 4) + (e % 4)) * rsb);
-          xa[d][e] = __builtin_bit_cast(__bf16, h);
-        }
+      const bf8(&xa)[DB] = cur.xk.v;
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb) {
         const uint2 lo = *reinterpret_cast<const uint2*>(t16 + (16 * gb + i) * 40 + 4 * j);
@@ -286,7 +284,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
           for (int vb = 0; vb < VB; ++vb) gf[vb][pb] = mm_gop_tile<BF, GB, VB, PB>(ug, vb, w, pb, zero4());
       }
-      acc_dW(dW[q], dw, tp0);
+      acc_dW(dW[q], dw, cur, tp0);
     }
 #pragma unroll
     for (int pb = 0; pb < PB; ++pb)

@@ -474,6 +474,42 @@ __device__ __forceinline__ f4 mm_gop_b(const GOp<BF, GB, CB>& o, int cb, const T
   return acc;
 }
 
+// Columns 0..16 DB-1 of a point-major matrix as the MFMA k operand of a contraction over the
+// TP = 16 PB points of a pass-B tile (dW += X^T da): lane (j, i) holds column 16 d + i of
+//   fp32: point 16 pb + 4 j + r for MFMA (pb, r);  bf16 (PB = 2): point 16 (e / 4) + 4 j + (e % 4).
+// Loaded with the tile it belongs to, so the loads are in flight while earlier tiles compute.
+template <bool BF, int DB, int PB>
+struct KGather;
+template <int DB, int PB>
+struct KGather<false, DB, PB> {
+  float v[PB][4][DB];
+};
+template <int DB, int PB>
+struct KGather<true, DB, PB> {
+  bf8 v[DB];
+};
+template <bool BF, int DB, int PB>
+__device__ __forceinline__ void gather_k(KGather<BF, DB, PB>& g, __amdgpu_buffer_rsrc_t r,
+                                         int rsb, int tb, int i, int j) {
+  if constexpr (!BF) {
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int d = 0; d < DB; ++d)
+          g.v[pb][q][d] = bld32(r, 4 * j * rsb + (16 * d + i) * 4, (tb + 16 * pb + q) * rsb);
+  } else {
+    static_assert(PB == 2, "bf16 pass-B tiles hold 32 points");
+#pragma unroll
+    for (int d = 0; d < DB; ++d)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        g.v[d][e] = __builtin_bit_cast(
+            __bf16, bld16(r, 4 * j * rsb + (16 * d + i) * 2, (tb + 16 * (e / 4) + (e % 4)) * rsb));
+  }
+}
+
 // Operand rows of a point-major matrix P (row stride rs) for a contraction over the 32 points
 // of a tile: lane (j, i) holds P(p, 16 cb + i) for the points of its k-set.
 //   fp32: point 16 pb + 4 j + r for MFMA (pb, r);  bf16: point 16 (e / 4) + 4 j + (e % 4).
