@@ -177,6 +177,13 @@ hipError_t launch_mix_bwd(const Geom& g, const MixArgs& m, const float* z, const
                           const float* zmix, const float* attn, const float* dzm, float* dz,
                           float* dU, float* ds, float* cen, float* scr, float* partM,
                           float* dmix, bool reduce_params, hipStream_t st);
+// As launch_tok_bwd, but dzm is first summed from pass A's per-chunk partials
+// [BH][chunks][G V] (fixed chunk order) inside the kernel and written to dzm_out.
+hipError_t launch_tok_bwd_from_parts(const Geom& g, const MixArgs& m, const float* z,
+                                     const float* s, const float* zmix, const float* attn,
+                                     const float* dzm_part, int chunks, float* dzm_out,
+                                     float* dz, float* dU, float* ds, float* cen, float* partM,
+                                     hipStream_t st);
 // Single-workgroup-per-(b, h) token mix kernels with every operand in LDS (fs_tokmix.hip);
 // tok_fused tells whether they apply to this problem and mix kind.
 bool tok_fused(const Geom& g, int mix_kind);

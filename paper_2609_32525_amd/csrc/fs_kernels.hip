@@ -139,24 +139,32 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
   a.part = partDZ;
   hipError_t e = timed(PASS_BWD_A, st, [&] { return run_pass_bwd_a(g, a, st); });
   if (e != hipSuccess) return e;
-  e = launch_reduce_rows(g, partDZ, dzm, a.chunks, (int64_t)g.G * g.V, st);
-  if (e != hipSuccess) return e;
+  // the single-workgroup token kernels sum pass A's partials themselves; the other mixes
+  // get dzmix from the reduction kernel first
+  const bool fused_red = tok_fused(g, m.kind);
+  if (!fused_red) {
+    e = launch_reduce_rows(g, partDZ, dzm, a.chunks, (int64_t)g.G * g.V, st);
+    if (e != hipSuccess) return e;
+  }
   // mix backward: dz, dU, ds, the slot-mean shifts (+ parameter gradients)
   float* cen = reinterpret_cast<float*>(ws + L.cen);
+  Geom gm = g;
+  const float* sm = s;
   if (clse != nullptr) {
     // LinearNO: the tokens carry no weight-sum normalisation, so dU = dz and
     // ds = -sum_v dz z (the token gradients with unit weight sums and no eps)
     float* ones = reinterpret_cast<float*>(ws + L.ones);
     e = launch_fill(ones, 1.0f, (int64_t)g.BH() * g.G, st);
     if (e != hipSuccess) return e;
-    Geom g1 = g;
-    g1.eps = 0.f;
-    e = launch_mix_bwd(g1, m, z, ones, zmix, attn, dzm, dz, dU, dsv, cen,
-                       reinterpret_cast<float*>(ws + L.scr), partM, dmix, false, st);
-  } else {
-    e = launch_mix_bwd(g, m, z, s, zmix, attn, dzm, dz, dU, dsv, cen,
-                       reinterpret_cast<float*>(ws + L.scr), partM, dmix, false, st);
+    gm.eps = 0.f;
+    sm = ones;
   }
+  if (fused_red)
+    e = launch_tok_bwd_from_parts(gm, m, z, sm, zmix, attn, partDZ, a.chunks, dzm, dz, dU, dsv,
+                                  cen, partM, st);
+  else
+    e = launch_mix_bwd(gm, m, z, sm, zmix, attn, dzm, dz, dU, dsv, cen,
+                       reinterpret_cast<float*>(ws + L.scr), partM, dmix, false, st);
   if (e != hipSuccess) return e;
   // pass B
   PassArgs b = base_args(g, PASS_BWD_B);

@@ -250,12 +250,14 @@ __global__ __launch_bounds__(kTokThreads) void k_tok_fwd(const float* z, float* 
 
 // Backward for one (b, h) per workgroup: dz = Mix^T(dzm), the per-(b, h) parameter partial
 // in partM, and (when s is given) dU, ds and the slot-mean shifts cen [2V + 1].
+// With dzm_part given, dzm is not read: it is summed here over the chunks of pass A's
+// partials [BH][chunks][G V] (chunk 0 first) and written to dzm_out.
 template <int KIND>
 __global__ __launch_bounds__(kTokThreads) void k_tok_bwd(
     const float* z, const float* s, const float* zmix, const float* P, const float* dzm,
-    float* dz, float* dU, float* ds, float* cen, float* partM, const float* A, const float* Wc,
-    const float* Wq, const float* Wk, const float* Wv, float scale, int a_per_head, int H,
-    int G, int V, float eps) {
+    const float* dzm_part, int chunks, float* dzm_out, float* dz, float* dU, float* ds,
+    float* cen, float* partM, const float* A, const float* Wc, const float* Wq, const float* Wk,
+    const float* Wv, float scale, int a_per_head, int H, int G, int V, float eps) {
   extern __shared__ float lds[];
   const TokLayout L = tok_layout(KIND, G, V, true);
   const int VP = V + 1, GP = G + 1, GV = G * V, VV = V * V;
@@ -272,7 +274,8 @@ __global__ __launch_bounds__(kTokThreads) void k_tok_bwd(
   {
     // the token gradients (s given) also need zmix and s
     const int tg = s != nullptr ? 1 : 0;
-    const Ld lz{zs, VP, z + tok, G, V}, lg{gz, VP, dzm + tok, G, V};
+    const int rg = dzm_part != nullptr ? 0 : 1;  // dzm comes from the partials instead
+    const Ld lz{zs, VP, z + tok, G, V}, lg{gz, VP, rg ? dzm + tok : nullptr, G * rg, V};
     const Ld lm{zms, VP, tg ? zmix + tok : nullptr, G * tg, V};
     const Ld ls{ss, G, tg ? s + (int64_t)bh * G : nullptr, tg, G};
     if constexpr (KIND == 0) {
@@ -289,6 +292,16 @@ __global__ __launch_bounds__(kTokThreads) void k_tok_bwd(
       const Ld l[8] = {lz, lg, lm, ls, {W, VP, Wq, V, V}, {W + V * VP, VP, Wk, V, V},
                        {W + 2 * V * VP, VP, Wv, V, V}, {lds + L.S, GP, P + (int64_t)bh * G * G, G, G}};
       load_all(l);
+    }
+  }
+  if (dzm_part != nullptr) {
+    const float* pp = dzm_part + (int64_t)bh * chunks * GV;
+    for (int idx = threadIdx.x; idx < GV; idx += blockDim.x) {
+      float acc = 0.f;
+#pragma unroll 16
+      for (int q = 0; q < chunks; ++q) acc += pp[(int64_t)q * GV + idx];
+      gz[(idx / V) * VP + idx % V] = acc;
+      dzm_out[tok + idx] = acc;
     }
   }
   __syncthreads();
@@ -490,9 +503,10 @@ hipError_t launch_tok_fwd(const Geom& g, const MixArgs& m, const float* z, float
 #undef FS_TOK_FWD
 }
 
-hipError_t launch_tok_bwd(const Geom& g, const MixArgs& m, const float* z, const float* s,
-                          const float* zmix, const float* attn, const float* dzm, float* dz,
-                          float* dU, float* ds, float* cen, float* partM, hipStream_t st) {
+static hipError_t tok_bwd(const Geom& g, const MixArgs& m, const float* z, const float* s,
+                          const float* zmix, const float* attn, const float* dzm,
+                          const float* dzm_part, int chunks, float* dzm_out, float* dz, float* dU,
+                          float* ds, float* cen, float* partM, hipStream_t st) {
   const size_t lds = tok_bytes(m.kind, g, true);
   const dim3 grid(g.BH()), block(kTokThreads);
   const int aph = m.a_per_head ? 1 : 0;
@@ -500,9 +514,9 @@ hipError_t launch_tok_bwd(const Geom& g, const MixArgs& m, const float* z, const
   {                                                                                            \
     hipError_t e = allow(k_tok_bwd<K>, lds);                                                   \
     if (e != hipSuccess) return e;                                                             \
-    hipLaunchKernelGGL(k_tok_bwd<K>, grid, block, lds, st, z, s, zmix, attn, dzm, dz, dU, ds,  \
-                       cen, partM, m.A, m.Wc, m.Wq, m.Wk, m.Wv, m.scale, aph, g.H, g.G, g.V,   \
-                       g.eps);                                                                 \
+    hipLaunchKernelGGL(k_tok_bwd<K>, grid, block, lds, st, z, s, zmix, attn, dzm, dzm_part,    \
+                       chunks, dzm_out, dz, dU, ds, cen, partM, m.A, m.Wc, m.Wq, m.Wk, m.Wv,   \
+                       m.scale, aph, g.H, g.G, g.V, g.eps);                                    \
     return hipGetLastError();                                                                  \
   }
   switch (m.kind) {
@@ -513,6 +527,21 @@ hipError_t launch_tok_bwd(const Geom& g, const MixArgs& m, const float* z, const
     default: return hipErrorInvalidValue;
   }
 #undef FS_TOK_BWD
+}
+
+hipError_t launch_tok_bwd(const Geom& g, const MixArgs& m, const float* z, const float* s,
+                          const float* zmix, const float* attn, const float* dzm, float* dz,
+                          float* dU, float* ds, float* cen, float* partM, hipStream_t st) {
+  return tok_bwd(g, m, z, s, zmix, attn, dzm, nullptr, 0, nullptr, dz, dU, ds, cen, partM, st);
+}
+
+hipError_t launch_tok_bwd_from_parts(const Geom& g, const MixArgs& m, const float* z,
+                                     const float* s, const float* zmix, const float* attn,
+                                     const float* dzm_part, int chunks, float* dzm_out,
+                                     float* dz, float* dU, float* ds, float* cen, float* partM,
+                                     hipStream_t st) {
+  return tok_bwd(g, m, z, s, zmix, attn, nullptr, dzm_part, chunks, dzm_out, dz, dU, ds, cen,
+                 partM, st);
 }
 
 }  // namespace fs
