@@ -29,9 +29,6 @@ bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 #ifndef FS_BLOCKED_MIN_G
 #define FS_BLOCKED_MIN_G 128
 #endif
-#ifndef FS_POINT_WAVES
-#define FS_POINT_WAVES 8
-#endif
 #ifndef FS_TARGET_DESLICE
 #define FS_TARGET_DESLICE 512
 #endif

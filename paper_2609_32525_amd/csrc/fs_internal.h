@@ -38,6 +38,19 @@ enum Pass {
 // per-point correction c = sum_g w dw from a point-owned pass that also writes dx and dfx.
 // Below the threshold every pass is one kernel whose wavefronts split the slots of a tile.
 bool blocked(const Geom& g);
+// Wavefronts per workgroup of the point-owned pass, and the range of resident wavefronts per
+// SIMD it is compiled for (the minimum caps its registers). Twelve wavefronts with three per
+// SIMD (a few registers spilled) measured 5-8% faster than eight with two; six and four
+// were slower.
+#ifndef FS_POINT_WAVES
+#define FS_POINT_WAVES 12
+#endif
+#ifndef FS_POINT_WPE
+#define FS_POINT_WPE 3
+#endif
+#ifndef FS_POINT_WPE_MIN
+#define FS_POINT_WPE_MIN 3
+#endif
 
 // Launch shape of one streaming pass over the points.
 //   GS: slots owned by one wavefront; NS = G / GS wavefronts share each point tile

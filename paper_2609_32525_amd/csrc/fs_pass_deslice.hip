@@ -94,8 +94,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
         for (int gb = 0; gb < GB; ++gb)
 #pragma unroll
           for (int r = 0; r < 4; ++r) mx = vmax(mx, w[gb][pb][r]);
-        mx = vmax(mx, __shfl_xor(mx, 16));
-        m[pb] = vmax(mx, __shfl_xor(mx, 32));
+        m[pb] = col4_max(mx);
         float sum = 0.f;
 #pragma unroll
         for (int gb = 0; gb < GB; ++gb)

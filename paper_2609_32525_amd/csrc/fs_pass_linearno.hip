@@ -93,8 +93,7 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice_col(PassArgs a) {
         for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
           for (int r = 0; r < 4; ++r) cm = valid[pb][r] ? vmax(cm, w[pb][gb][r]) : cm;
-        cm = vmax(cm, __shfl_xor(cm, 16));
-        cm = vmax(cm, __shfl_xor(cm, 32));
+        cm = col4_max(cm);
         const float mnew = vmax(mrun[gb], cm);
         fs[gb] = rescale(mrun[gb], mnew);
         moved = moved || mnew != mrun[gb];

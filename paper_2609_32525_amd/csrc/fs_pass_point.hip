@@ -39,9 +39,10 @@ struct PointImages {
   // per half: W (logits), zv, uv (dw), ug (dfx), wg (P, Q); then bias and ds of the block
   static constexpr int kHalf = kW + 2 * kZ + 2 * kU;
   static constexpr int kChunks = 2 * kHalf + 2 * 64 / 4;  // + bS[64], dsS[64] as uint4
-  // stride of one block's image set, padded so that a 512-thread workgroup copies it in
+  // stride of one block's image set, padded so that the point pass's workgroup copies it in
   // whole rounds
-  static constexpr int kStride = (kChunks + 511) / 512 * 512;
+  static constexpr int kRound = 64 * FS_POINT_WAVES;
+  static constexpr int kStride = (kChunks + kRound - 1) / kRound * kRound;
 };
 
 // The first nchunks 16-byte chunks of a per-lane operand (its register image), per lane.
@@ -184,7 +185,7 @@ __device__ __forceinline__ f4 mm_split_b(const GOp<BF, GBH, CB>& o, int cb, cons
 }
 
 template <bool BF, int D, int NW>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(1, 2))) void k_point(
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(FS_POINT_WPE_MIN, FS_POINT_WPE))) void k_point(
     PassArgs a) {
   using IM = PointImages<BF, D>;
   using SOp = typename IM::SOp;
@@ -373,16 +374,16 @@ size_t point_image_bytes(const Geom& g) {
 
 hipError_t run_pass_point(const Geom& g, const PassArgs& a, hipStream_t st) {
   const PassCfg cfg = pick_cfg(g, PASS_POINT);
-  if (cfg.NP != 8 || g.D > 32) return hipErrorInvalidConfiguration;
+  if (cfg.NP != FS_POINT_WAVES || g.D > 32) return hipErrorInvalidConfiguration;
   uint4* img = static_cast<uint4*>(const_cast<void*>(a.img));
   const dim3 igrid((g.G / 64) * g.BH()), iblock(64 * 11);
-  const dim3 grid(cfg.chunks * g.BH()), block(64 * 8);
+  const dim3 grid(cfg.chunks * g.BH()), block(64 * FS_POINT_WAVES);
 #define FS_POINT(BF_, D_)                                                                \
   {                                                                                      \
     hipLaunchKernelGGL((k_point_images<BF_, D_>), igrid, iblock, 0, st, a, img);         \
     hipError_t e = hipGetLastError();                                                    \
     if (e != hipSuccess) return e;                                                       \
-    hipLaunchKernelGGL((k_point<BF_, D_, 8>), grid, block, 0, st, a);                    \
+    hipLaunchKernelGGL((k_point<BF_, D_, FS_POINT_WAVES>), grid, block, 0, st, a);                    \
     return hipGetLastError();                                                            \
   }
   if (g.bf16 && g.D == 16) FS_POINT(true, 16)

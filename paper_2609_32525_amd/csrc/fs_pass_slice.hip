@@ -74,24 +74,42 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
       for (int gb = 0; gb < GB; ++gb)
         w[pb][gb] = mm_row_slot<BF, D, GB, SPLIT>(xo[pb], wop, gb, splat4(bS[gb]));
 
+    // per point (row): max over the slots, then the sum of 2^(a - max); the eight rows of a
+    // lane are reduced across the 16 slot lanes together
     float m[2][4], l[2][4];
+    {
+      float mx[8];
 #pragma unroll
-    for (int pb = 0; pb < 2; ++pb)
+      for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float mx = w[pb][0][r];
+        for (int r = 0; r < 4; ++r) {
+          float v = w[pb][0][r];
 #pragma unroll
-        for (int gb = 1; gb < GB; ++gb) mx = vmax(mx, w[pb][gb][r]);
-        m[pb][r] = row16_max(mx);
-        float sum = 0.f;
-#pragma unroll
-        for (int gb = 0; gb < GB; ++gb) {
-          const float e = __builtin_amdgcn_exp2f(w[pb][gb][r] - m[pb][r]);
-          w[pb][gb][r] = e;
-          sum += e;
+          for (int gb = 1; gb < GB; ++gb) v = vmax(v, w[pb][gb][r]);
+          mx[4 * pb + r] = v;
         }
-        l[pb][r] = row16_sum(sum);
-      }
+      row16_max_n(mx);
+      float sm[8];
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          m[pb][r] = mx[4 * pb + r];
+          float sum = 0.f;
+#pragma unroll
+          for (int gb = 0; gb < GB; ++gb) {
+            const float e = __builtin_amdgcn_exp2f(w[pb][gb][r] - m[pb][r]);
+            w[pb][gb][r] = e;
+            sum += e;
+          }
+          sm[4 * pb + r] = sum;
+        }
+      row16_sum_n(sm);
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) l[pb][r] = sm[4 * pb + r];
+    }
 
     float f[2][4], lse2[2][4];
     if constexpr (NS == 1) {

@@ -66,7 +66,8 @@ __device__ __forceinline__ f4 splat4(float v) { return f4{v, v, v, v}; }
 // Every lane of the row ends with the same bitwise result (each step adds commuted pairs).
 template <int CTRL>
 __device__ __forceinline__ float dpp(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+  // every lane's source lies in its own row for these patterns, so no lane keeps an old value
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
 }
 // IEEE maximum (v_maximum3_f32): unlike fmaxf it needs no canonicalising of its inputs.
 __device__ __forceinline__ float vmax(float a, float b) { return __builtin_elementwise_maximum(a, b); }
@@ -84,11 +85,51 @@ __device__ __forceinline__ float row16_sum(float v) {
   v = v + dpp<0x140>(v);
   return v;
 }
+// The same reductions over several independent values at once, one butterfly step for all of
+// them before the next: consecutive DPP reads of a just-written register need wait states,
+// which the other values' steps fill.
+template <int N>
+__device__ __forceinline__ void row16_max_n(float (&v)[N]) {
+#pragma unroll
+  for (int k = 0; k < N; ++k) v[k] = vmax(v[k], dpp<0xB1>(v[k]));
+#pragma unroll
+  for (int k = 0; k < N; ++k) v[k] = vmax(v[k], dpp<0x4E>(v[k]));
+#pragma unroll
+  for (int k = 0; k < N; ++k) v[k] = vmax(v[k], dpp<0x141>(v[k]));
+#pragma unroll
+  for (int k = 0; k < N; ++k) v[k] = vmax(v[k], dpp<0x140>(v[k]));
+}
+template <int N>
+__device__ __forceinline__ void row16_sum_n(float (&v)[N]) {
+#pragma unroll
+  for (int k = 0; k < N; ++k) v[k] = v[k] + dpp<0xB1>(v[k]);
+#pragma unroll
+  for (int k = 0; k < N; ++k) v[k] = v[k] + dpp<0x4E>(v[k]);
+#pragma unroll
+  for (int k = 0; k < N; ++k) v[k] = v[k] + dpp<0x141>(v[k]);
+#pragma unroll
+  for (int k = 0; k < N; ++k) v[k] = v[k] + dpp<0x140>(v[k]);
+}
 // Sum over the four 16-lane rows (lanes i, i+16, i+32, i+48): identical result in all four.
+// VALU lane swaps instead of LDS permutes: the 32-lane swap pairs row r with row r ^ 2, the
+// 16-lane swap then pairs odd rows with even ones; each pair is added in the same order in
+// both of its rows.
 __device__ __forceinline__ float col4_sum(float v) {
-  v = v + __shfl_xor(v, 16);
-  v = v + __shfl_xor(v, 32);
-  return v;
+  const unsigned u = __float_as_uint(v);
+  const auto h = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const float s = __uint_as_float(h[0]) + __uint_as_float(h[1]);
+  const unsigned us = __float_as_uint(s);
+  const auto q = __builtin_amdgcn_permlane16_swap(us, us, false, false);
+  return __uint_as_float(q[0]) + __uint_as_float(q[1]);
+}
+// Maximum over the four 16-lane rows, by the same two lane swaps.
+__device__ __forceinline__ float col4_max(float v) {
+  const unsigned u = __float_as_uint(v);
+  const auto h = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const float s = vmax(__uint_as_float(h[0]), __uint_as_float(h[1]));
+  const unsigned us = __float_as_uint(s);
+  const auto q = __builtin_amdgcn_permlane16_swap(us, us, false, false);
+  return vmax(__uint_as_float(q[0]), __uint_as_float(q[1]));
 }
 
 // Orders LDS traffic between lanes of one wavefront (no s_barrier needed within a wave).

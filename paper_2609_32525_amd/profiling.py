@@ -4,6 +4,11 @@ Two summaries, both written as short text (markdown) plus, for traffic, a JSON r
 
 * ``stats``: per-kernel call count and average / min / max duration from the
   ``kernel_stats.csv`` that ``rocprofv3 --kernel-trace --stats -f csv`` writes.
+* ``issue``: per-kernel issue picture from one SQ counter run (``--pmc SQ_WAVES SQ_INSTS_VALU
+  SQ_INSTS_MFMA SQ_INSTS_LDS SQ_VALU_MFMA_BUSY_CYCLES SQ_ACTIVE_INST_VALU GRBM_GUI_ACTIVE``):
+  the fraction of SIMD cycles the matrix cores are busy and the fraction in which a VALU
+  instruction (MFMAs included) is issued, over the kernel's cycles. GRBM_GUI_ACTIVE is summed
+  over the 8 XCDs, so the kernel's cycles are its value / 8; the SIMD count is 1024.
 * ``traffic``: HBM bytes per launch of each kernel from two counter runs
   (``--pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE``, ``-f csv``). Each counter is calibrated by
   what it reads for a plain device-to-device copy of known size that the profiled program
@@ -16,6 +21,7 @@ while the hash matches the sources it runs.
 Usage::
 
     python -m paper_2609_32525_amd.profiling stats DIR/kernel_stats.csv --command "..." --out F.md
+    python -m paper_2609_32525_amd.profiling issue DIR --command "..." --out F.md
     python -m paper_2609_32525_amd.profiling traffic FETCH_DIR WRITE_DIR --copy-mib 256 \
         --workload surface --command "..." --out profiles/pmc_<kernel>_<workload>
 """
@@ -110,6 +116,45 @@ def counter_values(path: str, counter: str) -> Dict[str, List[float]]:
     return out
 
 
+ISSUE_COUNTERS = ("SQ_WAVES", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_INSTS_LDS",
+                  "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_ACTIVE_INST_VALU", "GRBM_GUI_ACTIVE")
+SIMDS, XCDS = 1024, 8
+
+
+def issue_summary(path: str) -> Dict[str, Dict[str, float]]:
+    """Per kernel, averaged over its dispatches: cycles, waves, instruction counts, the
+    MFMA-busy and VALU-issue fractions of the SIMD cycles, and the implied clock."""
+    per: Dict[Tuple[str, str], Dict[str, float]] = collections.defaultdict(
+        lambda: collections.defaultdict(float))
+    dur: Dict[Tuple[str, str], float] = {}
+    with open(_find(path, "*counter_collection.csv")) as fh:
+        for r in csv.DictReader(fh):
+            key = (r["Dispatch_Id"], short_name(r["Kernel_Name"]))
+            per[key][r["Counter_Name"]] += float(r["Counter_Value"])
+            dur[key] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    agg: Dict[str, Dict[str, float]] = collections.defaultdict(lambda: collections.defaultdict(float))
+    for (d, k), cs in per.items():
+        if k.startswith(("__amd", "at::")):
+            continue
+        a = agg[k]
+        a["n"] += 1
+        a["ns"] += dur[(d, k)]
+        for c, v in cs.items():
+            a[c] += v
+    out = {}
+    for k, a in agg.items():
+        n = a["n"]
+        cyc = a["GRBM_GUI_ACTIVE"] / n / XCDS
+        simd_cyc = max(cyc * SIMDS, 1.0)
+        out[k] = {"dispatches": n, "us": a["ns"] / n * 1e-3, "cycles": cyc,
+                  "clock_ghz": cyc / max(a["ns"] / n, 1.0),
+                  "waves": a["SQ_WAVES"] / n, "valu_insts": a["SQ_INSTS_VALU"] / n,
+                  "mfma_insts": a["SQ_INSTS_MFMA"] / n, "lds_insts": a["SQ_INSTS_LDS"] / n,
+                  "mfma_busy": a["SQ_VALU_MFMA_BUSY_CYCLES"] / n / simd_cyc,
+                  "valu_issue": 4.0 * a["SQ_ACTIVE_INST_VALU"] / n / simd_cyc}
+    return out
+
+
 def calibrated_traffic(fetch_dir: str, write_dir: str, copy_mib: float):
     """Per-kernel average (fetch, write) bytes per launch, each counter scaled by its reading
     for the copy of ``copy_mib`` MiB (only copy dispatches of at least half that size count)."""
@@ -144,6 +189,11 @@ def _main():
     s.add_argument("--command", required=True, help="the rocprofv3 command that made it")
     s.add_argument("--title", default="Kernel durations")
     s.add_argument("--out", required=True)
+    q = sub.add_parser("issue")
+    q.add_argument("path")
+    q.add_argument("--command", required=True)
+    q.add_argument("--title", default="Issue picture")
+    q.add_argument("--out", required=True)
     t = sub.add_parser("traffic")
     t.add_argument("fetch")
     t.add_argument("write")
@@ -165,6 +215,28 @@ def _main():
             if n.startswith("at::"):
                 continue
             lines.append(f"| `{n}` | {c} | {av:.2f} | {mn:.2f} | {mx:.2f} | {100 * tt / tot:.1f} |")
+        with open(a.out, "w") as fh:
+            fh.write("\n".join(lines) + "\n")
+        print("\n".join(lines))
+        return
+
+    if a.cmd == "issue":
+        res = issue_summary(a.path)
+        lines = [f"# {a.title}", "", "Command:", "", "```", a.command, "```", "",
+                 f"Kernel sources sha256[:16] = `{kernel_source_hash()}`", "",
+                 "MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES over the SIMD cycles (1024 SIMDs x the "
+                 "kernel's cycles, GRBM_GUI_ACTIVE / 8 XCDs). VALU issue: 4 x "
+                 "SQ_ACTIVE_INST_VALU (quad-cycles in which a VALU or MFMA instruction issues) "
+                 "over the same SIMD cycles. The rest of the SIMD time is spent waiting.", "",
+                 "| kernel | us | GHz | waves | VALU insts / wave | MFMA insts / wave | "
+                 "LDS insts / wave | MFMA busy | VALU issue |",
+                 "|---|---:|---:|---:|---:|---:|---:|---:|---:|"]
+        for k, r in sorted(res.items(), key=lambda kv: -kv[1]["us"]):
+            w = max(r["waves"], 1.0)
+            lines.append(f"| `{k}` | {r['us']:.1f} | {r['clock_ghz']:.2f} | {r['waves']:.0f} | "
+                         f"{r['valu_insts'] / w:.0f} | {r['mfma_insts'] / w:.0f} | "
+                         f"{r['lds_insts'] / w:.0f} | {100 * r['mfma_busy']:.1f}% | "
+                         f"{100 * r['valu_issue']:.1f}% |")
         with open(a.out, "w") as fh:
             fh.write("\n".join(lines) + "\n")
         print("\n".join(lines))
