@@ -118,6 +118,26 @@ def cpu_baseline(w, budget_s=10.0):
             "cpu": platform.processor() or platform.machine()}
 
 
+def copy_bandwidth(torch, mib=1024, reps=5):
+    """HBM bytes per second of a plain device-to-device copy (read + write) of ``mib`` MiB,
+    measured before the timed region: the streaming rate this GPU reaches in practice, as
+    context for the roofline fraction (which is taken against the 8 TB/s peak)."""
+    src = torch.empty(mib << 18, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    b.record()
+    torch.cuda.synchronize()
+    sec = a.elapsed_time(b) * 1e-3 / reps
+    del src, dst
+    return 2 * (mib << 20) / sec / 1e9
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -151,6 +171,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+
+    # (skipped in counter runs, whose only large copy must be the calibration one)
+    copy_gbps = copy_bandwidth(torch) if args.copy_calibration_mib == 0 else None
 
     w = workloads.WORKLOADS[args.workload]
     fwd_only = w.forward_only
@@ -232,6 +255,7 @@ def main():
         roof = {"bound": "mfma", "achieved": flp * units / t_dom / 1e12,
                 "peak": MFMA_PEAK[w.dtype] / 1e12, "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["hbm_copy_gbps"] = copy_gbps  # measured device copy, context for the HBM peak
     roof["traffic"] = measured_traffic(args.workload, KERNEL_NAMES[dom])
     roof["kernel"] = KERNEL_NAMES[dom]
     roof["per_launch"] = {"units": units, "algorithmic_bytes": byt * units,

@@ -714,7 +714,10 @@ __device__ __forceinline__ void pipeline(int ntile, Load&& load, Body&& body) {
 #ifndef FS_NS_NOPF
 #define FS_NS_NOPF 8
 #endif
-// Minimum wavefronts per SIMD each pass is compiled for (1: no register cap).
+// Minimum wavefronts per SIMD each pass is compiled for (1: no register cap). Pass A at 2
+// keeps its accumulators in ordinary VGPRs within 256 registers, so two wavefronts share a
+// SIMD instead of one (the bf16 64-slot form needed 220 VGPRs plus 56 accumulation
+// registers otherwise).
 #ifndef FS_WPE_SLICE
 #define FS_WPE_SLICE 1
 #endif
@@ -722,7 +725,7 @@ __device__ __forceinline__ void pipeline(int ntile, Load&& load, Body&& body) {
 #define FS_WPE_DESLICE 1
 #endif
 #ifndef FS_WPE_BWD_A
-#define FS_WPE_BWD_A 1
+#define FS_WPE_BWD_A 2
 #endif
 #ifndef FS_WPE_BWD_B
 #define FS_WPE_BWD_B 1

@@ -5,10 +5,12 @@ Two summaries, both written as short text (markdown) plus, for traffic, a JSON r
 * ``stats``: per-kernel call count and average / min / max duration from the
   ``kernel_stats.csv`` that ``rocprofv3 --kernel-trace --stats -f csv`` writes.
 * ``issue``: per-kernel issue picture from one SQ counter run (``--pmc SQ_WAVES SQ_INSTS_VALU
-  SQ_INSTS_MFMA SQ_INSTS_LDS SQ_VALU_MFMA_BUSY_CYCLES SQ_ACTIVE_INST_VALU GRBM_GUI_ACTIVE``):
-  the fraction of SIMD cycles the matrix cores are busy and the fraction in which a VALU
-  instruction (MFMAs included) is issued, over the kernel's cycles. GRBM_GUI_ACTIVE is summed
-  over the 8 XCDs, so the kernel's cycles are its value / 8; the SIMD count is 1024.
+  SQ_INSTS_MFMA SQ_INSTS_VALU_TRANS_F32 SQ_INSTS_LDS SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE``):
+  the fraction of SIMD cycles in which the matrix cores are busy, and the fraction the vector
+  ALU needs for the kernel's instructions: a wave64 fp32 instruction occupies a SIMD for 2
+  cycles (128 lanes per clock per compute unit, the 157.3 TFLOP/s FMA rate), a
+  transcendental one for 8 (a quarter of that rate). GRBM_GUI_ACTIVE is summed over the 8
+  XCDs, so the kernel's cycles are its value / 8; the SIMD count is 1024.
 * ``traffic``: HBM bytes per launch of each kernel from two counter runs
   (``--pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE``, ``-f csv``). Each counter is calibrated by
   what it reads for a plain device-to-device copy of known size that the profiled program
@@ -116,9 +118,10 @@ def counter_values(path: str, counter: str) -> Dict[str, List[float]]:
     return out
 
 
-ISSUE_COUNTERS = ("SQ_WAVES", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_INSTS_LDS",
-                  "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_ACTIVE_INST_VALU", "GRBM_GUI_ACTIVE")
+ISSUE_COUNTERS = ("SQ_WAVES", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "SQ_INSTS_VALU_TRANS_F32",
+                  "SQ_INSTS_LDS", "SQ_VALU_MFMA_BUSY_CYCLES", "GRBM_GUI_ACTIVE")
 SIMDS, XCDS = 1024, 8
+VALU_CYCLES, TRANS_CYCLES = 2.0, 8.0  # SIMD cycles per wave64 instruction
 
 
 def issue_summary(path: str) -> Dict[str, Dict[str, float]]:
@@ -150,8 +153,12 @@ def issue_summary(path: str) -> Dict[str, Dict[str, float]]:
                   "clock_ghz": cyc / max(a["ns"] / n, 1.0),
                   "waves": a["SQ_WAVES"] / n, "valu_insts": a["SQ_INSTS_VALU"] / n,
                   "mfma_insts": a["SQ_INSTS_MFMA"] / n, "lds_insts": a["SQ_INSTS_LDS"] / n,
+                  "trans_insts": a["SQ_INSTS_VALU_TRANS_F32"] / n,
                   "mfma_busy": a["SQ_VALU_MFMA_BUSY_CYCLES"] / n / simd_cyc,
-                  "valu_issue": 4.0 * a["SQ_ACTIVE_INST_VALU"] / n / simd_cyc}
+                  # SQ_INSTS_VALU counts MFMAs too; they run on the matrix cores
+                  "valu_busy": (VALU_CYCLES * (a["SQ_INSTS_VALU"] - a["SQ_INSTS_MFMA"]
+                                               - a["SQ_INSTS_VALU_TRANS_F32"])
+                                + TRANS_CYCLES * a["SQ_INSTS_VALU_TRANS_F32"]) / n / simd_cyc}
     return out
 
 
@@ -225,18 +232,22 @@ def _main():
         lines = [f"# {a.title}", "", "Command:", "", "```", a.command, "```", "",
                  f"Kernel sources sha256[:16] = `{kernel_source_hash()}`", "",
                  "MFMA busy: SQ_VALU_MFMA_BUSY_CYCLES over the SIMD cycles (1024 SIMDs x the "
-                 "kernel's cycles, GRBM_GUI_ACTIVE / 8 XCDs). VALU issue: 4 x "
-                 "SQ_ACTIVE_INST_VALU (quad-cycles in which a VALU or MFMA instruction issues) "
-                 "over the same SIMD cycles. The rest of the SIMD time is spent waiting.", "",
-                 "| kernel | us | GHz | waves | VALU insts / wave | MFMA insts / wave | "
-                 "LDS insts / wave | MFMA busy | VALU issue |",
-                 "|---|---:|---:|---:|---:|---:|---:|---:|---:|"]
+                 "kernel's cycles, GRBM_GUI_ACTIVE / 8 XCDs). VALU busy: the vector instructions "
+                 "(SQ_INSTS_VALU less the MFMAs) at 2 SIMD cycles each, transcendentals "
+                 "(SQ_INSTS_VALU_TRANS_F32) at 8, over the same SIMD cycles. Idle: the SIMD "
+                 "time neither accounts for (waiting on memory, LDS or barriers, or on dependent "
+                 "results), taking MFMA and VALU work as overlapping perfectly.", "",
+                 "| kernel | us | waves | VALU / wave | exp / wave | MFMA / wave | "
+                 "LDS / wave | MFMA busy | VALU busy | idle |",
+                 "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
         for k, r in sorted(res.items(), key=lambda kv: -kv[1]["us"]):
             w = max(r["waves"], 1.0)
-            lines.append(f"| `{k}` | {r['us']:.1f} | {r['clock_ghz']:.2f} | {r['waves']:.0f} | "
-                         f"{r['valu_insts'] / w:.0f} | {r['mfma_insts'] / w:.0f} | "
+            idle = max(0.0, 1.0 - max(r["mfma_busy"], r["valu_busy"]))
+            lines.append(f"| `{k}` | {r['us']:.1f} | {r['waves']:.0f} | "
+                         f"{(r['valu_insts'] - r['mfma_insts']) / w:.0f} | "
+                         f"{r['trans_insts'] / w:.0f} | {r['mfma_insts'] / w:.0f} | "
                          f"{r['lds_insts'] / w:.0f} | {100 * r['mfma_busy']:.1f}% | "
-                         f"{100 * r['valu_issue']:.1f}% |")
+                         f"{100 * r['valu_busy']:.1f}% | {100 * idle:.0f}% |")
         with open(a.out, "w") as fh:
             fh.write("\n".join(lines) + "\n")
         print("\n".join(lines))
