@@ -23,7 +23,7 @@ namespace {
 // count (and so the number of resident wavefronts) in line with the other passes.
 // =======================================================================================
 template <bool BF, int D, int GS, int NS, int NP, int PB, bool PM, int ROLE>
-__global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_BWD_B))) void k_bwd_b(
+__global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM ? FS_WPE_BWD_PM : BF ? FS_WPE_BWD_B : FS_WPE_BWD_B_F32))) void k_bwd_b(
     PassArgs a) {
   static_assert(PB == 2 || !BF, "bf16 contracts over 32 points");
   static_assert(!PM || ROLE == 0, "the untied parts are point-and-parameter kernels");
