@@ -740,6 +740,11 @@ __device__ __forceinline__ void pipeline(int ntile, Load&& load, Body&& body) {
 #ifndef FS_WPE_BWD_PM
 #define FS_WPE_BWD_PM 2
 #endif
+// The one-kernel untied / LinearNO pass B with at most 32 slots fits two wavefronts per SIMD
+// in 256 VGPRs without spilling (one otherwise: 336 registers in fp32, 412 in bf16).
+#ifndef FS_WPE_BWD_B2_G32
+#define FS_WPE_BWD_B2_G32 2
+#endif
 
 // Workgroup -> (chunk, slot block, b*H+h): a 1-D grid of chunks * nblk * BH workgroups,
 // chunks of one (head, slot block) consecutive. (Ordering the workgroups per XCD so that the heads of one chunk share an L2
