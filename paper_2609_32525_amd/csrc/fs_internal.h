@@ -48,6 +48,10 @@ bool blocked(const Geom& g);
 #ifndef FS_POINT_WPE
 #define FS_POINT_WPE 3
 #endif
+// The statistics pass of the slot-blocked family: point-owned (1) or cooperative (0).
+#ifndef FS_STATS_POINT
+#define FS_STATS_POINT 1
+#endif
 #ifndef FS_POINT_WPE_MIN
 #define FS_POINT_WPE_MIN 3
 #endif
@@ -117,6 +121,8 @@ hipError_t run_pass_bwd_b(const Geom& g, const PassArgs& a, hipStream_t st);
 hipError_t run_pass_stats(const Geom& g, const PassArgs& a, hipStream_t st);
 hipError_t run_pass_slice_blk(const Geom& g, const PassArgs& a, hipStream_t st);
 hipError_t run_pass_point(const Geom& g, const PassArgs& a, hipStream_t st);
+// point-owned statistics pass of the slot-blocked family (lse only; chunks of PASS_POINT)
+hipError_t run_pass_stats_pt(const Geom& g, const PassArgs& a, hipStream_t st);
 size_t point_image_bytes(const Geom& g);  // workspace of the point-owned pass's operand images
 hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, hipStream_t st);
 // Untied variant, backward pass B in two parts: role 1 the slice weights (writes dx, dfx),

@@ -61,7 +61,7 @@ hipError_t launch_slice(const Geom& g, const void* x, const void* fx, const floa
   hipError_t e;
   if (blocked(g)) {
     // statistics pass (lse), then the slot-owned slice reading it
-    PassArgs sa = base_args(g, PASS_STATS);
+    PassArgs sa = base_args(g, FS_STATS_POINT ? PASS_POINT : PASS_STATS);
     sa.x = x;
     sa.Ws = Ws;
     sa.bias = bias;
@@ -69,7 +69,7 @@ hipError_t launch_slice(const Geom& g, const void* x, const void* fx, const floa
     sa.lse_out = lse != nullptr ? lse : reinterpret_cast<float*>(ws + L.lse);
     a.lse_in = sa.lse_out;
     e = timed(PASS_SLICE, st, [&] {
-      hipError_t e1 = run_pass_stats(g, sa, st);
+      hipError_t e1 = FS_STATS_POINT ? run_pass_stats_pt(g, sa, st) : run_pass_stats(g, sa, st);
       return e1 != hipSuccess ? e1 : run_pass_slice_blk(g, a, st);
     });
   } else {

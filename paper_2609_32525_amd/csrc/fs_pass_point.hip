@@ -363,6 +363,85 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(FS_POIN
   }
 }
 
+// Statistics pass of the slot-blocked family, point-owned: every wavefront takes a 32-point
+// tile and sweeps all slots in blocks of 64, keeping per point a running maximum of the base-2
+// logits and the sum of 2^(a - max), rescaled when the maximum grows; it writes
+// lse2 = max + log2(sum). The projection's operand images for all slots (scaled by
+// log2(e)/tau, bf16 hi + lo) and the scaled bias are built once per workgroup into LDS (up to
+// 132 KB at G = 1024), so the sweep needs no exchange between wavefronts and no barrier.
+template <bool BF, int D, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(FS_POINT_WPE_MIN, FS_POINT_WPE))) void k_stats_pt(
+    PassArgs a) {
+  using SOp = SlotOp<BF, D, 4>;
+  using T = typename Store<BF>::T;
+  constexpr int kB = lds_chunks<SOp>();  // one 64-slot block's image
+  constexpr int kMaxBlk = 1024 / 64;
+  __shared__ uint4 simg[kMaxBlk * kB + 1024 / 4];
+  const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
+  const int wave = threadIdx.x >> 6;
+  const int wpu = __builtin_amdgcn_readfirstlane(wave);
+  const HeadCtx c = head_ctx<D>(a, 0, 0);
+  const int NB = a.G / 64;
+  float* bS = reinterpret_cast<float*>(simg + kMaxBlk * kB);
+  for (int blk = wave; blk < NB; blk += NW) {
+    SOp o;
+    load_slotop<BF, D, 4, true, BF>(o, c.W, a.G, 64 * blk, c.sc, i, j);
+    lds_put(o, simg + blk * kB, lane);
+  }
+  for (int g = threadIdx.x; g < a.G; g += 64 * NW) bS[g] = c.sc * c.bias[g];
+  __syncthreads();
+
+  const int64_t rs = (int64_t)a.H * D;
+  const T* xb = (const T*)a.x + c.off;
+  const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
+  const int64_t pend = min(a.N, pbeg + a.chunk_pts);
+  const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
+  const int nstep = (npts + 32 * NW - 1) / (32 * NW);
+  const int rsb = (int)(rs * sizeof(T));
+  const auto rx = rows_rsrc(xb + pbeg * rs, npts, (int)rs, D);
+  const auto rl = rows_rsrc(a.lse_out + (int64_t)c.bh * a.N + pbeg, npts, 1, 1);
+  for (int step = 0; step < nstep; ++step) {
+    const int tp0 = (step * NW + wpu) * 32;
+    RowOp<BF, D> xo[2];
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) load_row_buf<BF, D>(xo[pb], rx, i * rsb, (tp0 + 16 * pb) * rsb, j);
+    // per lane: point 16 pb + i of the tile, slots 16 gb + 4 j + r of each block
+    float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
+    for (int blk = 0; blk < NB; ++blk) {
+      SOp wop;
+      lds_get(wop, simg + blk * kB, lane);
+      f4 t[4][2];
+#pragma unroll
+      for (int gb = 0; gb < 4; ++gb) {
+        const f4 bT = *reinterpret_cast<const f4*>(bS + 64 * blk + 16 * gb + 4 * j);
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) t[gb][pb] = mm_slot_row<BF, D, 4, BF>(wop, gb, xo[pb], bT);
+      }
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb) {
+        float bm = t[0][pb][0];
+#pragma unroll
+        for (int gb = 0; gb < 4; ++gb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) bm = vmax(bm, t[gb][pb][r]);
+        const float mn = vmax(m[pb], col4_max(bm));
+        float sum = 0.f;
+#pragma unroll
+        for (int gb = 0; gb < 4; ++gb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sum += __builtin_amdgcn_exp2f(t[gb][pb][r] - mn);
+        l[pb] = l[pb] * __builtin_amdgcn_exp2f(m[pb] - mn) + sum;
+        m[pb] = mn;
+      }
+    }
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      const float L = col4_sum(l[pb]);
+      if (j == 0) bst32(rl, m[pb] + __log2f(L), 4 * i, 4 * (tp0 + 16 * pb));
+    }
+  }
+}
+
 }  // namespace
 
 size_t point_image_bytes(const Geom& g) {
@@ -370,6 +449,24 @@ size_t point_image_bytes(const Geom& g) {
   const int ch = g.bf16 ? (g.D == 16 ? PointImages<true, 16>::kStride : PointImages<true, 32>::kStride)
                         : (g.D == 16 ? PointImages<false, 16>::kStride : PointImages<false, 32>::kStride);
   return (size_t)g.BH() * (g.G / 64) * ch * 16;
+}
+
+hipError_t run_pass_stats_pt(const Geom& g, const PassArgs& a, hipStream_t st) {
+  const PassCfg cfg = pick_cfg(g, PASS_POINT);
+  if (cfg.NP != FS_POINT_WAVES || g.D > 32 || g.G > 1024 || g.G % 64 != 0)
+    return hipErrorInvalidConfiguration;
+  const dim3 grid(cfg.chunks * g.BH()), block(64 * FS_POINT_WAVES);
+#define FS_STATS(BF_, D_)                                                              \
+  {                                                                                    \
+    hipLaunchKernelGGL((k_stats_pt<BF_, D_, FS_POINT_WAVES>), grid, block, 0, st, a);  \
+    return hipGetLastError();                                                          \
+  }
+  if (g.bf16 && g.D == 16) FS_STATS(true, 16)
+  if (g.bf16 && g.D == 32) FS_STATS(true, 32)
+  if (!g.bf16 && g.D == 16) FS_STATS(false, 16)
+  if (!g.bf16 && g.D == 32) FS_STATS(false, 32)
+#undef FS_STATS
+  return hipErrorInvalidConfiguration;
 }
 
 hipError_t run_pass_point(const Geom& g, const PassArgs& a, hipStream_t st) {
