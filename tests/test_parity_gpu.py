@@ -131,6 +131,25 @@ def test_edge_point_counts(N):
     compare(w, inp, got)
 
 
+@pytest.mark.parametrize("N,dtype,G", [(0, "bf16", 1024), (1, "bf16", 256), (33, "f32", 512),
+                                       (129, "bf16", 128), (1, "f32", 1024)],
+                         ids=["N0_bf16_G1024", "N1_bf16_G256", "N33_f32_G512",
+                              "N129_bf16_G128", "N1_f32_G1024"])
+def test_edge_point_counts_large_g(N, dtype, G):
+    """Empty, single-point and one-tile-plus-one point sets on the G = 128 family and the
+    slot-blocked family (statistics pass, slot-owned and point-owned passes)."""
+    w = small(f"edge_N{N}_{dtype}_G{G}", dtype, 32, G, O.MIX_LINEAR_G, N=N, B=2, H=2)
+    announce(f"edge N={N} {dtype} G={G}")
+    inp = W.make_inputs(w)
+    _, got = run_gpu(w, inp)
+    if N == 0:
+        assert np.all(got["s"] == 0) and np.all(got["z"] == 0)
+        for k in ("dWs", "db", "dtau", "dzmix"):
+            assert np.all(got[k] == 0), k
+        return
+    compare(w, inp, got)
+
+
 @pytest.mark.parametrize("scale,taus,extreme", [(3.0, (0.1, 0.5, 2.0), False),
                                                 (30.0, (0.05, 0.5, 2.0), True)],
                          ids=["logits~100", "logits~2000"])
