@@ -46,6 +46,9 @@ CASES = [
     case("bf16_D16_G128_linc", "bf16", 16, 128, O.MIX_LINEAR_C, tau_mode="uniform",
          ws_mode="std3"),
     case("bf16_D32_G256_linc", "bf16", 32, 256, O.MIX_LINEAR_C, N=700, H=2),
+    # one-tile-plus-one point sets (ragged tails only)
+    case("bf16_D32_G64_linc_N33", "bf16", 32, 64, O.MIX_LINEAR_C, N=33),
+    case("f32_D32_G256_linc_N33", "f32", 32, 256, O.MIX_LINEAR_C, N=33, H=2),
 ]
 
 

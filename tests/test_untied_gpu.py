@@ -48,6 +48,10 @@ CASES = [
     case("bf16_D16_G128_lin", "bf16", 16, 128, O.MIX_LINEAR_G, tau_mode="uniform",
          ws_mode="std3"),
     case("bf16_D32_G256_attn", "bf16", 32, 256, O.MIX_ATTN, N=700, H=2),
+    # single-point and one-tile-plus-one point sets (ragged tails only)
+    case("f32_D32_G32_lin_N1", "f32", 32, 32, O.MIX_LINEAR_G, N=1),
+    case("bf16_D32_G64_linc_N33", "bf16", 32, 64, O.MIX_LINEAR_C, N=33),
+    case("f32_D32_G256_lin_N33", "f32", 32, 256, O.MIX_LINEAR_G, N=33, H=2),
 ]
 
 
