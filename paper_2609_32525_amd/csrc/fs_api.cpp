@@ -41,6 +41,10 @@ bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 #ifndef FS_TARGET_LONG
 #define FS_TARGET_LONG 1024
 #endif
+// Most point tiles per chunk on long streams (0: no limit).
+#ifndef FS_MAX_TILES
+#define FS_MAX_TILES 64
+#endif
 
 }  // namespace
 
@@ -102,6 +106,12 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
     const int64_t more = std::min<int64_t>((FS_TARGET_LONG + units - 1) / units, ntiles / 16);
     chunks = std::max<int64_t>(chunks, more);
   }
+  // very long streams of the passes without partials (so the workspace stays bounded): at
+  // most FS_MAX_TILES tiles per chunk, so that the head workgroups of one chunk, which share
+  // the 128 B lines of the point rows through one L2, stay close together along the rows
+  // (block_pos dispatches them one after another on such grids)
+  if (FS_MAX_TILES > 0 && c.NS < 8 && !blk && !partials)
+    chunks = std::max<int64_t>(chunks, (ntiles + FS_MAX_TILES - 1) / FS_MAX_TILES);
   // the kernels address a chunk's rows with 32-bit byte offsets (raw buffer loads)
   const int64_t row_bytes = (int64_t)g.H * g.D * (g.bf16 ? 2 : 4);
   const int64_t max_tiles = std::max<int64_t>(1, (((int64_t)1 << 31) - 1) / (row_bytes * step) - 1);

@@ -746,15 +746,33 @@ __device__ __forceinline__ void pipeline(int ntile, Load&& load, Body&& body) {
 #define FS_WPE_BWD_B2_G32 2
 #endif
 
-// Workgroup -> (chunk, slot block, b*H+h): a 1-D grid of chunks * nblk * BH workgroups,
-// chunks of one (head, slot block) consecutive. (Ordering the workgroups per XCD so that the heads of one chunk share an L2
-// measured no faster.)
+// Workgroup -> (chunk, slot block, b*H+h) over a 1-D grid of chunks * nblk * BH workgroups,
+// chunks of one (head, slot block) consecutive. With the chunk count a multiple of 8 the
+// H * nblk workgroups that read the same point rows (each its own D-element segment of every
+// (B, N, H, D) row) get numbers equal mod 8, so the dispatcher, which deals workgroups
+// round-robin to the 8 XCDs, places them on one XCD and its L2. On grids larger than
+// FS_GROUP_GRID workgroups, which run in several waves, they are also numbered 8 apart
+// (workgroup L is the (L / 8 mod H nblk)-th unit of (sample, chunk) group
+// (L / 8 / (H nblk)) * 8 + L mod 8), so that they are dispatched together.
+#ifndef FS_GROUP_GRID
+#define FS_GROUP_GRID 4096
+#endif
 struct BlockPos {
   int chunk, blk, bh;
 };
 __device__ __forceinline__ BlockPos block_pos(const PassArgs& a) {
   BlockPos p;
   const int L = blockIdx.x;
+  const int per = a.nblk * a.H;
+  if ((int)gridDim.x > FS_GROUP_GRID && per > 1 && ((gridDim.x / per) & 7) == 0) {
+    const int k = L >> 3;
+    const int rg = (k / per) * 8 + (L & 7);
+    const int u = k % per;
+    p.chunk = rg % a.chunks;
+    p.blk = u % a.nblk;
+    p.bh = (rg / a.chunks) * a.H + u / a.nblk;
+    return p;
+  }
   p.chunk = L % a.chunks;
   const int r = L / a.chunks;
   p.blk = r % a.nblk;
