@@ -3,8 +3,8 @@
 
 One step = fs_slice_fwd, fs_mix, fs_deslice_fwd and fs_slice_deslice_bwd (which includes the
 mix backward) over one batch of seeded synthetic inputs already resident in device memory.
-The default workload is the car-surface-scale layer (fp32, B=1, N=32768 points, H=8 heads,
-dh=32, G=32 slices, single-head token self-attention). Prints ONE JSON line. A forward-only
+The default workload is the large-mesh volume layer (bf16 storage with fp32 accumulation,
+B=1, N=2^20 points, H=8 heads, dh=32, G=64 slices, fixed G x G token matrix). Prints ONE JSON line. A forward-only
 workload (``--workload infer``: bf16, N = 2^24) times fs_slice_fwd, fs_mix and fs_deslice_fwd
 with no saved normaliser instead.
 
@@ -70,52 +70,109 @@ def measured_traffic(workload, kernel):
     return d.get("traffic_bytes_per_launch")
 
 
-def cpu_baseline(w, budget_s=10.0):
-    """The fp64 oracle (unchanged) on the same workload, timed on the host cores. A workload
+# State the forked oracle workers read (set before the pool starts, shared copy-on-write).
+_ORACLE_JOB = {}
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
+def _mem_available():
+    """Bytes of host memory available to this run (MemAvailable, at most 256 GiB)."""
+    try:
+        with open("/proc/meminfo") as fh:
+            for line in fh:
+                if line.startswith("MemAvailable:"):
+                    return min(int(line.split()[1]) * 1024, 256 << 30)
+    except OSError:
+        pass
+    return 16 << 30
+
+
+def _oracle_pair(pair):
+    """One (sample, head) pair of the unchanged oracle, forward (+ backward); returns its
+    wall time. Runs in a forked worker with its BLAS pool capped to its share of the cores."""
+    from threadpoolctl import threadpool_limits
+    import oracle
+    job = _ORACLE_JOB
+    w, inp, args = job["w"], job["inp"], job["args"]
+    pairs = [pair]
+    with threadpool_limits(job["blas"]):
+        t0 = time.perf_counter()
+        if w.variant == "untied":
+            f = oracle.untied_forward(*args, eps=w.eps, pairs=pairs)
+            oracle.untied_backward(*args, inp["dout"], eps=w.eps, fwd=f, pairs=pairs)
+        elif w.variant == "linearno":
+            f = oracle.linearno_forward(*args, pairs=pairs)
+            oracle.linearno_backward(*args, inp["dout"], fwd=f, pairs=pairs)
+        else:
+            oracle.run_inputs(inp, w.mix, w.eps, backward_too=not w.forward_only, pairs=pairs)
+        return time.perf_counter() - t0
+
+
+def cpu_baseline(w, inp, budget_s=12.0, max_cores=16):
+    """The fp64 oracle (unchanged) on the same workload, timed on the host cores: its (sample,
+    head) pairs are independent, so a pool of forked workers runs them side by side, one pair
+    per worker at a time, each worker's BLAS pool taking its share of the cores. The pool
+    covers the cores this process may run on (os.sched_getaffinity), at most ``max_cores``
+    (the host share of one GPU). Whole passes over all pairs repeat until ``budget_s`` of wall
+    time has passed. Runs before the GPU is initialised (the workers are forked). A workload
     built from a repeated block is sampled on one block (its points per second)."""
+    import multiprocessing as mp
     try:
         libc = ctypes.CDLL("libc.so.6")
         libc.mallopt(-4, 0)
         libc.mallopt(-1, 2 ** 31 - 1)
     except OSError:
         pass
-    threads = int(os.environ.get("ORACLE_BLAS_THREADS", "8"))
-    from threadpoolctl import threadpool_info, threadpool_limits
-    import oracle
     import workloads
-    with threadpool_limits(threads):
-        used = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-        inp = workloads.make_inputs(w, with_grad=not w.forward_only)
-        if w.variant != "tied":
-            ut = workloads.untied_params(w)
-            prm = {k: inp.get(k) for k in ("A", "Wc", "Wq", "Wk", "Wv", "scale")}
-            args = (inp["x"], inp["fx"], inp["Ws"], inp["b"], inp["tau"], ut["Wd"], ut["bd"],
-                    ut["taud"], w.mix, prm)
-
-        def run_once():
-            if w.variant == "untied":
-                f = oracle.untied_forward(*args, eps=w.eps)
-                oracle.untied_backward(*args, inp["dout"], eps=w.eps, fwd=f)
-            elif w.variant == "linearno":
-                f = oracle.linearno_forward(*args)
-                oracle.linearno_backward(*args, inp["dout"], fwd=f)
-            else:
-                oracle.run_inputs(inp, w.mix, w.eps, backward_too=not w.forward_only)
-
-        runs, t_total = 0, 0.0
+    visible = len(os.sched_getaffinity(0))
+    cores = max(1, min(visible, max_cores))
+    pairs = [(b, h) for b in range(w.B) for h in range(w.H)]
+    # each worker touches every page of its own full-size fp64 point outputs (a pair's
+    # (N, V) slice is strided across them) and holds a few N x G fp64 temporaries: run no
+    # more workers than half the available host memory holds
+    n = w.block_N or w.N
+    per_worker = 8 * w.B * n * w.H * (w.D + 2 * w.V) + 8 * 12 * n * (w.G + max(w.D, w.V))
+    nproc = max(1, min(cores, len(pairs), int(0.5 * _mem_available() // per_worker)))
+    blas = max(1, cores // nproc)
+    args = None
+    if w.variant != "tied":
+        ut = workloads.untied_params(w)
+        prm = {k: inp.get(k) for k in ("A", "Wc", "Wq", "Wk", "Wv", "scale")}
+        args = (inp["x"], inp["fx"], inp["Ws"], inp["b"], inp["tau"], ut["Wd"], ut["bd"],
+                ut["taud"], w.mix, prm)
+    _ORACLE_JOB.update(w=w, inp=inp, args=args, blas=blas)
+    runs, t_total, t_said = 0, 0.0, 0.0
+    ctx = mp.get_context("fork")
+    with ctx.Pool(nproc) as pool:
         while runs == 0 or (t_total < budget_s and runs < 500):
             t0 = time.perf_counter()
-            run_once()
+            pool.map(_oracle_pair, pairs, chunksize=1)
             t_total += time.perf_counter() - t0
             runs += 1
+            if t_total - t_said > 5.0 or runs == 1:
+                print(f"[bench] oracle: {runs} pass(es), {t_total:.1f} s", file=sys.stderr,
+                      flush=True)
+                t_said = t_total
+    _ORACLE_JOB.clear()
     n = w.block_N or w.N
     pts = w.B * n * runs
     what = "whole workload" if not w.block_N else "one seeded block"
-    return {"value": pts / t_total, "unit": "points/s", "cores": used, "kind": "oracle",
+    return {"value": pts / t_total, "unit": "points/s", "cores": nproc * blas, "kind": "oracle",
             "sample": f"{what} (B={w.B}, N={n}, all {w.H} heads), "
                       f"{'forward' if w.forward_only else 'forward + backward'} in fp64, "
-                      f"{runs} run(s), {t_total:.1f} s",
-            "cpu": platform.processor() or platform.machine()}
+                      f"{runs} pass(es) over the {len(pairs)} (sample, head) pairs in "
+                      f"{t_total:.1f} s; {nproc} worker processes x {blas} BLAS thread(s)",
+            "cores_visible": visible, "cpu": _cpu_model()}
 
 
 def copy_bandwidth(torch, mib=1024, reps=5):
@@ -143,7 +200,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="surface")
+    ap.add_argument("--workload", default="volume")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true",
                     help="replay each step as one captured HIP graph")
@@ -159,8 +216,15 @@ def main():
         sys.exit(2)
 
     import numpy as np
-    import torch
     import workloads
+
+    w = workloads.WORKLOADS[args.workload]
+    fwd_only = w.forward_only
+    inp = workloads.make_inputs(w, with_grad=not fwd_only)
+    # the oracle's CPU baseline runs first, in forked workers, before anything touches the GPU
+    cpu = None if args.no_cpu_baseline else cpu_baseline(w, inp)
+
+    import torch
     import paper_2609_32525_amd as fs
     from paper_2609_32525_amd.runner import PathBuffers
 
@@ -175,9 +239,6 @@ def main():
     # (skipped in counter runs, whose only large copy must be the calibration one)
     copy_gbps = copy_bandwidth(torch) if args.copy_calibration_mib == 0 else None
 
-    w = workloads.WORKLOADS[args.workload]
-    fwd_only = w.forward_only
-    inp = workloads.make_inputs(w, with_grad=not fwd_only)
     pb = PathBuffers(inp, w.mix, w.dtype, w.eps, with_backward=not fwd_only, repeat=w.repeat,
                      keep_lse=not fwd_only,
                      untied=workloads.untied_params(w) if w.variant != "tied" else None,
@@ -294,8 +355,8 @@ def main():
         out["config"]["variant"] = w.variant
     if w.block_N:
         out["config"]["points"] = f"{w.repeat} copies of one seeded {w.block_N}-point block"
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(w)
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
 
 

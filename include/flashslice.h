@@ -103,9 +103,14 @@ typedef struct {
 /* Bytes of device workspace needed by fs_slice_fwd (for_backward = 0), by fs_mix_bwd and
  * fs_slice_deslice_bwd (for_backward = 1), by fs_untied_bwd (for_backward = 2), by
  * fs_linearno_slice_fwd (for_backward = 3) or by fs_linearno_bwd (for_backward = 4), for
- * this problem. The size never grows with N*G: it holds per-workgroup partial sums (bounded
- * number of workgroups) and token-sized buffers. Returns FS_OK and writes *bytes, or a
- * validation error (FS_ERR_ARG for another for_backward).                                  */
+ * this problem. It holds per-workgroup partial sums (a bounded number of workgroups) and
+ * token-sized buffers (G x V per sample and head). The slot-blocked kernels (G > 128 with
+ * D <= 32, tied path) add per-point state: 4 bytes per (point, head) in the forward (the
+ * normaliser) and 8 in the backward (the softmax correction and the weighted mean logit),
+ * plus per-head operand images (G x (2D + 3V) values). No size grows with N * G.
+ * Returns FS_OK and writes *bytes, or a validation error (FS_ERR_ARG for another
+ * for_backward). (A status return with an out-parameter, so that an invalid problem is an
+ * error code rather than a size.)                                                         */
 int fs_workspace_bytes(const fs_problem* prob, int for_backward, size_t* bytes);
 
 /* Slice (paper: Sec. 2; App. F.1 single-tile equation): recompute the slice weights per
@@ -123,10 +128,13 @@ int fs_slice_fwd(const fs_problem* prob, const void* x, const void* fx, const fl
 int fs_mix(const fs_problem* prob, const fs_mix_desc* mix, const float* z, float* zmix,
            float* attn_probs, void* hip_stream);
 
-/* Backward of the token mix: dz = Mix^T(dzmix) and the mix-parameter gradient (summed over
- * samples and heads; per head for a per-head A): dmix_params is dA (G,G)/(H,G,G) for
- * LINEAR_G, dWc (V,V) for LINEAR_C, [dWq; dWk; dWv] (3,V,V) for ATTN; nullable (skipped).
- * Needs the backward workspace.                                                             */
+/* Backward of the token mix (paper: the derivative of Eq. (1) and of the token
+ * self-attention of Sec. 2 with respect to the tokens and the mix parameters):
+ * dz = Mix^T(dzmix) and the mix-parameter gradient (summed over samples and heads; per head
+ * for a per-head A): dmix_params is dA (G,G)/(H,G,G) for LINEAR_G, dWc (V,V) for LINEAR_C,
+ * [dWq; dWk; dWv] (3,V,V) for ATTN; nullable (skipped). ws/ws_bytes: the backward workspace,
+ * fs_workspace_bytes(prob, 1, .) bytes (the attention backward keeps q, k, v and dP there,
+ * and the per-(sample, head) parameter partials are summed from it in a fixed order).     */
 int fs_mix_bwd(const fs_problem* prob, const fs_mix_desc* mix, const float* z,
                const float* attn_probs, const float* dzmix, float* dz, float* dmix_params,
                void* ws, size_t ws_bytes, void* hip_stream);

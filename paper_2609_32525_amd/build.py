@@ -58,6 +58,16 @@ def build(verbose: bool = False, extra=None) -> str:
         for e in errs:
             if e.strip():
                 print(e, file=sys.stderr)
+    # the wide-store wait states the compiler leaves out after raw buffer stores
+    if __package__:
+        from .isa_check import WAIT_STATES, check_library
+    else:  # run as a script from the package directory
+        from isa_check import WAIT_STATES, check_library
+    nstores, bad = check_library(tmp)
+    if bad:
+        lines = "\n".join("  " + " | ".join(b) for b in bad[:20])
+        raise RuntimeError(f"{len(bad)} of {nstores} wide stores have their data registers "
+                           f"overwritten within {WAIT_STATES} wait states:\n{lines}")
     os.replace(tmp, LIB)
     return LIB
 

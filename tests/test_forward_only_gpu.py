@@ -2,8 +2,9 @@
 
 The forward-only path saves no normaliser: fs_slice_fwd runs with lse = NULL and the deslice
 recomputes every point's softmax statistics from its logits (fs_deslice_fwd with lse = NULL,
-or fs_deslice_stats_fwd, which also writes lse). Errors are normwise relative, 1e-5 for fp32
-storage and 2e-2 for bf16 storage, as in the forward + backward parity tests.
+or fs_deslice_stats_fwd, which also writes lse). Outputs are compared normwise and element by
+element (tests/paritycheck.py), 1e-5 for fp32 storage and 2e-2 for bf16 storage, as in the
+forward + backward parity tests.
 """
 import sys
 
@@ -12,21 +13,11 @@ import pytest
 
 import oracle as O
 import workloads as W
+from paritycheck import TOL, Checker, announce, measures
 
 pytestmark = pytest.mark.gpu
 
-TOL = {"f32": 1e-5, "bf16": 2e-2}
 LN2 = float(np.log(2.0))
-
-
-def rel(a, b):
-    nb = np.linalg.norm(b)
-    return float(np.linalg.norm(a - b) / nb) if nb > 0 else float(np.linalg.norm(a))
-
-
-def announce(msg):
-    print(f"\n[case] {msg}", flush=True)
-    sys.stdout.flush()
 
 
 def case(name, dtype, D, G, mix, B=2, N=1000, H=3, **kw):
@@ -68,8 +59,9 @@ def test_forward_only(w):
     pb.forward()
     got = pb.results()
     ref, _ = O.run_inputs(inp, w.mix, w.eps, backward_too=False)
-    tol = TOL[w.dtype]
-    errs = {k: rel(got[k], ref[k]) for k in ("z", "s", "zmix", "out")}
+    c = Checker(f"forward/{w.name}", w.dtype)
+    for k in ("z", "s", "zmix", "out"):
+        c.add(k, got[k], ref[k], keep=False)
     # the same deslice writing its statistics: lse in the base-2 unit of the library
     lse = torch.full((w.B, w.H, w.N), float("nan"), device=pb.dev)
     out2 = torch.empty_like(pb.out)
@@ -77,11 +69,9 @@ def test_forward_only(w):
     torch.cuda.synchronize()
     lse_h = lse.double().cpu().numpy() * LN2
     out2_h = out2.float().cpu().numpy().astype(np.float64)
-    errs["lse"] = rel(lse_h, ref["lse"])
-    errs["out(stats)"] = rel(out2_h, ref["out"])
-    print("  errors:", {k: f"{e:.2e}" for k, e in errs.items()}, flush=True)
-    bad = {k: e for k, e in errs.items() if not e <= tol}
-    assert not bad, f"{w.name}: above {tol:g}: {bad}"
+    c.add("lse", lse_h, ref["lse"], keep=False)
+    c.add("out(stats)", out2_h, ref["out"], keep=False)
+    c.finish()
     # writing lse changes nothing else: both calls run the same arithmetic
     assert np.array_equal(out2_h, got["out"])
     # the saved-normaliser deslice, fed the recomputed lse, agrees with the recomputing one
@@ -89,7 +79,8 @@ def test_forward_only(w):
     fs.deslice_fwd(pb.prob, pb.x, pb.Ws, pb.b, pb.tau, pb.zmix, lse, out3)
     torch.cuda.synchronize()
     out3_h = out3.float().cpu().numpy().astype(np.float64)
-    assert rel(out3_h, got["out"]) <= tol
+    n3, e3 = measures(out3_h, got["out"], 1.0 if w.dtype == "f32" else 2.0)
+    assert n3 <= TOL[w.dtype] and e3 <= TOL[w.dtype], (n3, e3)
 
 
 def test_forward_only_empty_point_set():
@@ -152,13 +143,10 @@ def test_forward_only_full_size_infer():
     prm = {k: inp.get(k) for k in ("A", "Wc", "Wq", "Wk", "Wv", "scale")}
     ref = O.forward_repeated(inp["x"], inp["fx"], inp["Ws"], inp["b"], inp["tau"], w.mix, prm,
                              w.eps, w.repeat, pts, pairs=pairs)
-    errs = {}
+    c = Checker("forward/infer", w.dtype)
     for bb, h in pairs:
         for k, g in (("z", z), ("s", s), ("zmix", zmix)):
-            errs[f"{k}[{h}]"] = rel(g[bb, h], ref[k][bb, h])
-        errs[f"out[{h}]"] = rel(out_s[bb, :, h], ref["out"][bb, :, h])
-        errs[f"lse[{h}]"] = rel(lse_s[bb, h], ref["lse"][bb, h])
-    print("  errors:", {k: f"{e:.2e}" for k, e in errs.items()}, flush=True)
-    tol = TOL[w.dtype]
-    bad = {k: e for k, e in errs.items() if not e <= tol}
-    assert not bad, f"infer: above {tol:g}: {bad}"
+            c.add(f"{k}[{h}]", g[bb, h], ref[k][bb, h], keep=False)
+        c.add(f"out[{h}]", out_s[bb, :, h], ref["out"][bb, :, h], keep=False)
+        c.add(f"lse[{h}]", lse_s[bb, h], ref["lse"][bb, h], keep=False)
+    c.finish()

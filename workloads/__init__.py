@@ -109,9 +109,13 @@ for _g in (128, 256, 512, 1024):
 def round_to_bf16(a: np.ndarray) -> np.ndarray:
     """Nearest bf16 value of each fp32 entry (ties to even), returned as fp32."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    bits = a.view(np.uint32).astype(np.uint64)
-    rounded = ((bits + 0x7FFF + ((bits >> 16) & 1)) >> 16) << 16
-    out = rounded.astype(np.uint32).view(np.float32)
+    bits = a.view(np.uint32)
+    # bits + 0x7FFF + lsb stays below 2^32 for every non-NaN value (largest: -inf, 0xFF800000)
+    rounded = (bits >> 16) & np.uint32(1)
+    rounded += bits
+    rounded += np.uint32(0x7FFF)
+    rounded &= np.uint32(0xFFFF0000)
+    out = rounded.view(np.float32)
     nan = np.isnan(a)
     if nan.any():
         out = out.copy()
