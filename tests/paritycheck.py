@@ -23,7 +23,6 @@ held to 1e-5.
 from __future__ import annotations
 
 import sys
-from concurrent.futures import ThreadPoolExecutor
 from typing import Callable, Dict, Iterable, Optional, Tuple
 
 import numpy as np
@@ -158,13 +157,14 @@ def _pair_inputs(inp: Dict, b: int, h: int) -> Dict:
     return out
 
 
-def oracle_parallel(O, inp: Dict, kind: int, eps: float, pairs: Optional[Iterable] = None,
-                    workers: int = 8, backward: bool = True):
-    """The unchanged fp64 oracle (O.run_inputs) on each listed (sample, head) pair, pairs run
-    side by side in threads (numpy releases the interpreter lock in its array loops), merged
-    into full-size results: per-pair tensors at their place, parameter gradients summed over
-    the pairs in pair order. Returns (fwd, bwd) like O.run_inputs; entries of pairs not
-    listed stay zero."""
+def oracle_pairs(O, inp: Dict, kind: int, eps: float, pairs: Optional[Iterable] = None,
+                 backward: bool = True):
+    """The unchanged fp64 oracle (O.run_inputs) on each listed (sample, head) pair in turn, as a
+    problem of its own with B = H = 1, merged into full-size results: per-pair tensors at
+    their place, parameter gradients summed over the pairs in pair order (the order the
+    oracle sums them in). Returns (fwd, bwd) like O.run_inputs; entries of pairs not listed
+    stay zero. The pairs run one after another: concurrent BLAS calls from several threads of
+    one process gave wrong products at the full sizes."""
     x = inp["x"]
     B, N, H, D = x.shape
     V = inp["fx"].shape[3]
@@ -184,33 +184,33 @@ def oracle_parallel(O, inp: Dict, kind: int, eps: float, pairs: Optional[Iterabl
         bwd = dict(dx=np.zeros((B, N, H, D)), dfx=np.zeros((B, N, H, V)),
                    dWs=np.zeros(Ws.shape), db=np.zeros(bias.shape), dtau=np.zeros(H),
                    dzmix=np.zeros((B, H, G, V)), dz=np.zeros((B, H, G, V)))
-    with ThreadPoolExecutor(max_workers=max(1, min(workers, len(pairs)))) as ex:
-        for (b, h), (f, g) in zip(pairs, ex.map(one, pairs)):
-            for k in ("z", "s", "zmix", "lse"):
-                fwd[k][b, h] = f[k][0, 0]
-            if f.get("P") is not None:
-                fwd["P"][b, h] = f["P"][0, 0]
-            fwd["out"][b, :, h, :] = f["out"][0, :, 0, :]
-            if g is None:
+    for b, h in pairs:
+        f, g = one((b, h))
+        for k in ("z", "s", "zmix", "lse"):
+            fwd[k][b, h] = f[k][0, 0]
+        if f.get("P") is not None:
+            fwd["P"][b, h] = f["P"][0, 0]
+        fwd["out"][b, :, h, :] = f["out"][0, :, 0, :]
+        if g is None:
+            continue
+        bwd["dx"][b, :, h, :] = g["dx"][0, :, 0, :]
+        bwd["dfx"][b, :, h, :] = g["dfx"][0, :, 0, :]
+        bwd["dzmix"][b, h], bwd["dz"][b, h] = g["dzmix"][0, 0], g["dz"][0, 0]
+        bwd["dtau"][h] += g["dtau"][0]
+        if Ws.ndim == 3:            # per-head projection: the pair's head only
+            bwd["dWs"][h] += g["dWs"][0]
+        else:
+            bwd["dWs"] += g["dWs"]
+        if bias.ndim == 2:
+            bwd["db"][h] += g["db"][0]
+        else:
+            bwd["db"] += g["db"]
+        for k in ("dA", "dWc", "dWq", "dWk", "dWv"):
+            if k not in g:
                 continue
-            bwd["dx"][b, :, h, :] = g["dx"][0, :, 0, :]
-            bwd["dfx"][b, :, h, :] = g["dfx"][0, :, 0, :]
-            bwd["dzmix"][b, h], bwd["dz"][b, h] = g["dzmix"][0, 0], g["dz"][0, 0]
-            bwd["dtau"][h] += g["dtau"][0]
-            if Ws.ndim == 3:            # per-head projection: the pair's head only
-                bwd["dWs"][h] += g["dWs"][0]
+            if k == "dA" and np.asarray(inp["A"]).ndim == 3:
+                bwd.setdefault(k, np.zeros(np.asarray(inp["A"]).shape))[h] += g[k][0]
             else:
-                bwd["dWs"] += g["dWs"]
-            if bias.ndim == 2:
-                bwd["db"][h] += g["db"][0]
-            else:
-                bwd["db"] += g["db"]
-            for k in ("dA", "dWc", "dWq", "dWk", "dWv"):
-                if k not in g:
-                    continue
-                if k == "dA" and np.asarray(inp["A"]).ndim == 3:
-                    bwd.setdefault(k, np.zeros(np.asarray(inp["A"]).shape))[h] += g[k][0]
-                else:
-                    bwd.setdefault(k, np.zeros_like(g[k]))
-                    bwd[k] += g[k]
+                bwd.setdefault(k, np.zeros_like(g[k]))
+                bwd[k] += g[k]
     return fwd, bwd

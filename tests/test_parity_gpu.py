@@ -15,7 +15,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from paritycheck import TOL, Checker, announce, eager_gate, measures, oracle_parallel
+from paritycheck import TOL, Checker, announce, eager_gate, measures, oracle_pairs
 
 pytestmark = pytest.mark.gpu
 
@@ -263,7 +263,7 @@ def test_parity_full_size(name):
     for k in ("out", "dx", "dfx", "dWs", "db", "dtau"):
         assert np.isfinite(got[k]).all(), k
     print(f"  oracle on {'all pairs' if pairs is None else pairs}", flush=True)
-    fwd, bwd = oracle_parallel(O, inp, w.mix, w.eps, pairs=pairs, workers=8)
+    fwd, bwd = oracle_pairs(O, inp, w.mix, w.eps, pairs=pairs)
     if pairs is None:
         compare(w, inp, got, ref=(fwd, bwd))
         return

@@ -6,7 +6,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from paritycheck import Checker, TOL, measures, oracle_parallel
+from paritycheck import Checker, TOL, measures, oracle_pairs
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -45,13 +45,13 @@ def test_checker_reports_non_finite():
     assert measures(got, ref, 1.0) == (float("inf"), float("inf"))
 
 
-def test_oracle_parallel_matches_plain_call():
+def test_oracle_pairs_matches_plain_call():
     for w in (W.Workload("pp_lin", 901, "f32", 2, 300, 3, 16, 16, 32, O.MIX_LINEAR_G,
                          ws_per_head=True, a_per_head=True),
               W.Workload("pp_attn", 902, "bf16", 2, 257, 2, 32, 32, 64, O.MIX_ATTN)):
         inp = W.make_inputs(w)
         f0, b0 = O.run_inputs(inp, w.mix, w.eps)
-        f1, b1 = oracle_parallel(O, inp, w.mix, w.eps, workers=4)
+        f1, b1 = oracle_pairs(O, inp, w.mix, w.eps)
         for k, v in f0.items():
             if v is not None:
                 assert np.array_equal(v, f1[k]), (w.name, k)
