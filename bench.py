@@ -175,6 +175,114 @@ def cpu_baseline(w, inp, budget_s=12.0, max_cores=16):
             "cores_visible": visible, "cpu": _cpu_model()}
 
 
+def stack_flops_per_point(spec):
+    """fp32 flops of one training step per point: per layer three C x C projections and the
+    C -> 4C -> C MLP (2 * 11 C^2 forward, twice that backward), plus the path's contractions
+    12 G (D + V) per head."""
+    C, H, G, L = spec["C"], spec["H"], spec["G"], spec["L"]
+    D = C // H
+    return L * (66 * C * C + H * 12 * G * 2 * D)
+
+
+def stack_cpu_baseline(name, spec, budget_s=12.0, max_cores=16):
+    """The CPU reference of the stack (float64 torch layers around the oracle's path, unchanged)
+    timed on a sample of the workload's points: one sample of 4096 points, training steps
+    repeated until ``budget_s``; points per second. Runs before the GPU is initialised."""
+    import torch
+    import workloads
+    from oracle.stack import reference_step
+    cores = max(1, min(len(os.sched_getaffinity(0)), max_cores))
+    torch.set_num_threads(cores)
+    n = 4096
+    h, R = workloads.make_stack_inputs(name, B=1, N=n)
+    torch.manual_seed(workloads.SEED)
+    from paper_2609_32525_amd.layer import SliceStack
+    state = SliceStack(spec["L"], spec["C"], spec["H"], spec["G"]).state_dict()
+    runs, t_total = 0, 0.0
+    while runs == 0 or t_total < budget_s:
+        t0 = time.perf_counter()
+        reference_step(state, spec["L"], spec["C"], spec["H"], spec["G"], h, R)
+        t_total += time.perf_counter() - t0
+        runs += 1
+    return {"value": n * runs / t_total, "unit": "points/s", "cores": cores, "kind": "oracle",
+            "sample": f"one sample of {n} points (B=1), {runs} training step(s) of the float64 "
+                      f"reference stack (oracle path) in {t_total:.1f} s; {cores} threads",
+            "cores_visible": len(os.sched_getaffinity(0)), "cpu": _cpu_model()}
+
+
+def bench_stack(args):
+    """The full slicing stack: one training step (forward, loss sum(out * R), backward, plain
+    SGD update) over a batch resident in device memory."""
+    import numpy as np
+    import workloads
+    spec = workloads.STACKS[args.workload]
+    cpu = None if args.no_cpu_baseline else stack_cpu_baseline(args.workload, spec)
+    h_np, R_np = workloads.make_stack_inputs(args.workload)
+    import torch
+    from paper_2609_32525_amd.layer import SliceStack, training_step
+    dev = torch.device("cuda:0")
+    torch.manual_seed(workloads.SEED)
+    model = SliceStack(spec["L"], spec["C"], spec["H"], spec["G"]).to(dev)
+    h = torch.from_numpy(h_np).to(dev)
+    R = torch.from_numpy(R_np).to(dev)
+    del h_np, R_np
+    lr = 1e-6
+    for _ in range(args.warmup):
+        training_step(model, h, R, lr)
+    torch.cuda.synchronize(dev)
+    stream = torch.cuda.current_stream(dev)
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize(dev)
+    wall0 = time.perf_counter()
+    t0.record(stream)
+    for _ in range(args.steps):
+        training_step(model, h, R, lr)
+    t1.record(stream)
+    torch.cuda.synchronize(dev)
+    wall = time.perf_counter() - wall0
+    ms_step = t0.elapsed_time(t1) / args.steps
+    # the path's share: events around every path call (forward and backward) of a few more
+    # steps, against those steps' own time
+    nshare = max(1, min(args.steps, 5))
+    model.space.events = []
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(nshare):
+        training_step(model, h, R, lr)
+    b.record(stream)
+    torch.cuda.synchronize(dev)
+    path_ms = sum(x.elapsed_time(y) for x, y in model.space.events) / nshare
+    share_ms = a.elapsed_time(b) / nshare
+    model.space.events = None
+    points = spec["B"] * spec["N"]
+    flops = stack_flops_per_point(spec) * points
+    t_step = ms_step * 1e-3
+    out = {
+        "metric": "points/sec of one training step of the 8-layer slicing stack "
+                  "(forward + backward + SGD update)",
+        "value": points / t_step, "unit": "points/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": args.workload, "L": spec["L"], "B": spec["B"], "N": spec["N"],
+                   "C": spec["C"], "H": spec["H"], "dh": spec["C"] // spec["H"], "G": spec["G"],
+                   "mix": MIX_NAMES[1], "storage": "f32"},
+        "roofline": {"bound": "mfma", "achieved": flops / t_step / 1e12,
+                     "peak": MFMA_PEAK["f32"] / 1e12, "unit": "TFLOP/s",
+                     "frac": flops / t_step / MFMA_PEAK["f32"], "traffic": None,
+                     "kernel": "whole step (fp32 GEMMs of the projections and MLPs dominate)",
+                     "per_launch": {"units": points, "algorithmic_flops": flops,
+                                    "avg_duration_us": ms_step * 1e3}},
+        "path": {"ms_per_step": path_ms, "share": path_ms / share_ms,
+                 "calls_per_step": 2 * spec["L"]},
+        "wall_s_timed": wall,
+    }
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
+    print(json.dumps(out), flush=True)
+
+
 def copy_bandwidth(torch, mib=1024, reps=5):
     """HBM bytes per second of a plain device-to-device copy (read + write) of ``mib`` MiB,
     measured before the timed region: the streaming rate this GPU reaches in practice, as
@@ -218,6 +326,9 @@ def main():
     import numpy as np
     import workloads
 
+    if args.workload in workloads.STACKS:
+        bench_stack(args)
+        return
     w = workloads.WORKLOADS[args.workload]
     fwd_only = w.forward_only
     inp = workloads.make_inputs(w, with_grad=not fwd_only)

@@ -303,3 +303,34 @@ def test_linearno_validation():
     assert bwd(clse=None) == NULL
     assert bwd(lse_d=None) == NULL
     assert bwd(dbd=f(4)) == ALIGN
+
+
+def test_launch_error_reported_as_fs_err_hip():
+    """A call that passes validation on a machine without a GPU fails at its launch: the
+    status is FS_ERR_HIP and the HIP error is recorded for fs_last_hip_error (this thread)."""
+    f = Fake()
+    p = prob(N=64, H=2, G=32)
+    md = MixDesc.make(1, A=f())
+    st = fs.lib().fs_mix(ctypes.byref(p), ctypes.byref(md), f(), f(), None, None)
+    assert st == HIP
+    assert fs.last_hip_error() != 0
+    err = fs.FsError(st, "fs_mix")
+    assert "HIP runtime error" in str(err) and "hipError_t" in str(err)
+
+
+def test_device_memory_flat_in_G():
+    """The device memory of one forward + backward (point tensors, saved normaliser and both
+    workspaces) at fixed N = 2^18, H = 8, dh = 32, bf16, as G sweeps from 32 to 1024: it grows
+    by under 1.5% of one N x G fp32 slice-weight tensor at G = 1024 (the workspaces hold
+    partial sums and token-sized buffers, never an N x G tensor), where the slice weights
+    themselves grow by 31/32 of it."""
+    N, H, D = 1 << 18, 8, 32
+    points = 6 * N * H * D * 2 + N * H * 4          # x, fx, out, dout, dx, dfx; lse
+    totals = {}
+    for G in (32, 64, 128, 256, 512, 1024):
+        p = prob(N=N, H=H, D=D, V=D, G=G, dtype=1)
+        ws = fs.workspace_bytes(p, 0) + fs.workspace_bytes(p, 1)
+        totals[G] = points + ws
+        assert ws < 0.06 * N * H * G * 4, (G, ws)
+    w1024 = N * H * 1024 * 4
+    assert max(totals.values()) - totals[32] < 0.015 * w1024, totals

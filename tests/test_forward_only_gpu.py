@@ -13,7 +13,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from paritycheck import TOL, Checker, announce, measures
+from paritycheck import ELEM_TOL, KAPPA, TOL, Checker, announce, measures
 
 pytestmark = pytest.mark.gpu
 
@@ -79,8 +79,8 @@ def test_forward_only(w):
     fs.deslice_fwd(pb.prob, pb.x, pb.Ws, pb.b, pb.tau, pb.zmix, lse, out3)
     torch.cuda.synchronize()
     out3_h = out3.float().cpu().numpy().astype(np.float64)
-    n3, e3 = measures(out3_h, got["out"], 1.0 if w.dtype == "f32" else 2.0)
-    assert n3 <= TOL[w.dtype] and e3 <= TOL[w.dtype], (n3, e3)
+    n3, e3 = measures(out3_h, got["out"], KAPPA[w.dtype])
+    assert n3 <= TOL[w.dtype] and e3 <= ELEM_TOL[w.dtype], (n3, e3)
 
 
 def test_forward_only_empty_point_set():

@@ -6,7 +6,7 @@ import pytest
 
 import oracle as O
 import workloads as W
-from paritycheck import Checker, TOL, measures, oracle_pairs
+from paritycheck import ELEM_TOL, KAPPA, TOL, Checker, measures, oracle_pairs
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -14,24 +14,25 @@ def test_checker_rejects_one_perturbed_point(dtype):
     rng = np.random.default_rng(11)
     B, N, H, V = 1, 1 << 16, 8, 32
     ref = rng.standard_normal((B, N, H, V))
-    tol = TOL[dtype]
+    tol, etol, kappa = TOL[dtype], ELEM_TOL[dtype], KAPPA[dtype]
     # a correct result: relative noise well inside the tolerance everywhere
     good = ref * (1 + 0.1 * tol * rng.uniform(-1, 1, ref.shape))
-    n0, e0 = measures(good, ref, 2.0 if dtype == "bf16" else 1.0)
-    assert n0 <= tol and e0 <= tol
+    n0, e0 = measures(good, ref, kappa)
+    assert n0 <= tol and e0 <= etol
+    p = int(np.argmax(np.abs(ref[0, :, 3, :]).max(axis=1) > 1.5))   # a point with a value above 1.5 rms
     for planted in ("zero row", "sign flip", "swapped heads"):
         bad = good.copy()
-        p = 12345
         if planted == "zero row":
             bad[0, p, 3, :] = 0.0
         elif planted == "sign flip":
-            bad[0, p, 3, 7] = -bad[0, p, 3, 7]
+            v = int(np.argmax(np.abs(ref[0, p, 3, :])))
+            bad[0, p, 3, v] = -bad[0, p, 3, v]
         else:
             bad[0, p, [2, 3], :] = bad[0, p, [3, 2], :]
-        n, e = measures(bad, ref, 2.0 if dtype == "bf16" else 1.0)
+        n, e = measures(bad, ref, kappa)
         if dtype == "bf16":
             assert n <= tol, (planted, n)      # invisible to the normwise measure ...
-        assert e > tol, (planted, e)           # ... but not to the element-wise one
+        assert e > etol, (planted, e)          # ... but not to the element-wise one
         c = Checker("plant", dtype)
         c.add("out", bad, ref)
         with pytest.raises(AssertionError):

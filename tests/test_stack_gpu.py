@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import workloads as W
-from paritycheck import announce, eager_gate, measures
+from paritycheck import KAPPA, announce, eager_gate, measures
 from oracle.stack import reference_step
 
 pytestmark = pytest.mark.gpu
@@ -51,8 +51,8 @@ def test_stack_training_step_matches_reference():
     bad = {}
     worst = (0.0, "")
     for k in got:
-        n, e = measures(got[k], g64[k], 1.0)
-        en, ee = measures(g32[k], g64[k], 1.0)
+        n, e = measures(got[k], g64[k], KAPPA["f32"])
+        en, ee = measures(g32[k], g64[k], KAPPA["f32"])
         gn, ge = max(1e-5, eager_gate(en)), max(1e-5, eager_gate(ee))
         worst = max(worst, (n / gn, k))
         if not (n <= gn and e <= ge):

@@ -204,3 +204,23 @@ def random_like(w: Workload, seed_k: int, shape, std=1.0) -> np.ndarray:
     """Extra seeded N(0, std^2) tensor (for tests that need more random data)."""
     rng = np.random.default_rng([SEED, w.cfg_id, 1000 + seed_k, w.G])
     return _normal(rng, shape, std)
+
+
+# The full 8-layer slicing stack (each layer: LayerNorm -> projections -> slice, constant
+# G x G mix, deslice -> output projection -> residual -> GELU MLP at width 4C -> residual),
+# fp32, trained with the loss sum(out * R): the input features h and R, each (B, N, C), drawn
+# i.i.d. N(0, 1); the layer weights come from torch's seeded initialisation.
+STACKS = {"stack8": dict(L=8, B=4, N=1 << 17, C=256, H=8, G=64, cfg_id=9)}
+
+
+def make_stack_inputs(name: str, B: Optional[int] = None, N: Optional[int] = None):
+    """(h, R) of a stack workload as fp32 numpy arrays (B, N, C); B and N may be cut down
+    (the leading samples and points of the full draw are not reproduced: a cut is a draw of
+    its own, from the same streams)."""
+    spec = STACKS[name]
+    B = spec["B"] if B is None else B
+    N = spec["N"] if N is None else N
+    C = spec["C"]
+    h = np.random.default_rng([SEED, spec["cfg_id"], 1, C]).standard_normal((B, N, C), dtype=np.float32)
+    R = np.random.default_rng([SEED, spec["cfg_id"], 2, C]).standard_normal((B, N, C), dtype=np.float32)
+    return h, R
