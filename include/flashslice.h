@@ -122,6 +122,20 @@ int fs_slice_fwd(const fs_problem* prob, const void* x, const void* fx, const fl
                  const float* bias, const float* tau, float* z, float* s, float* lse,
                  void* ws, size_t ws_bytes, void* hip_stream);
 
+/* fs_slice_fwd for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same computation and
+ * the same outputs (z, s, optional lse), with the workspace taken from a static scratch
+ * array of 64 MiB that the library holds on every GPU it runs on until the process ends. With
+ * it the whole forward (this call, fs_mix, fs_deslice_fwd or fs_deslice_stats_fwd) needs no
+ * caller workspace. It allocates nothing and calls no allocating routine. Returns
+ * FS_ERR_WORKSPACE when the problem needs more than 64 MiB (fs_workspace_bytes(prob, 0, .)
+ * tells), FS_ERR_ARG when hip_stream belongs to a device other than the current one. The
+ * scratch is shared by every call on one GPU: calls that overlap on one GPU (other streams,
+ * other threads) race on it and must be serialised by the caller.                          */
+int fs_slice_fwd_noalloc(const fs_problem* prob, const void* x, const void* fx,
+                         const float* Ws, const float* bias, const float* tau, float* z,
+                         float* s, float* lse, void* hip_stream);
+
 /* Token mix (paper: Sec. 2; Eq. (1); the attention-free variant). z, zmix: (B,H,G,V).
  * attn_probs: (B,H,G,G) output, required for FS_MIX_ATTN (saved for the backward),
  * ignored otherwise. Needs no workspace for any G (attention up to G = 1024 included).      */

@@ -15,7 +15,8 @@ from typing import Optional
 
 __all__ = [
     "F32", "BF16", "MIX_IDENTITY", "MIX_LINEAR_G", "MIX_LINEAR_C", "MIX_ATTN",
-    "FsError", "Problem", "MixDesc", "lib", "lib_path", "workspace_bytes", "slice_fwd", "mix",
+    "FsError", "Problem", "MixDesc", "lib", "lib_path", "workspace_bytes", "slice_fwd",
+    "slice_fwd_noalloc", "mix",
     "mix_bwd", "deslice_fwd", "deslice_stats_fwd", "slice_deslice_bwd", "untied_bwd",
     "linearno_slice_fwd", "linearno_bwd", "status_string", "last_hip_error",
     "set_pass_events", "EXPORTED", "PASS_SLICE", "PASS_DESLICE", "PASS_BWD_A", "PASS_BWD_B",
@@ -24,7 +25,7 @@ __all__ = [
 F32, BF16 = 0, 1
 MIX_IDENTITY, MIX_LINEAR_G, MIX_LINEAR_C, MIX_ATTN = 0, 1, 2, 3
 
-EXPORTED = ("fs_workspace_bytes", "fs_slice_fwd", "fs_mix", "fs_mix_bwd", "fs_deslice_fwd",
+EXPORTED = ("fs_workspace_bytes", "fs_slice_fwd", "fs_slice_fwd_noalloc", "fs_mix", "fs_mix_bwd", "fs_deslice_fwd",
             "fs_deslice_stats_fwd", "fs_slice_deslice_bwd", "fs_untied_bwd",
             "fs_linearno_slice_fwd", "fs_linearno_bwd", "fs_set_pass_events", "fs_status_string",
             "fs_last_hip_error")
@@ -88,6 +89,7 @@ def lib() -> ctypes.CDLL:
         mixp = ctypes.POINTER(MixDesc)
         L.fs_workspace_bytes.argtypes = [prob, ctypes.c_int, ctypes.POINTER(S)]
         L.fs_slice_fwd.argtypes = [prob, P, P, P, P, P, P, P, P, P, S, P]
+        L.fs_slice_fwd_noalloc.argtypes = [prob, P, P, P, P, P, P, P, P, P]
         L.fs_mix.argtypes = [prob, mixp, P, P, P, P]
         L.fs_mix_bwd.argtypes = [prob, mixp, P, P, P, P, P, P, S, P]
         L.fs_deslice_fwd.argtypes = [prob, P, P, P, P, P, P, P, P]
@@ -167,6 +169,12 @@ def slice_fwd(prob, x, fx, Ws, b, tau, z, s, lse, ws, ws_bytes=None, stream=None
                               _ptr(tau), _ptr(z), _ptr(s), _ptr(lse), _ptr(ws),
                               _nbytes(ws) if ws_bytes is None else ws_bytes, _stream(stream)),
            "fs_slice_fwd")
+
+
+def slice_fwd_noalloc(prob, x, fx, Ws, b, tau, z, s, lse, stream=None) -> None:
+    _check(lib().fs_slice_fwd_noalloc(ctypes.byref(prob), _ptr(x), _ptr(fx), _ptr(Ws), _ptr(b),
+                                      _ptr(tau), _ptr(z), _ptr(s), _ptr(lse), _stream(stream)),
+           "fs_slice_fwd_noalloc")
 
 
 def mix(prob, mixdesc, z, zmix, attn=None, stream=None) -> None:

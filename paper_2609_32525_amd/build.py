@@ -13,7 +13,7 @@ OBJDIR = os.path.join(HERE, "_build")
 SOURCES = [os.path.join(HERE, "csrc", f) for f in (
     "fs_pass_bwd_b.hip", "fs_pass_slice.hip", "fs_pass_deslice.hip", "fs_pass_bwd_a.hip",
     "fs_pass_point.hip", "fs_pass_linearno.hip", "fs_pass_bwd_b2.hip",
-    "fs_kernels.hip", "fs_tokens.hip", "fs_tokmix.hip", "fs_api.cpp")]
+    "fs_kernels.hip", "fs_tokens.hip", "fs_tokmix.hip", "fs_noalloc.hip", "fs_api.cpp")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # Per-source flags: MFMA results in VGPRs rather than accumulation registers measured faster
 # for the slice and deslice passes (less accumulator traffic around the softmax) and slower

@@ -391,6 +391,36 @@ int fs_slice_fwd(const fs_problem* prob, const void* x, const void* fx, const fl
                                      static_cast<hipStream_t>(hip_stream)));
 }
 
+int fs_slice_fwd_noalloc(const fs_problem* prob, const void* x, const void* fx, const float* Ws,
+                         const float* bias, const float* tau, float* z, float* s, float* lse,
+                         void* hip_stream) {
+  Geom g;
+  int st = check_problem(prob, &g);
+  if (st != FS_OK) return st;
+  const Sizes zs = sizes(g);
+  const Buf in[] = {{x, zs.x, true}, {fx, zs.fx, true}, {Ws, zs.Ws, true},
+                    {bias, zs.b, true}, {tau, zs.tau, true}};
+  const Buf out[] = {{z, zs.tok, true}, {s, zs.s, true}, {lse, zs.lse, false}};
+  st = check_bufs(in, 5, out, 3);
+  if (st != FS_OK) return st;
+  if (fs::fwd_ws_layout(g).total > fs::kStaticScratchBytes) return FS_ERR_WORKSPACE;
+  hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e);
+  if (stream != nullptr) {
+    int sdev = -1;
+    e = hipStreamGetDevice(stream, &sdev);
+    if (e != hipSuccess) return hip_status(e);
+    if (sdev != dev) return FS_ERR_ARG;
+  }
+  void* scratch = nullptr;
+  e = fs::static_scratch(dev, &scratch);
+  if (e != hipSuccess) return hip_status(e);
+  return hip_status(fs::launch_slice(g, x, fx, Ws, bias, tau, z, s, lse,
+                                     static_cast<char*>(scratch), stream));
+}
+
 int fs_mix(const fs_problem* prob, const fs_mix_desc* mix, const float* z, float* zmix,
            float* attn_probs, void* hip_stream) {
   Geom g;

@@ -140,6 +140,10 @@ hipError_t launch_reduce_col(const Geom& g, const float* partU, const float* par
 hipError_t launch_linearno_slice(const Geom& g, const void* x, const void* fx, const float* Ws,
                                  const float* bias, const float* tau, float* z, float* clse,
                                  char* ws, hipStream_t st);
+// Static per-device scratch of fs_slice_fwd_noalloc (fs_noalloc.hip): its size, and the
+// device address of `device`'s copy (looked up once per device, with that device current).
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+hipError_t static_scratch(int device, void** ptr);
 // Fills n floats with v (workspace constants; a kernel, so it may be captured in a graph).
 hipError_t launch_fill(float* p, float v, int64_t n, hipStream_t st);
 

@@ -334,3 +334,16 @@ def test_device_memory_flat_in_G():
         assert ws < 0.06 * N * H * G * 4, (G, ws)
     w1024 = N * H * 1024 * 4
     assert max(totals.values()) - totals[32] < 0.015 * w1024, totals
+
+
+def test_noalloc_slice_refuses_oversized_problem():
+    """fs_slice_fwd_noalloc refuses, before anything is enqueued, a problem whose forward
+    workspace exceeds the library's static scratch (64 MiB)."""
+    prob = Problem.make(64, 1 << 22, 8, 32, 32, 1024, fs.BF16, 1e-5)
+    assert fs.workspace_bytes(prob, False) > 64 << 20
+    x, fx, W = 1 << 44, 1 << 45, 1 << 46
+    st = fs.lib().fs_slice_fwd_noalloc(prob, x, fx, W, W + (1 << 20), W + (1 << 21), 1 << 47,
+                                       (1 << 47) + (1 << 30), None, None)
+    assert st == WS
+    small = Problem.make(1, 4096, 8, 32, 32, 64, fs.BF16, 1e-5)
+    assert fs.workspace_bytes(small, False) <= 64 << 20
