@@ -2,19 +2,12 @@
 // computes the per-point softmax statistics itself (no lse input; optionally writes lse).
 // Kernel design and MFMA lane layouts are described at the top of fs_stream.h.
 
-#include <type_traits>
-
 #include "fs_stream.h"
 
 // Output tiles staged through LDS for whole-segment 16-byte stores (1) or stored straight
 // from the MFMA result layout, 4 values per lane (0).
 #ifndef FS_DESLICE_STAGE
 #define FS_DESLICE_STAGE 1
-#endif
-// bf16 point tiles loaded straight into LDS (buffer loads with the LDS destination), FS_DESLICE_DMA
-// tiles ahead of the one being computed, instead of through registers (0: register pipeline).
-#ifndef FS_DESLICE_DMA
-#define FS_DESLICE_DMA 0
 #endif
 
 namespace fs {
@@ -224,96 +217,8 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
       }
     }
   };
-  constexpr int KI = D * (int)sizeof(T) / 64;  // 1 KB direct-to-LDS loads per 16-point block
-  constexpr bool DMA = BF && FS_DESLICE_DMA > 0 && KI >= 1 && NS < FS_NS_NOPF;
-  if constexpr (DMA) {
-    // Ring of FS_DESLICE_DMA tile slots per wavefront, each its own LDS array (so that the
-    // compiler's wait counts track the slots separately). Lane (i, j)'s k-th load of 16-point
-    // block pb fetches the 16 bytes of row i that its own row operand holds (column chunk
-    // KI j + k), and the hardware places lane L's 16 bytes at slot + 16 L: every lane reads
-    // back exactly what it loaded, with no layout change and no bank conflicts.
-    constexpr int KS = FS_DESLICE_DMA;
-    static_assert(KS >= 2 && KS <= 4, "2 to 4 slots");
-    __shared__ __attribute__((aligned(16))) uint4 q0[NP][2][KI][64];
-    __shared__ __attribute__((aligned(16))) uint4 q1[NP][2][KI][64];
-    __shared__ __attribute__((aligned(16))) uint4 q2[KS > 2 ? NP : 1][2][KI][64];
-    __shared__ __attribute__((aligned(16))) uint4 q3[KS > 3 ? NP : 1][2][KI][64];
-    auto issue = [&](auto slot, int t) {
-      const int tb = (t * NP + wpu) * 32;
-#pragma unroll
-      for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-        for (int k = 0; k < KI; ++k) {
-          uint4* dst;
-          if constexpr (decltype(slot)::value == 0) dst = &q0[wp][pb][k][0];
-          else if constexpr (decltype(slot)::value == 1) dst = &q1[wp][pb][k][0];
-          else if constexpr (decltype(slot)::value == 2) dst = &q2[KS > 2 ? wp : 0][pb][k][0];
-          else dst = &q3[KS > 3 ? wp : 0][pb][k][0];
-          __builtin_amdgcn_raw_ptr_buffer_load_lds(
-              rx, (__attribute__((address_space(3))) void*)dst, 16,
-              i * rsb + (KI * j + k) * 16, (tb + 16 * pb) * rsb, 0, 0);
-        }
-    };
-    auto fetch = [&](auto slot, RowOp<BF, D>(&xo)[2]) {
-#pragma unroll
-      for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-        for (int k = 0; k < KI; ++k) {
-          uint4 v;
-          if constexpr (decltype(slot)::value == 0) v = q0[wp][pb][k][lane];
-          else if constexpr (decltype(slot)::value == 1) v = q1[wp][pb][k][lane];
-          else if constexpr (decltype(slot)::value == 2) v = q2[KS > 2 ? wp : 0][pb][k][lane];
-          else v = q3[KS > 3 ? wp : 0][pb][k][lane];
-          xo[pb].v[k] = __builtin_bit_cast(bf8, v);
-        }
-    };
-    auto lse_of = [&](int t, float (&l2)[2]) {
-      const int tb = (t * NP + wpu) * 32;
-#pragma unroll
-      for (int pb = 0; pb < 2; ++pb) {
-        if constexpr (!ST) {
-          const float l = bld32(rl, 4 * i, 4 * (tb + 16 * pb));
-          l2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
-        }
-      }
-    };
-    using I0 = std::integral_constant<int, 0>;
-    using I1 = std::integral_constant<int, 1>;
-    using I2 = std::integral_constant<int, 2>;
-    using I3 = std::integral_constant<int, 3>;
-    auto issue_q = [&](int q, int t) {
-      if (q == 0) issue(I0{}, t);
-      else if (q == 1) issue(I1{}, t);
-      else if (q == 2) issue(I2{}, t);
-      else issue(I3{}, t);
-    };
-    // prologue: tiles 0 .. KS - 2 in flight
-#pragma unroll
-    for (int q = 0; q < KS - 1; ++q) issue_q(q, q);
-    float l2n[2];
-    lse_of(0, l2n);
-    for (int t0 = 0; t0 < ntile; t0 += KS) {
-#pragma unroll
-      for (int u = 0; u < KS; ++u) {
-        const int t = t0 + u;
-        if (t >= ntile) break;
-        // refill the slot the previous tile used (unconditional: past the end the loads
-        // return zeros), then take this tile's lse and operands
-        issue_q((u + KS - 1) % KS, t + KS - 1);
-        float l2[2] = {l2n[0], l2n[1]};
-        lse_of(t + 1, l2n);
-        RowOp<BF, D> xo[2];
-        if (u == 0) fetch(I0{}, xo);
-        else if (u == 1) fetch(I1{}, xo);
-        else if (u == 2) fetch(I2{}, xo);
-        else fetch(I3{}, xo);
-        body(xo, l2, t);
-      }
-    }
-  } else {
-    pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_DESLICE), Tile>(
-        ntile, load_tile, [&](Tile& cur, int t) { body(cur.xo, cur.lse2, t); });
-  }
+  pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_DESLICE), Tile>(
+      ntile, load_tile, [&](Tile& cur, int t) { body(cur.xo, cur.lse2, t); });
 }
 
 template <bool ST>
