@@ -41,6 +41,10 @@ bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 #ifndef FS_TARGET_LONG
 #define FS_TARGET_LONG 1024
 #endif
+// The slice on long streams: chunks made of strided sub-chunks of FS_MAX_TILES tiles (1).
+#ifndef FS_SLICE_STRIDE
+#define FS_SLICE_STRIDE 1
+#endif
 // Most point tiles per chunk on long streams (0: no limit).
 #ifndef FS_MAX_TILES
 #define FS_MAX_TILES 64
@@ -119,6 +123,17 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
   int64_t tiles_per_chunk = (ntiles + chunks - 1) / chunks;
   c.chunk_pts = tiles_per_chunk * step;
   c.chunks = (int)std::max<int64_t>(1, (g.N + c.chunk_pts - 1) / c.chunk_pts);
+  c.nsub = c.chunks;
+  c.sub_pts = c.chunk_pts;
+  // very long streams of the slice: a chunk's points are sub-chunks of at most FS_MAX_TILES
+  // tiles spread over the stream (chunk c takes sub-chunks c, c + chunks, ...), so that the
+  // head workgroups of every row block, which share its lines through one L2, reach it close
+  // together, with the partial count (and so the workspace) unchanged
+  if (FS_MAX_TILES > 0 && FS_SLICE_STRIDE && pass == PASS_SLICE && c.NS < 8 && !blk &&
+      tiles_per_chunk > FS_MAX_TILES) {
+    c.sub_pts = (int64_t)FS_MAX_TILES * step;
+    c.nsub = (g.N + c.sub_pts - 1) / c.sub_pts;
+  }
   return c;
 }
 

@@ -69,6 +69,11 @@ struct PassCfg {
   int nblk;
   int chunks;
   int64_t chunk_pts;
+  // On long streams a chunk is a set of sub-chunks of sub_pts points, sub-chunks c, c + chunks,
+  // c + 2 chunks, ... of the nsub along the points (nsub = chunks, sub_pts = chunk_pts
+  // otherwise): a pass with per-chunk partials keeps its partial count while its workgroups
+  // sweep the rows together.
+  int64_t nsub, sub_pts;
 };
 
 PassCfg pick_cfg(const Geom& g, Pass pass);
@@ -109,6 +114,7 @@ struct PassArgs {
   int nblk;
   int chunks;
   int64_t chunk_pts;
+  int64_t nsub, sub_pts;  // sub-chunks (see PassCfg)
 };
 
 // One streaming pass over the points with the tiling pick_cfg chooses (fs_pass_*.hip).

@@ -34,6 +34,8 @@ PassArgs base_args(const Geom& g, Pass p) {
   a.nblk = cfg.nblk;
   a.chunks = cfg.chunks;
   a.chunk_pts = cfg.chunk_pts;
+  a.nsub = cfg.nsub;
+  a.sub_pts = cfg.sub_pts;
   return a;
 }
 

@@ -5,6 +5,12 @@
 
 #include "fs_stream.h"
 
+// bf16 head width 32: backward pass A (and the slot-owned slice) load dout / fx as rows and
+// form the point-ordered operand through LDS (1), or gather it point by point (0).
+#ifndef FS_BWDA_T
+#define FS_BWDA_T 1
+#endif
+
 namespace fs {
 namespace {
 
@@ -50,26 +56,61 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   const auto rl = rows_rsrc(lse + pbeg, npts, 1, 1);
   const int wpu = __builtin_amdgcn_readfirstlane(wp);
 
+  // TR: bf16 dout (or fx) tiles arrive as rows, 16 bytes per lane like x, and are turned into
+  // the point-ordered k-operand through this wavefront's LDS rows; lse arrives one value per
+  // point and is spread over the lanes by shuffles.
+  constexpr bool TR = FS_BWDA_T && BF && D == 32 && NS == 1;
+  constexpr int kTP = 80;  // LDS row pitch (64 bytes of a head row + 16)
+  __shared__ __attribute__((aligned(16))) char trs[TR ? NP : 1][TR ? 32 * kTP : 16];
   struct Tile {
     RowOp<BF, D> xo[2];
     float lse2[2][4];
     PtGather<BF, VB> g;
+    uint4 grow[TR ? 2 : 1];
+    float l1[TR ? 2 : 1];
   };
   auto load_tile = [&](Tile& tt, int t) {
     const int tb = (t * NP + wpu) * 32;
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) {
       load_row_buf<BF, D>(tt.xo[pb], rx, i * rsb, (tb + 16 * pb) * rsb, j);
+      if constexpr (TR) {
+        tt.grow[pb] = bld128u(rg, i * rsb + 16 * j, (tb + 16 * pb) * rsb);
+        const float l = bld32(rl, 4 * i, 4 * (tb + 16 * pb));
+        tt.l1[pb] = tb + 16 * pb + i < npts ? l : kMasked;
+      } else {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float l = bld32(rl, 4 * (4 * j + r), 4 * (tb + 16 * pb));
-        tt.lse2[pb][r] = tb + 16 * pb + 4 * j + r < npts ? l : kMasked;
+        for (int r = 0; r < 4; ++r) {
+          const float l = bld32(rl, 4 * (4 * j + r), 4 * (tb + 16 * pb));
+          tt.lse2[pb][r] = tb + 16 * pb + 4 * j + r < npts ? l : kMasked;
+        }
       }
     }
-    gather_points_buf<BF, VB>(tt.g, rg, rsb, tb * rsb, i, j);
+    if constexpr (!TR) gather_points_buf<BF, VB>(tt.g, rg, rsb, tb * rsb, i, j);
   };
   pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_BWD_A), Tile>(ntile, load_tile, [&](Tile& cur, int t) {
     const RowOp<BF, D>* xo = cur.xo;
+    if constexpr (TR) {
+      char* tr = trs[wp];
+      wave_lds_sync();
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+        *reinterpret_cast<uint4*>(tr + (16 * pb + i) * kTP + 16 * j) = cur.grow[pb];
+      wave_lds_sync();
+#pragma unroll
+      for (int cb = 0; cb < VB; ++cb) {
+        bf8 bt;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          bt[e] = *reinterpret_cast<const __bf16*>(tr + (16 * (e / 4) + 4 * j + (e % 4)) * kTP +
+                                                   (16 * cb + i) * 2);
+        cur.g.v[cb] = bt;
+      }
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) cur.lse2[pb][r] = __shfl(cur.l1[pb], 4 * j + r);
+    }
     const float(*lse2)[4] = cur.lse2;
     f4 w[2][GB];
 #pragma unroll

@@ -5,6 +5,13 @@
 
 #include "fs_stream.h"
 
+// bf16 head width 32 (the fused pass B, not the slot-owned parameter pass): dW_s's
+// point-ordered x operand from the loaded rows through LDS (1), or a second, point-by-point
+// load of x (0).
+#ifndef FS_BWDB_XT
+#define FS_BWDB_XT 1
+#endif
+
 namespace fs {
 namespace {
 
@@ -133,6 +140,11 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
   __shared__ __attribute__((aligned(16))) char smem[kGxBytes > kDaBytes ? kGxBytes : kDaBytes];
   f4* gx = reinterpret_cast<f4*>(smem);
   float* myda = reinterpret_cast<float*>(smem) + (size_t)wave * kDaWords;
+  // XT: bf16 with head width 32 forms dW_s's point-ordered x operand from the row operand the
+  // logits already loaded, through this wavefront's LDS rows, instead of loading x again
+  constexpr bool XT = FS_BWDB_XT && BF && D == 32 && PB == 2 && !PM;
+  constexpr int kXP = 80;  // LDS row pitch
+  __shared__ __attribute__((aligned(16))) char xts[XT ? NS * NP : 1][XT ? 32 * kXP : 16];
 
   const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
@@ -177,7 +189,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
         tt.ct[pb][1] = bld32(rc, 8 * i + 4, 8 * (tb + 16 * pb));
       }
     }
-    gather_k<BF, DB, PB>(tt.xk, rx, rsb, tb, i, j);
+    if constexpr (!XT) gather_k<BF, DB, PB>(tt.xk, rx, rsb, tb, i, j);
   };
   // fp32 with 64-slot waves has the longest tiles to cover: one more tile in flight there
   constexpr int PF = NS >= FS_NS_NOPF ? 0 : (!BF && GS == 64 && NS == 1 ? FS_PF_BWD_B + 1 : FS_PF_BWD_B);
@@ -345,6 +357,22 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
     }
     }
     // dW_s += X^T da over the tile's points: da goes through LDS to put points on the k index.
+    if constexpr (XT) {
+      char* xt = xts[wave];
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+        *reinterpret_cast<bf8*>(xt + (16 * pb + i) * kXP + 16 * j) = xo[pb].v[0];
+      wave_lds_sync();
+#pragma unroll
+      for (int d = 0; d < DB; ++d) {
+        bf8 bt;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          bt[e] = *reinterpret_cast<const __bf16*>(xt + (16 * (e / 4) + 4 * j + (e % 4)) * kXP +
+                                                   (16 * d + i) * 2);
+        cur.xk.v[d] = bt;
+      }
+    }
     const KGather<BF, DB, PB>& XK = cur.xk;
     if constexpr (!BF) {
       // myda[p * (GS + 1) + gl]

@@ -4,14 +4,22 @@
 
 #include "fs_stream.h"
 
+// bf16 head width 32, one slot wave per tile: the slice loads fx as rows and forms the
+// point-ordered operand through LDS when it writes no normaliser (1: the forward-only slice;
+// 2: always), or gathers it point by point (0). Measured at N = 2^24 (no normaliser) 2%
+// faster, and at N = 2^20 with the normaliser written 6% slower.
+#ifndef FS_SLICE_T
+#define FS_SLICE_T 1
+#endif
+
 namespace fs {
 namespace {
 
 // =======================================================================================
 // Slice pass
 // =======================================================================================
-// ST: statistics only (lse), no token accumulation.
-template <bool BF, int D, int GS, int NS, int NP, bool ST>
+// ST: statistics only (lse), no token accumulation. TRX: fx through LDS (above).
+template <bool BF, int D, int GS, int NS, int NP, bool ST, bool TRX>
 __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_SLICE))) void k_slice(
     PassArgs a) {
   constexpr int GB = GS / 16, VB = D / 16;
@@ -42,26 +50,39 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   __shared__ float st_m[NS > 1 ? 2 : 1][NP][NS][32];
   __shared__ float st_l[NS > 1 ? 2 : 1][NP][NS][32];
 
-  const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
-  const int64_t pend = min(a.N, pbeg + a.chunk_pts);
+  const int rsb = (int)(rs * sizeof(T));
+  const bool want_lse = a.lse_out != nullptr;
+  const int wpu = __builtin_amdgcn_readfirstlane(wp);
+  // this chunk's sub-chunks: c.chunk, c.chunk + chunks, ... (one unless the stream is long)
+  for (int64_t sub = c.chunk; sub < a.nsub; sub += a.chunks) {
+  const int64_t pbeg = sub * a.sub_pts;
+  const int64_t pend = min(a.N, pbeg + a.sub_pts);
   const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
   const int ntile = (npts + 32 * NP - 1) / (32 * NP);
-  const int rsb = (int)(rs * sizeof(T));
   const auto rx = rows_rsrc(xb + pbeg * rs, npts, (int)rs, D);
   const auto rf = rows_rsrc(fb + pbeg * rs, npts, (int)rs, D);
-  const bool want_lse = a.lse_out != nullptr;
   const auto rl = rows_rsrc(want_lse ? a.lse_out + (int64_t)c.bh * a.N + pbeg : a.Ws, npts, 1, 1);
-  const int wpu = __builtin_amdgcn_readfirstlane(wp);
 
+  // TR: bf16 fx tiles (head width 32) arrive as rows, 16 bytes per lane, and become the
+  // point-ordered k-operand of U += w^T fx through this wavefront's LDS rows
+  constexpr bool TR = TRX && BF && D == 32 && !ST && NS == 1;
+  constexpr int kTP = 80;  // LDS row pitch (64 bytes of a head row + 16)
+  __shared__ __attribute__((aligned(16))) char trs[TR ? NP : 1][TR ? 32 * kTP : 16];
   struct Tile {
     RowOp<BF, D> xo[2];
     PtGather<BF, ST ? 1 : VB> f;
+    uint4 frow[TR ? 2 : 1];
   };
   auto load_tile = [&](Tile& tt, int t) {
     const int tbo = (t * NP + wpu) * 32 * rsb;
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) load_row_buf<BF, D>(tt.xo[pb], rx, i * rsb, tbo + 16 * pb * rsb, j);
-    if constexpr (!ST) gather_points_buf<BF, VB>(tt.f, rf, rsb, tbo, i, j);
+    if constexpr (TR) {
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb) tt.frow[pb] = bld128u(rf, i * rsb + 16 * j, tbo + 16 * pb * rsb);
+    } else if constexpr (!ST) {
+      gather_points_buf<BF, VB>(tt.f, rf, rsb, tbo, i, j);
+    }
   };
   pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_SLICE), Tile>(ntile, load_tile, [&](Tile& cur, int t) {
     const int tb = (t * NP + wpu) * 32;
@@ -173,8 +194,26 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
         for (int r = 0; r < 4; ++r) sum += w[pb][gb][r];
       sacc[gb] += sum;
     }
+    if constexpr (TR) {
+      char* tr = trs[wp];
+      wave_lds_sync();
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb)
+        *reinterpret_cast<uint4*>(tr + (16 * pb + i) * kTP + 16 * j) = cur.frow[pb];
+      wave_lds_sync();
+#pragma unroll
+      for (int cb = 0; cb < VB; ++cb) {
+        bf8 bt;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          bt[e] = *reinterpret_cast<const __bf16*>(tr + (16 * (e / 4) + 4 * j + (e % 4)) * kTP +
+                                                   (16 * cb + i) * 2);
+        cur.f.v[cb] = bt;
+      }
+    }
     if constexpr (!ST) mm_points<BF, GB, VB>(U, w, cur.f);
   });
+  }
   if constexpr (ST) return;
 
   // ---- combine the NP point groups and write this workgroup's partials --------------------
@@ -223,7 +262,11 @@ struct Run_k_slice_ {
   struct R {
     static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
       dim3 grid(cfg.chunks * BH * cfg.nblk);
-      hipLaunchKernelGGL((k_slice<BF, D, GS, NS, NP, ST>), grid, dim3(64 * NS * NP), 0, st, a);
+      constexpr bool kCanTR = FS_SLICE_T > 0 && BF && D == 32 && NS == 1 && !ST;
+      if (kCanTR && (FS_SLICE_T == 2 || a.lse_out == nullptr))
+        hipLaunchKernelGGL((k_slice<BF, D, GS, NS, NP, ST, kCanTR>), grid, dim3(64 * NS * NP), 0, st, a);
+      else
+        hipLaunchKernelGGL((k_slice<BF, D, GS, NS, NP, ST, false>), grid, dim3(64 * NS * NP), 0, st, a);
       return hipGetLastError();
     }
   };
