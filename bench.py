@@ -11,7 +11,10 @@ with no saved normaliser instead.
 Besides the step time it reports, for the dominant kernel (backward pass B), the roofline
 point from algorithmic bytes or MFMA flops per launch over its average duration measured with
 HIP events recorded around its launch on the stream it runs on, and the fp64 oracle timed on
-the host cores as a CPU baseline.
+the host cores as a CPU baseline. ``valu`` sets the vector ALU, which binds before the matrix
+cores at large G, beside them: the VALU issue time and the MFMA busy time one step needs, from
+the committed rocprofv3 SQ-counter record of the workload (``profiles/issue_<workload>.json``,
+used only while the kernel sources match it), over the measured step time.
 """
 from __future__ import annotations
 
@@ -68,6 +71,20 @@ def measured_traffic(workload, kernel):
     if d.get("kernel_source_sha256") != kernel_source_hash():
         return None
     return d.get("traffic_bytes_per_launch")
+
+
+def measured_issue(workload):
+    """The vector-ALU and matrix-core time per step from the committed rocprofv3 issue record
+    (SQ instruction counters), if it was taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", f"issue_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        d = json.load(fh)
+    from paper_2609_32525_amd.profiling import kernel_source_hash
+    if d.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return d
 
 
 # State the forked oracle workers read (set before the pool starts, shared copy-on-write).
@@ -447,6 +464,17 @@ def main():
                  "t_hbm_us": step_bytes / HBM_PEAK * 1e6,
                  "t_mfma_us": step_flops / MFMA_PEAK[w.dtype] * 1e6}
 
+    # the vector ALU beside the matrix cores (it binds first at large G): the VALU issue time
+    # and the MFMA busy time one step needs, from the counters, over the measured step time
+    iss = measured_issue(args.workload)
+    valu = None
+    if iss is not None:
+        valu = {"frac": iss["t_valu_us_per_step"] * 1e-6 / t_step,
+                "mfma_busy_frac": iss["t_mfma_us_per_step"] * 1e-6 / t_step,
+                "t_valu_us": iss["t_valu_us_per_step"],
+                "t_mfma_busy_us": iss["t_mfma_us_per_step"],
+                "source": f"profiles/issue_{args.workload}.json"}
+
     value = w.B * w.N / t_step
     out = {
         "metric": METRIC_FWD if fwd_only else METRIC, "value": value, "unit": "points/s", "n_gpus": 1,
@@ -457,6 +485,7 @@ def main():
                    "mix": MIX_NAMES[w.mix], "storage": w.dtype, "graph": bool(args.graph)},
         "roofline": roof,
         "step_roofline": step_roof,
+        "valu": valu,
         "passes_us": pass_us,
         "wall_s_timed": wall,
     }

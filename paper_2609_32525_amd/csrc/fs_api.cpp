@@ -45,6 +45,10 @@ bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 #ifndef FS_SLICE_STRIDE
 #define FS_SLICE_STRIDE 1
 #endif
+// Chunk counts rounded up to a multiple of 8 (1).
+#ifndef FS_XCD_CHUNKS
+#define FS_XCD_CHUNKS 1
+#endif
 // Most point tiles per chunk on long streams (0: no limit).
 #ifndef FS_MAX_TILES
 #define FS_MAX_TILES 64
@@ -123,6 +127,12 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
   int64_t tiles_per_chunk = (ntiles + chunks - 1) / chunks;
   c.chunk_pts = tiles_per_chunk * step;
   c.chunks = (int)std::max<int64_t>(1, (g.N + c.chunk_pts - 1) / c.chunk_pts);
+  // the head (and slot-block) workgroups of one chunk are numbered `chunks` apart, and the 8
+  // XCDs take workgroups round robin: a multiple of 8 puts them on one XCD, so the 128 B lines
+  // that neighbouring heads' row segments share are fetched once into its L2. Chunks past the
+  // last point are empty (their workgroups exit, their partials are zero).
+  if (FS_XCD_CHUNKS && units > 1 && c.chunks >= 8 && c.chunks % 8 != 0)
+    c.chunks = (c.chunks + 7) / 8 * 8;
   c.nsub = c.chunks;
   c.sub_pts = c.chunk_pts;
   // very long streams of the slice: a chunk's points are sub-chunks of at most FS_MAX_TILES

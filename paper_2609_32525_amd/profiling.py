@@ -1,6 +1,7 @@
 """Summaries of rocprofv3 output for the library's kernels (host-side post-processing only).
 
-Two summaries, both written as short text (markdown) plus, for traffic, a JSON record:
+Three summaries, each written as short text (markdown), the issue picture and the traffic
+also as a JSON record:
 
 * ``stats``: per-kernel call count and average / min / max duration from the
   ``kernel_stats.csv`` that ``rocprofv3 --kernel-trace --stats -f csv`` writes.
@@ -11,6 +12,9 @@ Two summaries, both written as short text (markdown) plus, for traffic, a JSON r
   cycles (128 lanes per clock per compute unit, the 157.3 TFLOP/s FMA rate), a
   transcendental one for 8 (a quarter of that rate). GRBM_GUI_ACTIVE is summed over the 8
   XCDs, so the kernel's cycles are its value / 8; the SIMD count is 1024.
+  With ``--workload`` it also writes a JSON record of the vector-ALU and matrix-core time
+  per step (each kernel's busy fraction times its duration and launches per step), which
+  ``bench.py`` divides by its measured step time.
 * ``traffic``: HBM bytes per launch of each kernel from two counter runs
   (``--pmc FETCH_SIZE`` and ``--pmc WRITE_SIZE``, ``-f csv``). Each counter is calibrated by
   what it reads for a plain device-to-device copy of known size that the profiled program
@@ -162,6 +166,31 @@ def issue_summary(path: str) -> Dict[str, Dict[str, float]]:
     return out
 
 
+def issue_record(res: Dict[str, Dict[str, float]], workload: str, command: str) -> dict:
+    """Per-step vector-ALU and matrix-core time from an issue summary: each kernel's SIMD
+    cycles of VALU issue (valu_busy x its cycles) and of MFMA busy, over the 1024 SIMDs at
+    its measured clock, times its launches per step. Launches per step are counted against
+    the deslice, which every step of the path launches exactly once."""
+    steps = max((r["dispatches"] for k, r in res.items() if k.startswith("k_deslice")),
+                default=0)
+    if steps == 0:
+        raise RuntimeError("no deslice dispatches to count steps by")
+    kernels = {}
+    t_valu = t_mfma = 0.0
+    for k, r in res.items():
+        per_step = r["dispatches"] / steps
+        tv = r["valu_busy"] * r["us"]
+        tm = r["mfma_busy"] * r["us"]
+        kernels[k] = {"launches_per_step": per_step, "us": r["us"], "valu_busy": r["valu_busy"],
+                      "mfma_busy": r["mfma_busy"], "t_valu_us": tv, "t_mfma_us": tm}
+        t_valu += tv * per_step
+        t_mfma += tm * per_step
+    return {"workload": workload, "kernel_source_sha256": kernel_source_hash(),
+            "t_valu_us_per_step": t_valu, "t_mfma_us_per_step": t_mfma,
+            "valu_cycles_per_inst": VALU_CYCLES, "trans_cycles_per_inst": TRANS_CYCLES,
+            "kernels": kernels, "command": command}
+
+
 def calibrated_traffic(fetch_dir: str, write_dir: str, copy_mib: float):
     """Per-kernel average (fetch, write) bytes per launch, each counter scaled by its reading
     for the copy of ``copy_mib`` MiB (only copy dispatches of at least half that size count)."""
@@ -201,12 +230,16 @@ def _main():
     q.add_argument("--command", required=True)
     q.add_argument("--title", default="Issue picture")
     q.add_argument("--out", required=True)
+    q.add_argument("--workload", default=None,
+                   help="also write a JSON record (OUT with .json) that bench.py reads")
     t = sub.add_parser("traffic")
     t.add_argument("fetch")
     t.add_argument("write")
     t.add_argument("--copy-mib", type=float, required=True)
     t.add_argument("--workload", required=True)
-    t.add_argument("--kernel", default="k_bwd_b", help="kernel whose JSON record bench reads")
+    t.add_argument("--kernel", action="append",
+                   help="kernel(s) whose summed traffic the JSON record holds (default k_bwd_b; "
+                        "a pass made of two kernels, such as the slot-blocked pass B, names both)")
     t.add_argument("--command", action="append", required=True)
     t.add_argument("--out", required=True, help="output path without extension")
     a = ap.parse_args()
@@ -251,6 +284,10 @@ def _main():
         with open(a.out, "w") as fh:
             fh.write("\n".join(lines) + "\n")
         print("\n".join(lines))
+        if a.workload:
+            rec = issue_record(res, a.workload, a.command)
+            with open(os.path.splitext(a.out)[0] + ".json", "w") as fh:
+                json.dump(rec, fh, indent=1)
         return
 
     cf, cw, res = calibrated_traffic(a.fetch, a.write, a.copy_mib)
@@ -266,16 +303,16 @@ def _main():
     with open(a.out + ".md", "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print("\n".join(lines))
-    mine = [n for n in res if n.startswith(a.kernel + "<") or n == a.kernel]
+    kernels = a.kernel or ["k_bwd_b"]
+    mine = [n for n in res if any(n.startswith(k + "<") or n == k for k in kernels)]
     if mine:
-        r = res[mine[0]]
-        rec = {"workload": a.workload, "kernel": mine[0],
+        fb = sum(res[n]["fetch_bytes"] for n in mine)
+        wb = sum(res[n]["write_bytes"] for n in mine)
+        rec = {"workload": a.workload, "kernel": " + ".join(mine),
                "kernel_source_sha256": kernel_source_hash(),
                "fetch_scale": cf, "write_scale": cw, "copy_mib": a.copy_mib,
-               "fetch_bytes_per_launch": r["fetch_bytes"],
-               "write_bytes_per_launch": r["write_bytes"],
-               "traffic_bytes_per_launch": r["fetch_bytes"] + r["write_bytes"],
-               "commands": a.command}
+               "fetch_bytes_per_launch": fb, "write_bytes_per_launch": wb,
+               "traffic_bytes_per_launch": fb + wb, "commands": a.command}
         with open(a.out + ".json", "w") as fh:
             json.dump(rec, fh, indent=1)
 
