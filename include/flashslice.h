@@ -39,8 +39,9 @@
  *   - tau > 0 is a precondition (tau lives in device memory and is not read by the host).
  *   - Results are deterministic: no atomics; every reduction has a fixed order, so repeated
  *     calls give bitwise identical outputs.
- *   - Supported shapes: D == V in {16, 32, 64}; G a power of two in [16, 1024] (fp32
- *     storage) or [32, 1024] (bf16 storage), for every mix kind; B * H <= 65535. Anything
+ *   - Supported shapes: D == V in {16, 32, 64}; G a multiple of 16 in [16, 1024], for every
+ *     mix kind and storage type (slot counts between the kernels' tile sizes run padded up
+ *     to the next one, the padding slots carrying zero weight); B * H <= 65535. Anything
  *     else returns FS_ERR_UNSUPPORTED.
  *   - Concurrent calls are safe as long as they do not share a workspace.
  */

@@ -21,7 +21,6 @@ thread_local int g_last_hip_error = 0;
 constexpr size_t kAlign = 256;
 constexpr int64_t kCUs = 256;  // MI355X compute units
 size_t up(size_t v, size_t a = kAlign) { return (v + a - 1) / a * a; }
-bool pow2(int v) { return v > 0 && (v & (v - 1)) == 0; }
 
 #ifndef FS_TARGET_PARTIAL
 #define FS_TARGET_PARTIAL 512
@@ -68,22 +67,25 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
   c.nblk = 1;
   const bool blk = blocked(g);
   const bool slot_owned = blk && (pass == PASS_SLICE || pass == PASS_BWD_A || pass == PASS_BWD_B);
+  // Slot counts that are not a whole tiling are padded up to one: the padding slots get a
+  // masked logit (zero weight) and zero operands, and nothing of theirs is stored.
   if (g.G <= 64) {
-    c.GS = g.G;
+    c.GS = g.G <= 16 && !g.bf16 ? 16 : (g.G <= 32 ? 32 : 64);  // bf16: 32-slot MFMA k sets
     c.NS = 1;
     c.NP = 4;
   } else if (slot_owned) {
     c.GS = 64;
     c.NS = 1;
     c.NP = 4;
-    c.nblk = g.G / 64;
+    c.nblk = (g.G + 63) / 64;
   } else if (pass == PASS_POINT) {
     c.GS = 64;  // slot block streamed through LDS
     c.NS = 1;
     c.NP = FS_POINT_WAVES;
   } else {
     c.GS = 64;
-    c.NS = g.G / 64;
+    c.NS = 2;  // the slot-wave counts with a tiling: 2, 4, 8, 16
+    while (64 * c.NS < g.G) c.NS *= 2;
     c.NP = c.NS == 2 ? 2 : 1;
   }
   // fp32 backward pass B works on 16-point tiles (its register footprint is the largest)
@@ -252,8 +254,7 @@ int check_problem(const fs_problem* p, Geom* g) {
   // what the kernels implement
   if (p->D != p->V) return FS_ERR_UNSUPPORTED;
   if (p->D != 16 && p->D != 32 && p->D != 64) return FS_ERR_UNSUPPORTED;
-  if (!fs::pow2(p->G) || p->G > 1024 || p->G < (p->dtype == FS_BF16 ? 32 : 16))
-    return FS_ERR_UNSUPPORTED;
+  if (p->G % 16 != 0 || p->G > 1024) return FS_ERR_UNSUPPORTED;
   if (p->B * (int64_t)p->H > 65535) return FS_ERR_UNSUPPORTED;
   if (p->N > ((int64_t)1 << 40)) return FS_ERR_UNSUPPORTED;
   g->B = p->B;

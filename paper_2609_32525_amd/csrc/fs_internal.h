@@ -115,6 +115,7 @@ struct PassArgs {
   int chunks;
   int64_t chunk_pts;
   int64_t nsub, sub_pts;  // sub-chunks (see PassCfg)
+  int padded;  // the tiling covers more slots than G: slots >= G are padding (masked)
 };
 
 // One streaming pass over the points with the tiling pick_cfg chooses (fs_pass_*.hip).

@@ -36,6 +36,10 @@ PassArgs base_args(const Geom& g, Pass p) {
   a.chunk_pts = cfg.chunk_pts;
   a.nsub = cfg.nsub;
   a.sub_pts = cfg.sub_pts;
+  // slots the tiling covers: GS per slot wave, NS waves, nblk blocks (the point-owned passes
+  // sweep blocks of 64)
+  const int covered = p == PASS_POINT ? 64 * ((g.G + 63) / 64) : cfg.GS * cfg.NS * cfg.nblk;
+  a.padded = covered != g.G ? 1 : 0;
   return a;
 }
 

@@ -33,10 +33,10 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   const float* lse = a.lse_in + (int64_t)c.bh * a.N;
 
   SlotOp<BF, D, GB> wop;
-  load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, c.sc, i, j);
+  load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, slot_lim(a), c.sc, i, j);
   float bS[GB];
 #pragma unroll
-  for (int gb = 0; gb < GB; ++gb) bS[gb] = c.sc * c.bias[c.g0 + 16 * gb + i];
+  for (int gb = 0; gb < GB; ++gb) bS[gb] = slot_bias(c, a, c.g0 + 16 * gb, i);
   f4 Z[GB][VB];
   float sacc[GB];
 #pragma unroll
@@ -169,13 +169,15 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
       for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          pZ[(int64_t)(c.g0 + 16 * gb + 4 * j + r) * D + 16 * vb + i] = Z[gb][vb][r];
+        for (int r = 0; r < 4; ++r) {
+          const int g = c.g0 + 16 * gb + 4 * j + r;
+          if (g < a.G) pZ[(int64_t)g * D + 16 * vb + i] = Z[gb][vb][r];
+        }
     if constexpr (SL) {
       float* pS = a.part2 + ((int64_t)c.bh * a.chunks + c.chunk) * a.G;
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb)
-        if (j == 0) pS[c.g0 + 16 * gb + i] = sacc[gb];
+        if (j == 0 && c.g0 + 16 * gb + i < a.G) pS[c.g0 + 16 * gb + i] = sacc[gb];
     }
   }
 }

@@ -69,9 +69,13 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
   for (int gb = 0; gb < GB; ++gb)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int slot = c.g0 + 16 * gb + 4 * j + r;
-      bT[gb][r] = c.sc * c.bias[slot] - (COLN ? a.clse[(int64_t)c.bh * a.G + slot] : 0.f);
-      dsT[gb][r] = ROLE == 2 ? 0.f : a.ds[(int64_t)c.bh * a.G + slot] - (COLN ? 0.f : cen[2 * D]);
+      // padding blocks (slots >= G) read the last real block and take a masked logit, no ds
+      bool real;
+      const int sl = slot_block(c.g0 + 16 * gb, slot_lim(a), real) + 4 * j + r;
+      const float bv = c.sc * c.bias[sl] - (COLN ? a.clse[(int64_t)c.bh * a.G + sl] : 0.f);
+      const float dv = ROLE == 2 ? 0.f : a.ds[(int64_t)c.bh * a.G + sl] - (COLN ? 0.f : cen[2 * D]);
+      bT[gb][r] = slot_mask(real, bv, kMaskedSlot);
+      dsT[gb][r] = slot_mask(real, dv, 0.f);
     }
 
   // operands: W_s (logits), zmix and dU (dw, contraction over v), dU (dfx) and W_s / tau (dx)
@@ -85,11 +89,11 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
     UOp t3;
     XOp t4;
     if (!OPL || wp == 0) {
-      load_slotop<BF, D, GB, true, SPLIT>(t0, c.W, a.G, c.g0, c.sc, i, j);
-      load_slotop<BF, D, GB, false, false>(t1, zm, D, c.g0, 1.0f, i, j, cen);
-      load_slotop<BF, D, GB, false, false>(t2, dU, D, c.g0, 1.0f, i, j, COLN ? nullptr : cen + D);
-      load_gop<BF, GB, VB, false>(t3, dU, D, c.g0, 1.0f, i, j);
-      load_gop<BF, GB, DB, true>(t4, c.W, a.G, c.g0, inv_tau, i, j);
+      load_slotop<BF, D, GB, true, SPLIT>(t0, c.W, a.G, c.g0, slot_lim(a), c.sc, i, j);
+      load_slotop<BF, D, GB, false, false>(t1, zm, D, c.g0, slot_lim(a), 1.0f, i, j, cen);
+      load_slotop<BF, D, GB, false, false>(t2, dU, D, c.g0, slot_lim(a), 1.0f, i, j, COLN ? nullptr : cen + D);
+      load_gop<BF, GB, VB, false>(t3, dU, D, c.g0, slot_lim(a), 1.0f, i, j);
+      load_gop<BF, GB, DB, true>(t4, c.W, a.G, c.g0, slot_lim(a), inv_tau, i, j);
     }
     if constexpr (OPL) {
       uint4* b = opl[ws];
@@ -469,10 +473,13 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
       for (int d = 0; d < DB; ++d)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          pp[(int64_t)(16 * d + 4 * j + r) * a.G + c.g0 + 16 * gb + i] = dW[d][gb][r] * inv_tau;
+          if (c.g0 + 16 * gb + i < a.G)
+            pp[(int64_t)(16 * d + 4 * j + r) * a.G + c.g0 + 16 * gb + i] = dW[d][gb][r] * inv_tau;
       if (i == 0)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) pp[(int64_t)D * a.G + c.g0 + 16 * gb + 4 * j + r] = dbv[gb][r] * inv_tau;
+        for (int r = 0; r < 4; ++r)
+          if (c.g0 + 16 * gb + 4 * j + r < a.G)
+            pp[(int64_t)D * a.G + c.g0 + 16 * gb + 4 * j + r] = dbv[gb][r] * inv_tau;
     }
   }
   if (threadIdx.x == 0) {

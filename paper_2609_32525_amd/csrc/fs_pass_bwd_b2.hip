@@ -51,10 +51,15 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(GS
   for (int gb = 0; gb < GB; ++gb)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int slot = c.g0 + 16 * gb + 4 * j + r;
-      bT[gb][r] = c.sc * c.bias[slot] - (COLN ? a.clse[(int64_t)c.bh * a.G + slot] : 0.f);
-      bTd[gb][r] = scd * bd[slot];
-      dsT[gb][r] = a.ds[(int64_t)c.bh * a.G + slot] - (COLN ? 0.f : cen[2 * D]);
+      // padding blocks (slots >= G) read the last real block and take masked logits, no ds
+      bool real;
+      const int sl = slot_block(c.g0 + 16 * gb, slot_lim(a), real) + 4 * j + r;
+      const float bv = c.sc * c.bias[sl] - (COLN ? a.clse[(int64_t)c.bh * a.G + sl] : 0.f);
+      const float bdv = scd * bd[sl];
+      const float dv = a.ds[(int64_t)c.bh * a.G + sl] - (COLN ? 0.f : cen[2 * D]);
+      bT[gb][r] = slot_mask(real, bv, kMaskedSlot);
+      bTd[gb][r] = slot_mask(real, bdv, kMaskedSlot);
+      dsT[gb][r] = slot_mask(real, dv, 0.f);
     }
 
   // operand images in LDS, shared by the point groups: W_s, W_d (logits), zmix and dU
@@ -63,21 +68,21 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(GS
   __shared__ uint4 opl[4 * kS + kU + 2 * kX];
   if (wp == 0) {
     SOp t;
-    load_slotop<BF, D, GB, true, SPLIT>(t, c.W, a.G, c.g0, c.sc, i, j);
+    load_slotop<BF, D, GB, true, SPLIT>(t, c.W, a.G, c.g0, slot_lim(a), c.sc, i, j);
     lds_put(t, opl, lane);
-    load_slotop<BF, D, GB, true, SPLIT>(t, Wd, a.G, c.g0, scd, i, j);
+    load_slotop<BF, D, GB, true, SPLIT>(t, Wd, a.G, c.g0, slot_lim(a), scd, i, j);
     lds_put(t, opl + kS, lane);
-    load_slotop<BF, D, GB, false, false>(t, zm, D, c.g0, 1.0f, i, j, cen);
+    load_slotop<BF, D, GB, false, false>(t, zm, D, c.g0, slot_lim(a), 1.0f, i, j, cen);
     lds_put(t, opl + 2 * kS, lane);
-    load_slotop<BF, D, GB, false, false>(t, dU, D, c.g0, 1.0f, i, j, COLN ? nullptr : cen + D);
+    load_slotop<BF, D, GB, false, false>(t, dU, D, c.g0, slot_lim(a), 1.0f, i, j, COLN ? nullptr : cen + D);
     lds_put(t, opl + 3 * kS, lane);
     UOp u;
-    load_gop<BF, GB, VB, false>(u, dU, D, c.g0, 1.0f, i, j);
+    load_gop<BF, GB, VB, false>(u, dU, D, c.g0, slot_lim(a), 1.0f, i, j);
     lds_put(u, opl + 4 * kS, lane);
     XOp x;
-    load_gop<BF, GB, DB, true>(x, c.W, a.G, c.g0, inv_tau, i, j);
+    load_gop<BF, GB, DB, true>(x, c.W, a.G, c.g0, slot_lim(a), inv_tau, i, j);
     lds_put(x, opl + 4 * kS + kU, lane);
-    load_gop<BF, GB, DB, true>(x, Wd, a.G, c.g0, inv_taud, i, j);
+    load_gop<BF, GB, DB, true>(x, Wd, a.G, c.g0, slot_lim(a), inv_taud, i, j);
     lds_put(x, opl + 4 * kS + kU + kX, lane);
   }
   __syncthreads();
@@ -340,10 +345,13 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(GS
         for (int d = 0; d < DB; ++d)
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            pp[(int64_t)(16 * d + 4 * j + r) * a.G + c.g0 + 16 * gb + i] = dW[q][d][gb][r] * it;
+            if (c.g0 + 16 * gb + i < a.G)
+              pp[(int64_t)(16 * d + 4 * j + r) * a.G + c.g0 + 16 * gb + i] = dW[q][d][gb][r] * it;
         if (i == 0)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) pp[(int64_t)D * a.G + c.g0 + 16 * gb + 4 * j + r] = dbv[gb][r] * it;
+          for (int r = 0; r < 4; ++r)
+            if (c.g0 + 16 * gb + 4 * j + r < a.G)
+              pp[(int64_t)D * a.G + c.g0 + 16 * gb + 4 * j + r] = dbv[gb][r] * it;
       }
     }
     if (threadIdx.x == 0) {

@@ -18,7 +18,7 @@ namespace {
 // sum over the slot groups, combined across the NS slot waves through LDS) instead of read.
 // =======================================================================================
 template <bool BF, int D, int GS, int NS, int NP, bool ST>
-__global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_DESLICE))) void k_deslice(
+__global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(D <= 32 ? FS_WPE_DESLICE : 1))) void k_deslice(
     PassArgs a) {
   constexpr int GB = GS / 16, VB = D / 16;
   constexpr bool SPLIT = BF;
@@ -33,14 +33,14 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   const bool want_lse = !ST || a.lse_out != nullptr;
 
   SlotOp<BF, D, GB> wop;
-  load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, c.sc, i, j);
+  load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, slot_lim(a), c.sc, i, j);
   float bT[GB][4];
 #pragma unroll
   for (int gb = 0; gb < GB; ++gb)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) bT[gb][r] = c.sc * c.bias[c.g0 + 16 * gb + 4 * j + r];
+    for (int r = 0; r < 4; ++r) bT[gb][r] = slot_bias(c, a, c.g0 + 16 * gb, 4 * j + r);
   GOp<BF, GB, VB> zop;
-  load_gop<BF, GB, VB, false>(zop, a.zmix + (int64_t)c.bh * a.G * D, D, c.g0, 1.0f, i, j);
+  load_gop<BF, GB, VB, false>(zop, a.zmix + (int64_t)c.bh * a.G * D, D, c.g0, slot_lim(a), 1.0f, i, j);
 
   __shared__ f4 ox[NS > 1 ? NP : 1][NS > 1 ? NS : 1][VB][2][64];
   // output staging: one 32-point tile per point group, rows of D values padded by 16 bytes

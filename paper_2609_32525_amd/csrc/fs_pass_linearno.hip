@@ -33,10 +33,10 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice_col(PassArgs a) {
   const T* fb = (const T*)a.fx + c.off;
 
   SlotOp<BF, D, GB> wop;
-  load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, c.sc, i, j);
+  load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, slot_lim(a), c.sc, i, j);
   float bS[GB];
 #pragma unroll
-  for (int gb = 0; gb < GB; ++gb) bS[gb] = c.sc * c.bias[c.g0 + 16 * gb + i];
+  for (int gb = 0; gb < GB; ++gb) bS[gb] = slot_bias(c, a, c.g0 + 16 * gb, i);
 
   // U rows are slots 16 gb + 4 j + r (C layout); mrun, lrun belong to slot column 16 gb + i
   f4 U[GB][VB];
@@ -174,9 +174,11 @@ __global__ __launch_bounds__(64 * NS * NP) void k_slice_col(PassArgs a) {
 #pragma unroll
       for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          pU[(int64_t)(c.g0 + 16 * gb + 4 * j + r) * D + 16 * vb + i] = U[gb][vb][r];
-      if (j == 0) {
+        for (int r = 0; r < 4; ++r) {
+          const int g = c.g0 + 16 * gb + 4 * j + r;
+          if (g < a.G) pU[(int64_t)g * D + 16 * vb + i] = U[gb][vb][r];
+        }
+      if (j == 0 && c.g0 + 16 * gb + i < a.G) {
         pML[c.g0 + 16 * gb + i] = mrun[gb];
         pML[a.G + c.g0 + 16 * gb + i] = lsum[gb];
       }

@@ -83,31 +83,34 @@ __device__ __forceinline__ void build_job(int q, int blk, const HeadCtx& c, cons
     uint4* hb = out + h * IM::kHalf;
     if (kind <= 2) {
       SOp o;
-      if (kind == 0) load_slotop<BF, D, GBH, true, BF>(o, c.W, a.G, gh, c.sc, i, j);
-      if (kind == 1) load_slotop<BF, D, GBH, false, false>(o, zm, D, gh, 1.0f, i, j, cen);
-      if (kind == 2) load_slotop<BF, D, GBH, false, false>(o, dU, D, gh, 1.0f, i, j, cen + D);
+      if (kind == 0) load_slotop<BF, D, GBH, true, BF>(o, c.W, a.G, gh, slot_lim(a), c.sc, i, j);
+      if (kind == 1) load_slotop<BF, D, GBH, false, false>(o, zm, D, gh, slot_lim(a), 1.0f, i, j, cen);
+      if (kind == 2) load_slotop<BF, D, GBH, false, false>(o, dU, D, gh, slot_lim(a), 1.0f, i, j, cen + D);
       if (kind == 0) put_first(o, hb, lane, IM::kW / 64);
       if (kind == 1) put_first(o, hb + IM::kW, lane, IM::kZ / 64);
       if (kind == 2) put_first(o, hb + IM::kW + IM::kZ, lane, IM::kZ / 64);
     } else {
       UOp o;
-      if (kind == 3) load_gop<BF, GBH, VB, false>(o, dU, D, gh, 1.0f, i, j);
-      if (kind == 4) load_gop<BF, GBH, DB, true>(o, c.W, a.G, gh, inv_tau, i, j);
+      if (kind == 3) load_gop<BF, GBH, VB, false>(o, dU, D, gh, slot_lim(a), 1.0f, i, j);
+      if (kind == 4) load_gop<BF, GBH, DB, true>(o, c.W, a.G, gh, slot_lim(a), inv_tau, i, j);
       put_first(o, hb + IM::kW + 2 * IM::kZ + (kind == 4 ? IM::kU : 0), lane, IM::kU / 64);
     }
   } else if (q == 10) {
     float* f = reinterpret_cast<float*>(out + 2 * IM::kHalf);
-    f[lane] = c.sc * c.bias[g0 + lane];
-    f[64 + lane] = dsv[g0 + lane] - cen[2 * D];
+    const bool real = g0 + lane < a.G;  // padding slots: masked logit, no ds
+    const float dv = dsv[min(g0 + lane, a.G - 1)] - cen[2 * D];
+    f[lane] = slot_bias_at(c, a, g0 + lane);
+    f[64 + lane] = slot_mask(real, dv, 0.f);
   }
 }
 
-// Image sets of every slot block of every (b, h), [BH][G / 64][kChunks] uint4: built once per
-// backward so that the point-owned pass only copies them. grid (G / 64) * BH, 11 wavefronts.
+// Image sets of every slot block of every (b, h), [BH][ceil(G / 64)][kChunks] uint4: built once
+// per backward so that the point-owned pass only copies them. grid ceil(G / 64) BH, 11
+// wavefronts.
 template <bool BF, int D>
 __global__ __launch_bounds__(64 * 11) void k_point_images(PassArgs a, uint4* img) {
   using IM = PointImages<BF, D>;
-  const int NB = a.G / 64;
+  const int NB = (a.G + 63) / 64;
   const int blk = blockIdx.x % NB;
   const int bh = blockIdx.x / NB;
   HeadCtx c;
@@ -204,7 +207,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(FS_POIN
   T* dxb = (T*)a.out + c.off;
   T* dfb = (T*)a.out2 + c.off;
   const float* lse = a.lse_in + (int64_t)c.bh * a.N;
-  const int NB = a.G / 64;
+  const int NB = (a.G + 63) / 64;
 
   __shared__ uint4 img[2][IM::kStride];
 
@@ -381,14 +384,14 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(FS_POIN
   const int wave = threadIdx.x >> 6;
   const int wpu = __builtin_amdgcn_readfirstlane(wave);
   const HeadCtx c = head_ctx<D>(a, 0, 0);
-  const int NB = a.G / 64;
+  const int NB = (a.G + 63) / 64;
   float* bS = reinterpret_cast<float*>(simg + kMaxBlk * kB);
   for (int blk = wave; blk < NB; blk += NW) {
     SOp o;
-    load_slotop<BF, D, 4, true, BF>(o, c.W, a.G, 64 * blk, c.sc, i, j);
+    load_slotop<BF, D, 4, true, BF>(o, c.W, a.G, 64 * blk, slot_lim(a), c.sc, i, j);
     lds_put(o, simg + blk * kB, lane);
   }
-  for (int g = threadIdx.x; g < a.G; g += 64 * NW) bS[g] = c.sc * c.bias[g];
+  for (int g = threadIdx.x; g < 64 * NB; g += 64 * NW) bS[g] = slot_bias_at(c, a, g);
   __syncthreads();
 
   const int64_t rs = (int64_t)a.H * D;
@@ -448,13 +451,12 @@ size_t point_image_bytes(const Geom& g) {
   if (g.D > 32) return 0;
   const int ch = g.bf16 ? (g.D == 16 ? PointImages<true, 16>::kStride : PointImages<true, 32>::kStride)
                         : (g.D == 16 ? PointImages<false, 16>::kStride : PointImages<false, 32>::kStride);
-  return (size_t)g.BH() * (g.G / 64) * ch * 16;
+  return (size_t)g.BH() * ((g.G + 63) / 64) * ch * 16;
 }
 
 hipError_t run_pass_stats_pt(const Geom& g, const PassArgs& a, hipStream_t st) {
   const PassCfg cfg = pick_cfg(g, PASS_POINT);
-  if (cfg.NP != FS_POINT_WAVES || g.D > 32 || g.G > 1024 || g.G % 64 != 0)
-    return hipErrorInvalidConfiguration;
+  if (cfg.NP != FS_POINT_WAVES || g.D > 32 || g.G > 1024) return hipErrorInvalidConfiguration;
   const dim3 grid(cfg.chunks * g.BH()), block(64 * FS_POINT_WAVES);
 #define FS_STATS(BF_, D_)                                                              \
   {                                                                                    \
@@ -473,7 +475,7 @@ hipError_t run_pass_point(const Geom& g, const PassArgs& a, hipStream_t st) {
   const PassCfg cfg = pick_cfg(g, PASS_POINT);
   if (cfg.NP != FS_POINT_WAVES || g.D > 32) return hipErrorInvalidConfiguration;
   uint4* img = static_cast<uint4*>(const_cast<void*>(a.img));
-  const dim3 igrid((g.G / 64) * g.BH()), iblock(64 * 11);
+  const dim3 igrid(((g.G + 63) / 64) * g.BH()), iblock(64 * 11);
   const dim3 grid(cfg.chunks * g.BH()), block(64 * FS_POINT_WAVES);
 #define FS_POINT(BF_, D_)                                                                \
   {                                                                                      \

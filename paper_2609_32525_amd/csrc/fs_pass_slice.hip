@@ -33,10 +33,10 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
   const T* fb = (const T*)a.fx + c.off;
 
   SlotOp<BF, D, GB> wop;
-  load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, c.sc, i, j);
+  load_slotop<BF, D, GB, true, SPLIT>(wop, c.W, a.G, c.g0, slot_lim(a), c.sc, i, j);
   float bS[GB];
 #pragma unroll
-  for (int gb = 0; gb < GB; ++gb) bS[gb] = c.sc * c.bias[c.g0 + 16 * gb + i];
+  for (int gb = 0; gb < GB; ++gb) bS[gb] = slot_bias(c, a, c.g0 + 16 * gb, i);
 
   f4 U[GB][VB];
   float sacc[GB];
@@ -249,9 +249,11 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
       for (int vb = 0; vb < VB; ++vb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          pU[(int64_t)(c.g0 + 16 * gb + 4 * j + r) * D + 16 * vb + i] = U[gb][vb][r];
-      if (j == 0) pS[c.g0 + 16 * gb + i] = sacc[gb];
+        for (int r = 0; r < 4; ++r) {
+          const int g = c.g0 + 16 * gb + 4 * j + r;
+          if (g < a.G) pU[(int64_t)g * D + 16 * vb + i] = U[gb][vb][r];
+        }
+      if (j == 0 && c.g0 + 16 * gb + i < a.G) pS[c.g0 + 16 * gb + i] = sacc[gb];
     }
   }
 }

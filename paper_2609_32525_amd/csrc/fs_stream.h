@@ -45,6 +45,10 @@ typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kMasked = 1.0e30f;  // base-2 lse of padding points: exp2(a - kMasked) == 0
+// Base-2 logit of a padding slot (slot counts that are not a whole number of 16-slot tiles per
+// wave are padded up): its weight exp2(kMaskedSlot - m) is exactly 0 and, being finite, it
+// leaves every product with a zero weight or gradient at zero.
+constexpr float kMaskedSlot = -1.0e30f;
 
 __device__ __forceinline__ f4 mfma_f32(float a, float b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -335,22 +339,47 @@ struct SlotOp<true, D, GB> {
   bf8 lo[GB][K];
 };
 
+// Slot limit of the guarded slot reads: the real slot count G when the tiling pads the slots,
+// else kNoPad (every slot real). G is a multiple of 16 and slot groups start at multiples of
+// 16, so every 16-slot block is wholly real or wholly padding: a padding block reads the last
+// real block (slots glim - 16 ..) scaled by zero. The block choice is wave-uniform and the
+// guard arithmetic, never a branch: with a branch around the loads (or between guarded and
+// plain reads) the compiler waited on each load separately, or moved the buffer descriptors
+// of the streaming loops to vector registers; with per-lane clamped indices it spent more
+// registers on addresses.
+constexpr int kNoPad = 0x7fffffff;
+
+// First slot to read for the 16-slot block starting at gblk (itself if real, else the last
+// real block), and whether it is real.
+__device__ __forceinline__ int slot_block(int gblk, int glim, bool& real) {
+  real = gblk < glim;
+  return real ? gblk : glim - 16;
+}
+
+// v where the slot is real, else pad (v finite), as one multiply-add.
+__device__ __forceinline__ float slot_mask(bool real, float v, float pad) {
+  return fmaf(v, real ? 1.f : 0.f, real ? 0.f : pad);
+}
+
 // TRANSPOSED = true: element (g, k) read from src[k * ld + g] (W_s (D,G)); else
 // src[g * ld + k] - cen[k] (cen nullable: a per-column shift removed before rounding).
+// Slots g >= glim (padding) are zero.
 template <bool BF, int D, int GB, bool TRANSPOSED, bool SPLIT>
 __device__ __forceinline__ void load_slotop(SlotOp<BF, D, GB>& o, const float* src, int ld,
-                                            int g0, float sc, int i, int j,
+                                            int g0, int glim, float sc, int i, int j,
                                             const float* cen = nullptr) {
-  auto M = [&](int g, int k) -> float {
-    if (TRANSPOSED) return sc * src[(int64_t)k * ld + g];
-    return sc * (src[(int64_t)g * ld + k] - (cen != nullptr ? cen[k] : 0.f));
+  auto M = [&](int g, int k, float s) -> float {
+    if (TRANSPOSED) return s * src[(int64_t)k * ld + g];
+    return s * (src[(int64_t)g * ld + k] - (cen != nullptr ? cen[k] : 0.f));
   };
 #pragma unroll
   for (int gb = 0; gb < GB; ++gb) {
-    const int g = g0 + 16 * gb + i;
+    bool real;
+    const int gc = slot_block(g0 + 16 * gb, glim, real) + i;
+    const float s = real ? sc : 0.f;
     if constexpr (!BF) {
 #pragma unroll
-      for (int kk = 0; kk < D / 4; ++kk) o.v[gb][kk] = M(g, kcol_f<D>(j, kk));
+      for (int kk = 0; kk < D / 4; ++kk) o.v[gb][kk] = M(gc, kcol_f<D>(j, kk), s);
     } else {
 #pragma unroll
       for (int kk = 0; kk < SlotOp<true, D, GB>::K; ++kk) {
@@ -359,7 +388,7 @@ __device__ __forceinline__ void load_slotop(SlotOp<BF, D, GB>& o, const float* s
         for (int e = 0; e < 8; ++e) {
           const int k = kcol_bf<D>(j, kk, e);
           float val = 0.f;
-          if (k >= 0) val = M(g, k);
+          if (k >= 0) val = M(gc, k, s);
           const __bf16 h = (__bf16)val;
           hi[e] = h;
           lo[e] = SPLIT ? (__bf16)(val - (float)h) : (__bf16)0.f;
@@ -422,12 +451,18 @@ struct GOp<true, GB, CB> {
   bf8 v[GB / 2][CB];
 };
 
-// TRANSPOSED = true: M(g, c) = src[c * ld + g] * sc, else src[g * ld + c] * sc.
+// TRANSPOSED = true: M(g, c) = src[c * ld + g] * sc, else src[g * ld + c] * sc; zero for
+// the padding slots g >= glim.
 template <bool BF, int GB, int CB, bool TRANSPOSED>
 __device__ __forceinline__ void load_gop(GOp<BF, GB, CB>& o, const float* src, int ld, int g0,
-                                         float sc, int i, int j) {
-  auto M = [&](int g, int c) -> float {
-    return sc * (TRANSPOSED ? src[(int64_t)c * ld + g] : src[(int64_t)g * ld + c]);
+                                         int glim, float sc, int i, int j) {
+  // element (16-slot block gblk, slot offset go within it, column c); padding blocks read the
+  // last real block scaled by zero (see kNoPad)
+  auto M = [&](int gblk, int go, int c) -> float {
+    bool real;
+    const int gc = slot_block(gblk, glim, real) + go;
+    const float s = real ? sc : 0.f;
+    return s * (TRANSPOSED ? src[(int64_t)c * ld + gc] : src[(int64_t)gc * ld + c]);
   };
   if constexpr (!BF) {
 #pragma unroll
@@ -435,7 +470,7 @@ __device__ __forceinline__ void load_gop(GOp<BF, GB, CB>& o, const float* src, i
 #pragma unroll
       for (int r = 0; r < 4; ++r)
 #pragma unroll
-        for (int cb = 0; cb < CB; ++cb) o.v[gb][r][cb] = M(g0 + 16 * gb + 4 * j + r, 16 * cb + i);
+        for (int cb = 0; cb < CB; ++cb) o.v[gb][r][cb] = M(g0 + 16 * gb, 4 * j + r, 16 * cb + i);
   } else {
 #pragma unroll
     for (int q = 0; q < GB / 2; ++q)
@@ -444,7 +479,7 @@ __device__ __forceinline__ void load_gop(GOp<BF, GB, CB>& o, const float* src, i
         bf8 t;
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-          t[e] = (__bf16)M(g0 + 32 * q + 16 * (e / 4) + 4 * j + (e % 4), 16 * cb + i);
+          t[e] = (__bf16)M(g0 + 32 * q + 16 * (e / 4), 4 * j + (e % 4), 16 * cb + i);
         o.v[q][cb] = t;
       }
   }
@@ -721,6 +756,7 @@ __device__ __forceinline__ void pipeline(int ntile, Load&& load, Body&& body) {
 #ifndef FS_WPE_SLICE
 #define FS_WPE_SLICE 1
 #endif
+// The deslice's target applies up to head width 32 (64 would spill at three).
 #ifndef FS_WPE_DESLICE
 #define FS_WPE_DESLICE 1
 #endif
@@ -798,12 +834,28 @@ __device__ __forceinline__ HeadCtx head_ctx(const PassArgs& a, int ws, int GS) {
   c.bh = bp.bh;
   c.b = c.bh / a.H;
   c.h = c.bh % a.H;
-  c.g0 = (bp.blk + ws) * GS;  // nblk > 1 only with one slot group per tile
+  // nblk > 1 only with one slot group per tile; ws is the wave's slot-group index (the same in
+  // every lane: it comes from the wave number)
+  c.g0 = (bp.blk + __builtin_amdgcn_readfirstlane(ws)) * GS;
   c.sc = kLog2e / a.tau[c.h];
   c.W = a.Ws + (a.ws_per_head ? (int64_t)c.h * D * a.G : 0);
   c.bias = a.bias + (a.ws_per_head ? (int64_t)c.h * a.G : 0);
   c.off = ((int64_t)c.b * a.N * a.H + c.h) * D;
   return c;
+}
+
+// Slot limit for the operand loaders (see kNoPad).
+__device__ __forceinline__ int slot_lim(const PassArgs& a) { return a.padded ? a.G : kNoPad; }
+
+// Scaled base-2 bias of slot gblk + go of the 16-slot block gblk (kMaskedSlot for padding).
+__device__ __forceinline__ float slot_bias(const HeadCtx& c, const PassArgs& a, int gblk, int go) {
+  bool real;
+  const int gc = slot_block(gblk, slot_lim(a), real) + go;
+  return slot_mask(real, c.sc * c.bias[gc], kMaskedSlot);
+}
+// The same for any slot g (per-lane block choice; for one-time set-up loops).
+__device__ __forceinline__ float slot_bias_at(const HeadCtx& c, const PassArgs& a, int g) {
+  return slot_bias(c, a, g & ~15, g & 15);
 }
 
 // =======================================================================================

@@ -50,7 +50,8 @@ int main(void) {
   bad = p; bad.N = -1;                  EXPECT(fs_workspace_bytes(&bad, 0, &wsf), FS_ERR_SHAPE);
   bad = p; bad.dtype = 9;               EXPECT(fs_workspace_bytes(&bad, 0, &wsf), FS_ERR_DTYPE);
   bad = p; bad.eps = -1.f;              EXPECT(fs_workspace_bytes(&bad, 0, &wsf), FS_ERR_ARG);
-  bad = p; bad.G = 48;                  EXPECT(fs_workspace_bytes(&bad, 0, &wsf), FS_ERR_UNSUPPORTED);
+  bad = p; bad.G = 40;                  EXPECT(fs_workspace_bytes(&bad, 0, &wsf), FS_ERR_UNSUPPORTED);
+  { size_t w48; bad = p; bad.G = 48;    EXPECT(fs_workspace_bytes(&bad, 0, &w48), FS_OK); }
   bad = p; bad.D = 32; bad.V = 16;      EXPECT(fs_workspace_bytes(&bad, 0, &wsf), FS_ERR_UNSUPPORTED);
   bad = p; bad.ws_per_head = 2;         EXPECT(fs_workspace_bytes(&bad, 0, &wsf), FS_ERR_ARG);
 

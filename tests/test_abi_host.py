@@ -111,11 +111,20 @@ def test_workspace_formula_bounded():
     assert a == b
 
 
+@pytest.mark.parametrize("G,dt", [(16, 1), (48, 0), (48, 1), (80, 1), (144, 0), (336, 1),
+                                  (1008, 1)])
+def test_multiple_of_16_slot_counts_accepted(G, dt):
+    # slot counts between the tile sizes are padded up by the kernels, not refused
+    for bwd in (0, 1):
+        st, n = ws_bytes(prob(N=4096, G=G, dtype=dt), bwd)
+        assert st == OK and n > 0, (G, dt, bwd, st)
+
+
 @pytest.mark.parametrize("kw,code", [
     (dict(B=0), SHAPE), (dict(N=-1), SHAPE), (dict(H=0), SHAPE), (dict(G=0), SHAPE),
     (dict(dtype=7), DTYPE), (dict(eps=-1.0), ARG), (dict(eps=float("nan")), ARG),
     (dict(per_head=3), ARG), (dict(D=24, V=24), UNSUP), (dict(D=32, V=16), UNSUP),
-    (dict(G=48), UNSUP), (dict(G=2048), UNSUP), (dict(G=16, dtype=1), UNSUP),
+    (dict(G=40), UNSUP), (dict(G=2048), UNSUP), (dict(G=1040), UNSUP),
     (dict(G=8), UNSUP), (dict(B=70000), UNSUP),
 ])
 def test_problem_validation(kw, code):

@@ -50,6 +50,10 @@ CASES = [
     # one-tile-plus-one point sets (ragged tails only)
     case("bf16_D32_G64_linc_N33", "bf16", 32, 64, O.MIX_LINEAR_C, N=33),
     case("f32_D32_G256_linc_N33", "f32", 32, 256, O.MIX_LINEAR_C, N=33, H=2),
+    # padded tilings: one wave (48), two waves (80), four waves with a partial one (208)
+    case("f32_D32_G48_linc", "f32", 32, 48, O.MIX_LINEAR_C),
+    case("bf16_D32_G80_linc", "bf16", 32, 80, O.MIX_LINEAR_C, N=900),
+    case("f32_D32_G208_linc", "f32", 32, 208, O.MIX_LINEAR_C, N=600, H=2),
 ]
 
 

@@ -95,6 +95,21 @@ SMALL = [
     # attention over large token sets inside the whole path
     small("f32_D32_G1024_attn", "f32", 32, 1024, O.MIX_ATTN, N=600, H=2, B=1),
     small("bf16_D64_G512_attn", "bf16", 64, 512, O.MIX_ATTN, N=600, H=2),
+    # slot counts between the tile sizes (padded tilings): one padded wave (G = 16 in bf16,
+    # 48), two slot waves (80, 112), slot blocks with a partial last block (144, 336, 1008),
+    # cooperative waves with no real slot at all (272 and 336 run on 8 slot waves)
+    small("bf16_D32_G16_lin", "bf16", 32, 16, O.MIX_LINEAR_G, N=777),
+    small("f32_D32_G48_attn", "f32", 32, 48, O.MIX_ATTN),
+    small("bf16_D32_G48_lin", "bf16", 32, 48, O.MIX_LINEAR_G, N=1031),
+    small("f32_D16_G80_linc", "f32", 16, 80, O.MIX_LINEAR_C),
+    small("bf16_D64_G112_attn", "bf16", 64, 112, O.MIX_ATTN, N=900),
+    small("bf16_D32_G144_lin", "bf16", 32, 144, O.MIX_LINEAR_G, tau_mode="uniform",
+          ws_mode="std3", N=900),
+    small("f32_D32_G336_attn", "f32", 32, 336, O.MIX_ATTN, N=700, H=2),
+    small("bf16_D64_G272_lin", "bf16", 64, 272, O.MIX_LINEAR_G, N=600, H=2),
+    small("bf16_D32_G1008_lin", "bf16", 32, 1008, O.MIX_LINEAR_G, tau_mode="uniform",
+          ws_mode="std3", N=700, H=2, B=1),
+    small("f32_D32_G48_lin_N33", "f32", 32, 48, O.MIX_LINEAR_G, N=33),
 ]
 
 
@@ -337,6 +352,10 @@ MIX_CASES = [
     # attention over large token sets (the row-block forward and the batched-product backward)
     ("attention", O.MIX_ATTN, 512, False), ("attention", O.MIX_ATTN, 1024, False),
     ("attention_v64", O.MIX_ATTN, 256, False, 64), ("attention_v16", O.MIX_ATTN, 1024, False, 16),
+    # token counts that are multiples of 16 but not of 64
+    ("fixed", O.MIX_LINEAR_G, 48, False), ("channel", O.MIX_LINEAR_C, 336, False),
+    ("attention", O.MIX_ATTN, 48, False), ("attention", O.MIX_ATTN, 80, False),
+    ("attention", O.MIX_ATTN, 336, False),
 ]
 
 

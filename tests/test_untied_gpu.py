@@ -46,6 +46,10 @@ CASES = [
     case("f32_D32_G32_lin_N1", "f32", 32, 32, O.MIX_LINEAR_G, N=1),
     case("bf16_D32_G64_linc_N33", "bf16", 32, 64, O.MIX_LINEAR_C, N=33),
     case("f32_D32_G256_lin_N33", "f32", 32, 256, O.MIX_LINEAR_G, N=33, H=2),
+    # padded tilings: one wave (48), two waves (80), 8 waves of which 3 hold no real slot (272)
+    case("f32_D32_G48_lin", "f32", 32, 48, O.MIX_LINEAR_G),
+    case("bf16_D32_G80_attn", "bf16", 32, 80, O.MIX_ATTN, N=900),
+    case("f32_D32_G272_lin", "f32", 32, 272, O.MIX_LINEAR_G, N=600, H=2),
 ]
 
 
