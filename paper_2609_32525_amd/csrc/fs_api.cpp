@@ -60,7 +60,7 @@ PassEvents& pass_events() {
   return ev;
 }
 
-bool blocked(const Geom& g) { return !g.untied && g.G > FS_BLOCKED_MIN_G && g.D <= 32; }
+bool blocked(const Geom& g) { return g.G > FS_BLOCKED_MIN_G && g.D <= 32; }
 
 PassCfg pick_cfg(const Geom& g, Pass pass) {
   PassCfg c{};

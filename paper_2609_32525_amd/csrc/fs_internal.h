@@ -35,8 +35,9 @@ enum Pass {
 // Slot-blocked family (large G): the slice, backward pass A and the parameter half of
 // backward pass B run slot-owned (a workgroup owns one block of 64 slots and streams its
 // chunk of points), with the per-point softmax statistics from a statistics pass and the
-// per-point correction c = sum_g w dw from a point-owned pass that also writes dx and dfx.
-// Below the threshold every pass is one kernel whose wavefronts split the slots of a tile.
+// per-point correction c = sum_g w dw from a point-owned pass that also writes dx and dfx
+// (once per weight set for the untied variant and LinearNO). Head widths up to 32. Below the
+// threshold every pass is one kernel whose wavefronts split the slots of a tile.
 bool blocked(const Geom& g);
 // Wavefronts per workgroup of the point-owned pass, and the range of resident wavefronts per
 // SIMD it is compiled for (the minimum caps its registers). Twelve wavefronts with three per
@@ -127,11 +128,13 @@ hipError_t run_pass_bwd_b(const Geom& g, const PassArgs& a, hipStream_t st);
 // (dx, dfx and per-point (c, tb)), slot-owned parameter half of backward pass B.
 hipError_t run_pass_stats(const Geom& g, const PassArgs& a, hipStream_t st);
 hipError_t run_pass_slice_blk(const Geom& g, const PassArgs& a, hipStream_t st);
-hipError_t run_pass_point(const Geom& g, const PassArgs& a, hipStream_t st);
+// role: 0 tied; 1 / 2 the untied slice / deslice weights; 3 LinearNO's slice weights (the
+// same roles as run_pass_bwd_b_untied).
+hipError_t run_pass_point(const Geom& g, const PassArgs& a, int role, hipStream_t st);
 // point-owned statistics pass of the slot-blocked family (lse only; chunks of PASS_POINT)
 hipError_t run_pass_stats_pt(const Geom& g, const PassArgs& a, hipStream_t st);
 size_t point_image_bytes(const Geom& g);  // workspace of the point-owned pass's operand images
-hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, hipStream_t st);
+hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, int role, hipStream_t st);
 // Untied variant, backward pass B in two parts: role 1 the slice weights (writes dx, dfx),
 // role 2 the deslice weights (adds to dx); each writes its own parameter partials.
 hipError_t run_pass_bwd_b_untied(const Geom& g, const PassArgs& a, int role, hipStream_t st);

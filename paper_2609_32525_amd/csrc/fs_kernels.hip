@@ -188,6 +188,29 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
   b.cen = cen;
   b.lse_in = lse;
   b.part = partP;
+  // slot-blocked family: the point-owned pass (dx, dfx, per-point c and tb) with the operand
+  // images of one weight set, ahead of its slot-owned parameter pass
+  float* cpt = reinterpret_cast<float*>(ws + L.cpt);
+  auto point_args = [&](const PassArgs& w) {
+    PassArgs pa = base_args(g, PASS_POINT);
+    pa.x = x;
+    pa.fx = fx;
+    pa.dout = dout;
+    pa.out = dx;
+    pa.out2 = dfx;
+    pa.Ws = w.Ws;
+    pa.bias = w.bias;
+    pa.tau = w.tau;
+    pa.zmix = zmix;
+    pa.dU = dU;
+    pa.ds = dsv;
+    pa.cen = cen;
+    pa.lse_in = w.lse_in;
+    pa.clse = w.clse;
+    pa.cpt_out = cpt;
+    pa.img = ws + L.img;
+    return pa;
+  };
   if (u != nullptr) {
     // untied: the slice weights' part writes dx and dfx; the deslice weights' part (own
     // projection, bias, temperature and normaliser) adds its dx contribution
@@ -198,7 +221,19 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
     b2.lse_in = u->lse_d;
     b2.part = reinterpret_cast<float*>(ws + L.partP2);
     b.clse = clse;
-    if (fused_untied_bwd_b(g)) {
+    const int role1 = clse != nullptr ? 3 : 1;
+    if (blocked(g)) {
+      // each weight set: point-owned pass, then its parameter pass (they share the images
+      // and the per-point (c, tb) buffer, in stream order)
+      const PassArgs p1 = point_args(b), p2 = point_args(b2);
+      b.cpt = b2.cpt = cpt;
+      e = timed(PASS_BWD_B, st, [&] {
+        hipError_t e1 = run_pass_point(g, p1, role1, st);
+        if (e1 == hipSuccess) e1 = run_pass_bwd_params(g, b, role1, st);
+        if (e1 == hipSuccess) e1 = run_pass_point(g, p2, 2, st);
+        return e1 != hipSuccess ? e1 : run_pass_bwd_params(g, b2, 2, st);
+      });
+    } else if (fused_untied_bwd_b(g)) {
       // both weight sets per tile in one kernel: X read once, dx written once
       b.Wd = u->Wd;
       b.bd = u->bd;
@@ -208,7 +243,7 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
       e = timed(PASS_BWD_B, st, [&] { return run_pass_bwd_b2(g, b, clse != nullptr, st); });
     } else {
       e = timed(PASS_BWD_B, st, [&] {
-        hipError_t e1 = run_pass_bwd_b_untied(g, b, clse != nullptr ? 3 : 1, st);
+        hipError_t e1 = run_pass_bwd_b_untied(g, b, role1, st);
         return e1 != hipSuccess ? e1 : run_pass_bwd_b_untied(g, b2, 2, st);
       });
     }
@@ -220,26 +255,11 @@ hipError_t launch_bwd(const Geom& g, const MixArgs& m, const void* x, const void
   }
   if (blocked(g)) {
     // point-owned pass (dx, dfx, per-point c and tb), then the slot-owned parameter pass
-    PassArgs pa = base_args(g, PASS_POINT);
-    pa.x = x;
-    pa.fx = fx;
-    pa.dout = dout;
-    pa.out = dx;
-    pa.out2 = dfx;
-    pa.Ws = Ws;
-    pa.bias = bias;
-    pa.tau = tau;
-    pa.zmix = zmix;
-    pa.dU = dU;
-    pa.ds = dsv;
-    pa.cen = cen;
-    pa.lse_in = lse;
-    pa.cpt_out = reinterpret_cast<float*>(ws + L.cpt);
-    pa.img = ws + L.img;
-    b.cpt = pa.cpt_out;
+    const PassArgs pa = point_args(b);
+    b.cpt = cpt;
     e = timed(PASS_BWD_B, st, [&] {
-      hipError_t e1 = run_pass_point(g, pa, st);
-      return e1 != hipSuccess ? e1 : run_pass_bwd_params(g, b, st);
+      hipError_t e1 = run_pass_point(g, pa, 0, st);
+      return e1 != hipSuccess ? e1 : run_pass_bwd_params(g, b, 0, st);
     });
   } else {
     e = timed(PASS_BWD_B, st, [&] { return run_pass_bwd_b(g, b, st); });

@@ -33,7 +33,7 @@ template <bool BF, int D, int GS, int NS, int NP, int PB, bool PM, int ROLE>
 __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM ? FS_WPE_BWD_PM : BF ? FS_WPE_BWD_B : FS_WPE_BWD_B_F32))) void k_bwd_b(
     PassArgs a) {
   static_assert(PB == 2 || !BF, "bf16 contracts over 32 points");
-  static_assert(!PM || ROLE == 0, "the untied parts are point-and-parameter kernels");
+  static_assert(!PM || (GS == 64 && NS == 1), "the parameter pass owns one 64-slot block");
   constexpr bool USE_DOUT = ROLE == 0 || ROLE == 2, USE_FX = ROLE != 2;
   constexpr bool COLN = ROLE == 3;  // weights normalised over the points of each slot
   constexpr int GB = GS / 16, VB = D / 16, DB = D / 16, TP = 16 * PB;
@@ -496,7 +496,9 @@ struct Run_k_bwd_b_ {
   template <bool BF, int D, int GS, int NS, int NP, int PB>
   struct R {
     static hipError_t run(const PassCfg& cfg, int BH, const PassArgs& a, hipStream_t st) {
-      if constexpr (PM && NS != 1) {  // the parameter half of the blocked family is slot-owned
+      // the parameter half of the blocked family is slot-owned: 64-slot blocks (head width up
+      // to 32 for the roles other than 0)
+      if constexpr (PM && (NS != 1 || GS != 64 || (ROLE != 0 && D > 32))) {
         return hipErrorInvalidConfiguration;
       } else {
         dim3 grid(cfg.chunks * BH * cfg.nblk);
@@ -514,8 +516,14 @@ hipError_t run_pass_bwd_b(const Geom& g, const PassArgs& a, hipStream_t st) {
   return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<false, 0>::R>(g, a, st);
 }
 
-hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, hipStream_t st) {
-  return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<true, 0>::R>(g, a, st);
+hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, int role, hipStream_t st) {
+  switch (role) {
+    case 0: return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<true, 0>::R>(g, a, st);
+    case 1: return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<true, 1>::R>(g, a, st);
+    case 2: return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<true, 2>::R>(g, a, st);
+    case 3: return run_pass_tilings<PASS_BWD_B, Run_k_bwd_b_<true, 3>::R>(g, a, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t run_pass_bwd_b_untied(const Geom& g, const PassArgs& a, int role, hipStream_t st) {

@@ -8,6 +8,11 @@
 // The last identity lets dx be accumulated in the same sweep over the slot blocks, before c
 // is known (paper: App. F.1, "G-blocked kernels": a point-owned backward kernel; here one
 // sweep instead of two). The slot-owned parameter pass then reads (c, tb) per point.
+// ROLE (as in the fused pass B): 0 tied; 1 the untied slice weights (dw = F dU^T + ds; dx and
+// dfx written); 2 the untied deslice weights (dw = dout zmix^T, no ds; their dx part added to
+// the dx role 1 wrote; no dfx); 3 LinearNO's slice weights (weights 2^(a - clse_g), already
+// normalised over the points, so no per-point normaliser and no correction: c = 0, dx = P;
+// dw = F dz^T + ds with no slot-mean shifts).
 //
 // The per-head operands (W_s, zmix, dU, bias, ds) are far too large at large G to stay in
 // registers, so each block's MFMA operand images are built once per workgroup in LDS, double
@@ -64,9 +69,12 @@ __device__ __forceinline__ void get_first(Op& o, const uint4* base, int lane, in
 // LDS, same layout): jobs 0..9 are (half h = q / 5, kind q % 5) with kinds W (logits, scaled by
 // log2(e)/tau), zv and uv (centred zmix and dU for dw), ug (dU for dfx), wg (W^T / tau for P
 // and Q); job 10 is the block's scaled bias and centred ds. Called by a whole wavefront.
-template <bool BF, int D>
+template <bool BF, int D, int ROLE>
 __device__ __forceinline__ void build_job(int q, int blk, const HeadCtx& c, const PassArgs& a,
                                           uint4* out, int lane) {
+  constexpr bool ZV = ROLE == 0 || ROLE == 2;  // dw has the dout zmix^T term
+  constexpr bool UV = ROLE != 2;               // dw has the F dU^T term (and dfx is written)
+  constexpr bool SHIFT = ROLE != 3;            // slot-mean shifts of the dw operands
   using IM = PointImages<BF, D>;
   using SOp = typename IM::SOp;
   using UOp = typename IM::UOp;
@@ -83,13 +91,18 @@ __device__ __forceinline__ void build_job(int q, int blk, const HeadCtx& c, cons
     uint4* hb = out + h * IM::kHalf;
     if (kind <= 2) {
       SOp o;
+      if (kind == 1 && !ZV) return;  // images the role does not read
+      if (kind == 2 && !UV) return;
       if (kind == 0) load_slotop<BF, D, GBH, true, BF>(o, c.W, a.G, gh, slot_lim(a), c.sc, i, j);
       if (kind == 1) load_slotop<BF, D, GBH, false, false>(o, zm, D, gh, slot_lim(a), 1.0f, i, j, cen);
-      if (kind == 2) load_slotop<BF, D, GBH, false, false>(o, dU, D, gh, slot_lim(a), 1.0f, i, j, cen + D);
+      if (kind == 2)
+        load_slotop<BF, D, GBH, false, false>(o, dU, D, gh, slot_lim(a), 1.0f, i, j,
+                                              SHIFT ? cen + D : nullptr);
       if (kind == 0) put_first(o, hb, lane, IM::kW / 64);
       if (kind == 1) put_first(o, hb + IM::kW, lane, IM::kZ / 64);
       if (kind == 2) put_first(o, hb + IM::kW + IM::kZ, lane, IM::kZ / 64);
     } else {
+      if (kind == 3 && !UV) return;
       UOp o;
       if (kind == 3) load_gop<BF, GBH, VB, false>(o, dU, D, gh, slot_lim(a), 1.0f, i, j);
       if (kind == 4) load_gop<BF, GBH, DB, true>(o, c.W, a.G, gh, slot_lim(a), inv_tau, i, j);
@@ -98,16 +111,19 @@ __device__ __forceinline__ void build_job(int q, int blk, const HeadCtx& c, cons
   } else if (q == 10) {
     float* f = reinterpret_cast<float*>(out + 2 * IM::kHalf);
     const bool real = g0 + lane < a.G;  // padding slots: masked logit, no ds
-    const float dv = dsv[min(g0 + lane, a.G - 1)] - cen[2 * D];
-    f[lane] = slot_bias_at(c, a, g0 + lane);
-    f[64 + lane] = slot_mask(real, dv, 0.f);
+    const int gl = min(g0 + lane, a.G - 1);
+    const float dv = dsv[gl] - (SHIFT ? cen[2 * D] : 0.f);
+    // LinearNO: the weights' per-slot normaliser over the points enters as a bias shift
+    const float cl = ROLE == 3 ? a.clse[(int64_t)c.bh * a.G + gl] : 0.f;
+    f[lane] = slot_bias_at(c, a, g0 + lane) - slot_mask(real, cl, 0.f);
+    f[64 + lane] = ROLE == 2 ? 0.f : slot_mask(real, dv, 0.f);
   }
 }
 
 // Image sets of every slot block of every (b, h), [BH][ceil(G / 64)][kChunks] uint4: built once
 // per backward so that the point-owned pass only copies them. grid ceil(G / 64) BH, 11
 // wavefronts.
-template <bool BF, int D>
+template <bool BF, int D, int ROLE>
 __global__ __launch_bounds__(64 * 11) void k_point_images(PassArgs a, uint4* img) {
   using IM = PointImages<BF, D>;
   const int NB = (a.G + 63) / 64;
@@ -120,8 +136,8 @@ __global__ __launch_bounds__(64 * 11) void k_point_images(PassArgs a, uint4* img
   c.sc = kLog2e / a.tau[c.h];
   c.W = a.Ws + (a.ws_per_head ? (int64_t)c.h * D * a.G : 0);
   c.bias = a.bias + (a.ws_per_head ? (int64_t)c.h * a.G : 0);
-  build_job<BF, D>(threadIdx.x >> 6, blk, c, a, img + ((int64_t)bh * NB + blk) * IM::kStride,
-                   threadIdx.x & 63);
+  build_job<BF, D, ROLE>(threadIdx.x >> 6, blk, c, a, img + ((int64_t)bh * NB + blk) * IM::kStride,
+                         threadIdx.x & 63);
 }
 
 // A thread's share of one block's image set on its way from global memory to LDS: chunks
@@ -187,9 +203,12 @@ __device__ __forceinline__ f4 mm_split_b(const GOp<BF, GBH, CB>& o, int cb, cons
   }
 }
 
-template <bool BF, int D, int NW>
+template <bool BF, int D, int NW, int ROLE>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(FS_POINT_WPE_MIN, FS_POINT_WPE))) void k_point(
     PassArgs a) {
+  constexpr bool ZV = ROLE == 0 || ROLE == 2;  // dw = dout zmix^T + ...
+  constexpr bool UV = ROLE != 2;               // dw = ... + F dU^T; dfx = w dU
+  constexpr bool COLN = ROLE == 3;             // no per-point normaliser or correction
   using IM = PointImages<BF, D>;
   using SOp = typename IM::SOp;
   using UOp = typename IM::UOp;
@@ -244,9 +263,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(FS_POIN
     for (int pb = 0; pb < 2; ++pb) {
       const int so = (tp0 + 16 * pb) * rsb;
       load_row_buf<BF, D>(xo[pb], rx, i * rsb, so, j);
-      load_row_buf<BF, D>(go[pb], rg, i * rsb, so, j);
-      load_row_buf<BF, D>(fo[pb], rf, i * rsb, so, j);
-      const float l = bld32(rl, 4 * i, 4 * (tp0 + 16 * pb));
+      if constexpr (ZV) load_row_buf<BF, D>(go[pb], rg, i * rsb, so, j);
+      if constexpr (UV) load_row_buf<BF, D>(fo[pb], rf, i * rsb, so, j);
+      const float l = COLN ? 0.f : bld32(rl, 4 * i, 4 * (tp0 + 16 * pb));
       lse2[pb] = tp0 + 16 * pb + i < npts ? l : kMasked;
     }
     f4 gf[VB][2], P[DB][2], Q[DB][2];
@@ -298,16 +317,16 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(FS_POIN
             zv = SOp{};
             uv = SOp{};
           }
-          get_first(zv, hb + IM::kW, lane, IM::kZ / 64);
-          get_first(uv, hb + IM::kW + IM::kZ, lane, IM::kZ / 64);
+          if constexpr (ZV) get_first(zv, hb + IM::kW, lane, IM::kZ / 64);
+          if constexpr (UV) get_first(uv, hb + IM::kW + IM::kZ, lane, IM::kZ / 64);
 #pragma unroll
           for (int gb = 0; gb < GBH; ++gb) {
             const f4 dsT = *reinterpret_cast<const f4*>(bS + 64 + kHS * h + 16 * gb + 4 * j);
 #pragma unroll
             for (int pb = 0; pb < 2; ++pb) {
               f4 g = dsT;
-              g = mm_slot_row<BF, D, GBH, false>(zv, gb, go[pb], g);
-              g = mm_slot_row<BF, D, GBH, false>(uv, gb, fo[pb], g);
+              if constexpr (ZV) g = mm_slot_row<BF, D, GBH, false>(zv, gb, go[pb], g);
+              if constexpr (UV) g = mm_slot_row<BF, D, GBH, false>(uv, gb, fo[pb], g);
 #pragma unroll
               for (int r = 0; r < 4; ++r) {
                 g[r] *= w[gb][pb][r];  // w dw
@@ -319,19 +338,23 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(FS_POIN
         }
         {
           UOp ug, wg;
-          lds_get(ug, hb + IM::kW + 2 * IM::kZ, lane);
+          if constexpr (UV) lds_get(ug, hb + IM::kW + 2 * IM::kZ, lane);
           lds_get(wg, hb + IM::kW + 2 * IM::kZ + IM::kU, lane);
-          const TileB<BF, GBH, 2> wt = tile_b<BF, GBH, 2>(w);
-          const SplitB<BF, GBH> ws = split_b<BF, GBH>(w), dws = split_b<BF, GBH>(dw);
+          const SplitB<BF, GBH> dws = split_b<BF, GBH>(dw);
 #pragma unroll
           for (int pb = 0; pb < 2; ++pb) {
+            if constexpr (UV) {
+              const TileB<BF, GBH, 2> wt = tile_b<BF, GBH, 2>(w);
 #pragma unroll
-            for (int vb = 0; vb < VB; ++vb)
-              gf[vb][pb] = mm_gop_b<BF, GBH, VB, 2>(ug, vb, wt, pb, gf[vb][pb]);
+              for (int vb = 0; vb < VB; ++vb)
+                gf[vb][pb] = mm_gop_b<BF, GBH, VB, 2>(ug, vb, wt, pb, gf[vb][pb]);
+            }
 #pragma unroll
-            for (int d = 0; d < DB; ++d) {
-              P[d][pb] = mm_split_b<BF, GBH, DB>(wg, d, dws, pb, P[d][pb]);
-              Q[d][pb] = mm_split_b<BF, GBH, DB>(wg, d, ws, pb, Q[d][pb]);
+            for (int d = 0; d < DB; ++d) P[d][pb] = mm_split_b<BF, GBH, DB>(wg, d, dws, pb, P[d][pb]);
+            if constexpr (!COLN) {  // Q only for the correction c Q
+              const SplitB<BF, GBH> ws = split_b<BF, GBH>(w);
+#pragma unroll
+              for (int d = 0; d < DB; ++d) Q[d][pb] = mm_split_b<BF, GBH, DB>(wg, d, ws, pb, Q[d][pb]);
             }
           }
         }
@@ -344,20 +367,24 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(FS_POIN
     // per point: c and tb over the four lane rows; dx = P - c Q; stores
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) {
-      const float cc = col4_sum(csum[pb]);
-      const float tb = col4_sum(tsum[pb]);
+      const float cc = COLN ? 0.f : col4_sum(csum[pb]);
+      const float tb = COLN ? 0.f : col4_sum(tsum[pb]);
       const int so = (tp0 + 16 * pb) * rsb;
+      if constexpr (UV) {
 #pragma unroll
-      for (int vb = 0; vb < VB; ++vb)
-        bst_row4<BF>(rdf, gf[vb][pb], i * rsb + (16 * vb + 4 * j) * (int)sizeof(T), so);
+        for (int vb = 0; vb < VB; ++vb)
+          bst_row4<BF>(rdf, gf[vb][pb], i * rsb + (16 * vb + 4 * j) * (int)sizeof(T), so);
+      }
 #pragma unroll
       for (int d = 0; d < DB; ++d) {
+        const int vo = i * rsb + (16 * d + 4 * j) * (int)sizeof(T);
         f4 v;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = P[d][pb][r] - cc * Q[d][pb][r];
-        bst_row4<BF>(rdx, v, i * rsb + (16 * d + 4 * j) * (int)sizeof(T), so);
+        for (int r = 0; r < 4; ++r) v[r] = COLN ? P[d][pb][r] : P[d][pb][r] - cc * Q[d][pb][r];
+        if constexpr (ROLE == 2) v += bld_row4<BF>(rdx, vo, so);  // the slice weights' dx part
+        bst_row4<BF>(rdx, v, vo, so);
       }
-      if (j == 0) {
+      if (!COLN && j == 0) {
         bst32(rc, cc, 8 * i, 8 * (tp0 + 16 * pb));
         bst32(rc, tb, 8 * i + 4, 8 * (tp0 + 16 * pb));
       }
@@ -471,19 +498,21 @@ hipError_t run_pass_stats_pt(const Geom& g, const PassArgs& a, hipStream_t st) {
   return hipErrorInvalidConfiguration;
 }
 
-hipError_t run_pass_point(const Geom& g, const PassArgs& a, hipStream_t st) {
+namespace {
+template <int ROLE>
+hipError_t run_point_role(const Geom& g, const PassArgs& a, hipStream_t st) {
   const PassCfg cfg = pick_cfg(g, PASS_POINT);
   if (cfg.NP != FS_POINT_WAVES || g.D > 32) return hipErrorInvalidConfiguration;
   uint4* img = static_cast<uint4*>(const_cast<void*>(a.img));
   const dim3 igrid(((g.G + 63) / 64) * g.BH()), iblock(64 * 11);
   const dim3 grid(cfg.chunks * g.BH()), block(64 * FS_POINT_WAVES);
-#define FS_POINT(BF_, D_)                                                                \
-  {                                                                                      \
-    hipLaunchKernelGGL((k_point_images<BF_, D_>), igrid, iblock, 0, st, a, img);         \
-    hipError_t e = hipGetLastError();                                                    \
-    if (e != hipSuccess) return e;                                                       \
-    hipLaunchKernelGGL((k_point<BF_, D_, FS_POINT_WAVES>), grid, block, 0, st, a);                    \
-    return hipGetLastError();                                                            \
+#define FS_POINT(BF_, D_)                                                                  \
+  {                                                                                        \
+    hipLaunchKernelGGL((k_point_images<BF_, D_, ROLE>), igrid, iblock, 0, st, a, img);     \
+    hipError_t e = hipGetLastError();                                                      \
+    if (e != hipSuccess) return e;                                                         \
+    hipLaunchKernelGGL((k_point<BF_, D_, FS_POINT_WAVES, ROLE>), grid, block, 0, st, a);   \
+    return hipGetLastError();                                                              \
   }
   if (g.bf16 && g.D == 16) FS_POINT(true, 16)
   if (g.bf16 && g.D == 32) FS_POINT(true, 32)
@@ -491,6 +520,17 @@ hipError_t run_pass_point(const Geom& g, const PassArgs& a, hipStream_t st) {
   if (!g.bf16 && g.D == 32) FS_POINT(false, 32)
 #undef FS_POINT
   return hipErrorInvalidConfiguration;
+}
+}  // namespace
+
+hipError_t run_pass_point(const Geom& g, const PassArgs& a, int role, hipStream_t st) {
+  switch (role) {
+    case 0: return run_point_role<0>(g, a, st);
+    case 1: return run_point_role<1>(g, a, st);
+    case 2: return run_point_role<2>(g, a, st);
+    case 3: return run_point_role<3>(g, a, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 }  // namespace fs

@@ -54,6 +54,11 @@ CASES = [
     case("f32_D32_G48_linc", "f32", 32, 48, O.MIX_LINEAR_C),
     case("bf16_D32_G80_linc", "bf16", 32, 80, O.MIX_LINEAR_C, N=900),
     case("f32_D32_G208_linc", "f32", 32, 208, O.MIX_LINEAR_C, N=600, H=2),
+    # slot-blocked family at G = 1024 and with a partial last block; head width 64 stays on
+    # the cooperative form
+    case("bf16_D32_G1024_linc", "bf16", 32, 1024, O.MIX_LINEAR_C, N=600, H=2, B=1),
+    case("f32_D32_G336_lin", "f32", 32, 336, O.MIX_LINEAR_G, N=500, H=2),
+    case("f32_D64_G256_linc", "f32", 64, 256, O.MIX_LINEAR_C, N=500, H=2),
 ]
 
 

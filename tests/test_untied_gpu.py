@@ -50,6 +50,11 @@ CASES = [
     case("f32_D32_G48_lin", "f32", 32, 48, O.MIX_LINEAR_G),
     case("bf16_D32_G80_attn", "bf16", 32, 80, O.MIX_ATTN, N=900),
     case("f32_D32_G272_lin", "f32", 32, 272, O.MIX_LINEAR_G, N=600, H=2),
+    # slot-blocked family (point-owned pass and parameter pass per weight set) at G = 1024;
+    # the cooperative form beyond 128 slots remains for head width 64
+    case("f32_D32_G1024_lin", "f32", 32, 1024, O.MIX_LINEAR_G, N=500, H=2, B=1),
+    case("bf16_D16_G512_attn", "bf16", 16, 512, O.MIX_ATTN, N=600, H=2, B=1),
+    case("f32_D64_G256_lin", "f32", 64, 256, O.MIX_LINEAR_G, N=500, H=2),
 ]
 
 
