@@ -60,7 +60,11 @@ PassEvents& pass_events() {
   return ev;
 }
 
-bool blocked(const Geom& g) { return g.G > FS_BLOCKED_MIN_G && g.D <= 32; }
+bool blocked(const Geom& g) {
+  // head width 64: bf16 storage and the tied path (fp32 images of a 64-slot block would not
+  // fit twice in LDS)
+  return g.G > FS_BLOCKED_MIN_G && (g.D <= 32 || (g.D == 64 && g.bf16 && !g.untied));
+}
 
 PassCfg pick_cfg(const Geom& g, Pass pass) {
   PassCfg c{};
@@ -81,7 +85,7 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
   } else if (pass == PASS_POINT) {
     c.GS = 64;  // slot block streamed through LDS
     c.NS = 1;
-    c.NP = FS_POINT_WAVES;
+    c.NP = g.D > 32 ? FS_POINT_WAVES_WIDE : FS_POINT_WAVES;
   } else {
     c.GS = 64;
     c.NS = 2;  // the slot-wave counts with a tiling: 2, 4, 8, 16
@@ -172,6 +176,8 @@ FwdWs fwd_ws_layout(const Geom& g) {
   off += up(sizeof(float) * (size_t)g.BH() * c.chunks * g.G);
   L.lse = off;
   off += up(blocked(g) ? sizeof(float) * (size_t)g.BH() * (size_t)g.N : 0);
+  L.simg = off;
+  off += up(blocked(g) ? stat_image_bytes(g) : 0);
   L.total = off;
   return L;
 }
@@ -184,7 +190,7 @@ FwdWs linearno_fwd_ws_layout(const Geom& g) {
   off += up(sizeof(float) * (size_t)g.BH() * c.chunks * g.G * g.V);
   L.partS = off;
   off += up(sizeof(float) * (size_t)g.BH() * c.chunks * 2 * g.G);
-  L.lse = off;
+  L.lse = L.simg = off;
   L.total = off;
   return L;
 }

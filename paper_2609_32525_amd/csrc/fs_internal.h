@@ -46,6 +46,11 @@ bool blocked(const Geom& g);
 #ifndef FS_POINT_WAVES
 #define FS_POINT_WAVES 12
 #endif
+// Wavefronts per workgroup of the point-owned passes at head width 64 (one per SIMD: their
+// register footprint is about twice that of head width 32).
+#ifndef FS_POINT_WAVES_WIDE
+#define FS_POINT_WAVES_WIDE 4
+#endif
 #ifndef FS_POINT_WPE
 #define FS_POINT_WPE 3
 #endif
@@ -134,6 +139,10 @@ hipError_t run_pass_point(const Geom& g, const PassArgs& a, int role, hipStream_
 // point-owned statistics pass of the slot-blocked family (lse only; chunks of PASS_POINT)
 hipError_t run_pass_stats_pt(const Geom& g, const PassArgs& a, hipStream_t st);
 size_t point_image_bytes(const Geom& g);  // workspace of the point-owned pass's operand images
+// Head width 64: the statistics pass with its slot blocks' images streamed through LDS (built
+// into img, stat_image_bytes of workspace, first).
+size_t stat_image_bytes(const Geom& g);
+hipError_t run_pass_stats_stream(const Geom& g, const PassArgs& a, void* img, hipStream_t st);
 hipError_t run_pass_bwd_params(const Geom& g, const PassArgs& a, int role, hipStream_t st);
 // Untied variant, backward pass B in two parts: role 1 the slice weights (writes dx, dfx),
 // role 2 the deslice weights (adds to dx); each writes its own parameter partials.
@@ -166,7 +175,8 @@ PassEvents& pass_events();
 
 // Workspace carve-up (byte offsets, 256-byte aligned).
 struct FwdWs {
-  size_t partU, partS, lse, total;  // lse: [BH][N] when the blocked family needs it
+  size_t partU, partS, lse, simg, total;  // lse: [BH][N] when the blocked family needs it;
+                                          // simg: the streamed statistics pass's images
 };
 struct BwdWs {
   size_t partDZ, dzm, dz, dU, ds, cen, partP, partM, scr, cpt, img, partP2, ones, total;

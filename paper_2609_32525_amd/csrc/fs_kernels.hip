@@ -75,7 +75,9 @@ hipError_t launch_slice(const Geom& g, const void* x, const void* fx, const floa
     sa.lse_out = lse != nullptr ? lse : reinterpret_cast<float*>(ws + L.lse);
     a.lse_in = sa.lse_out;
     e = timed(PASS_SLICE, st, [&] {
-      hipError_t e1 = FS_STATS_POINT ? run_pass_stats_pt(g, sa, st) : run_pass_stats(g, sa, st);
+      hipError_t e1 = g.D > 32 ? run_pass_stats_stream(g, sa, ws + L.simg, st)
+                               : FS_STATS_POINT ? run_pass_stats_pt(g, sa, st)
+                                                : run_pass_stats(g, sa, st);
       return e1 != hipSuccess ? e1 : run_pass_slice_blk(g, a, st);
     });
   } else {

@@ -204,7 +204,7 @@ __device__ __forceinline__ f4 mm_split_b(const GOp<BF, GBH, CB>& o, int cb, cons
 }
 
 template <bool BF, int D, int NW, int ROLE>
-__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(FS_POINT_WPE_MIN, FS_POINT_WPE))) void k_point(
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(D > 32 ? 1 : FS_POINT_WPE_MIN, D > 32 ? 1 : FS_POINT_WPE))) void k_point(
     PassArgs a) {
   constexpr bool ZV = ROLE == 0 || ROLE == 2;  // dw = dout zmix^T + ...
   constexpr bool UV = ROLE != 2;               // dw = ... + F dU^T; dfx = w dU
@@ -472,11 +472,145 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(FS_POIN
   }
 }
 
+// Statistics pass for head widths whose operand images of all slots do not fit in LDS
+// (dh = 64: 256 KB at G = 1024): the same running maximum and rescaled sum per point, with the
+// slot blocks' images (W_s split in two bf16 parts, scaled bias; built once per forward by
+// k_stats_images) streamed through double-buffered LDS as in the point-owned pass.
+template <bool BF, int D>
+struct StatImages {
+  using SOp = SlotOp<BF, D, 4>;
+  static constexpr int kW = lds_chunks<SOp>();
+  static constexpr int kChunks = kW + 64 / 4;  // + the block's 64 scaled biases
+};
+template <int NW>
+constexpr int stat_stride(int chunks) {
+  return (chunks + 64 * NW - 1) / (64 * NW) * (64 * NW);  // whole copy rounds
+}
+
+template <bool BF, int D, int NW>
+__global__ __launch_bounds__(64) void k_stats_images(PassArgs a, uint4* img) {
+  using SI = StatImages<BF, D>;
+  constexpr int kStride = stat_stride<NW>(SI::kChunks);
+  const int NB = (a.G + 63) / 64;
+  const int blk = blockIdx.x % NB, bh = blockIdx.x / NB;
+  const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
+  HeadCtx c;
+  c.bh = bh;
+  c.h = bh % a.H;
+  c.sc = kLog2e / a.tau[c.h];
+  c.W = a.Ws + (a.ws_per_head ? (int64_t)c.h * D * a.G : 0);
+  c.bias = a.bias + (a.ws_per_head ? (int64_t)c.h * a.G : 0);
+  uint4* out = img + ((int64_t)bh * NB + blk) * kStride;
+  typename SI::SOp o;
+  load_slotop<BF, D, 4, true, BF>(o, c.W, a.G, 64 * blk, slot_lim(a), c.sc, i, j);
+  put_first(o, out, lane, SI::kW / 64);
+  reinterpret_cast<float*>(out + SI::kW)[lane] = slot_bias_at(c, a, 64 * blk + lane);
+}
+
+template <bool BF, int D, int NW>
+__global__ __launch_bounds__(64 * NW) void k_stats_stream(PassArgs a, const uint4* img) {
+  using SI = StatImages<BF, D>;
+  using SOp = typename SI::SOp;
+  using T = typename Store<BF>::T;
+  constexpr int kStride = stat_stride<NW>(SI::kChunks);
+  constexpr int kCopy = kStride / (64 * NW);
+  __shared__ uint4 simg[2][kStride];
+  const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
+  const int wpu = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const HeadCtx c = head_ctx<D>(a, 0, 0);
+  const int NB = (a.G + 63) / 64;
+  const uint4* himg = img + (int64_t)c.bh * NB * kStride;
+
+  const int64_t rs = (int64_t)a.H * D;
+  const T* xb = (const T*)a.x + c.off;
+  const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
+  const int64_t pend = min(a.N, pbeg + a.chunk_pts);
+  const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
+  const int nstep = (npts + 32 * NW - 1) / (32 * NW);
+  const int rsb = (int)(rs * sizeof(T));
+  const auto rx = rows_rsrc(xb + pbeg * rs, npts, (int)rs, D);
+  const auto rl = rows_rsrc(a.lse_out + (int64_t)c.bh * a.N + pbeg, npts, 1, 1);
+
+  Stage<kCopy> stg;
+  if (nstep == 0) return;  // uniform over the workgroup
+  stage_load<0, kCopy, 64 * NW>(stg, himg);
+  stage_put<0, kCopy, 64 * NW>(stg, simg[0]);
+  __syncthreads();
+  int kbuf = 0;
+  for (int step = 0; step < nstep; ++step) {
+    const int tp0 = (step * NW + wpu) * 32;
+    RowOp<BF, D> xo[2];
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) load_row_buf<BF, D>(xo[pb], rx, i * rsb, (tp0 + 16 * pb) * rsb, j);
+    float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
+    for (int blk = 0; blk < NB; ++blk) {
+      const bool more = blk + 1 < NB || step + 1 < nstep;
+      if (more)
+        stage_load<0, kCopy, 64 * NW>(stg, himg + (int64_t)(blk + 1 < NB ? blk + 1 : 0) * kStride);
+      const uint4* cb = simg[kbuf];
+      const float* bS = reinterpret_cast<const float*>(cb + SI::kW);
+      SOp wop;
+      lds_get(wop, cb, lane);
+      f4 t[4][2];
+#pragma unroll
+      for (int gb = 0; gb < 4; ++gb) {
+        const f4 bT = *reinterpret_cast<const f4*>(bS + 16 * gb + 4 * j);
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) t[gb][pb] = mm_slot_row<BF, D, 4, BF>(wop, gb, xo[pb], bT);
+      }
+#pragma unroll
+      for (int pb = 0; pb < 2; ++pb) {
+        float bm = t[0][pb][0];
+#pragma unroll
+        for (int gb = 0; gb < 4; ++gb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) bm = vmax(bm, t[gb][pb][r]);
+        const float mn = vmax(m[pb], col4_max(bm));
+        float sum = 0.f;
+#pragma unroll
+        for (int gb = 0; gb < 4; ++gb)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sum += __builtin_amdgcn_exp2f(t[gb][pb][r] - mn);
+        l[pb] = l[pb] * __builtin_amdgcn_exp2f(m[pb] - mn) + sum;
+        m[pb] = mn;
+      }
+      if (more) stage_put<0, kCopy, 64 * NW>(stg, simg[kbuf ^ 1]);
+      __syncthreads();
+      kbuf ^= 1;
+    }
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      const float L = col4_sum(l[pb]);
+      if (j == 0) bst32(rl, m[pb] + __log2f(L), 4 * i, 4 * (tp0 + 16 * pb));
+    }
+  }
+}
+
 }  // namespace
 
+size_t stat_image_bytes(const Geom& g) {
+  if (g.D != 64 || !g.bf16) return 0;  // the in-LDS statistics pass builds its own
+  const int ch = stat_stride<FS_POINT_WAVES_WIDE>(StatImages<true, 64>::kChunks);
+  return (size_t)g.BH() * ((g.G + 63) / 64) * ch * 16;
+}
+
+hipError_t run_pass_stats_stream(const Geom& g, const PassArgs& a, void* img, hipStream_t st) {
+  const PassCfg cfg = pick_cfg(g, PASS_POINT);
+  if (g.D != 64 || !g.bf16 || cfg.NP != FS_POINT_WAVES_WIDE) return hipErrorInvalidConfiguration;
+  uint4* im = static_cast<uint4*>(img);
+  const dim3 igrid(((g.G + 63) / 64) * g.BH()), grid(cfg.chunks * g.BH());
+  hipLaunchKernelGGL((k_stats_images<true, 64, FS_POINT_WAVES_WIDE>), igrid, dim3(64), 0, st, a, im);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((k_stats_stream<true, 64, FS_POINT_WAVES_WIDE>), grid,
+                     dim3(64 * FS_POINT_WAVES_WIDE), 0, st, a, im);
+  return hipGetLastError();
+}
+
 size_t point_image_bytes(const Geom& g) {
-  if (g.D > 32) return 0;
-  const int ch = g.bf16 ? (g.D == 16 ? PointImages<true, 16>::kStride : PointImages<true, 32>::kStride)
+  if (g.D > 64 || (g.D == 64 && !g.bf16)) return 0;
+  const int ch = g.bf16 ? (g.D == 16 ? PointImages<true, 16>::kStride
+                           : g.D == 32 ? PointImages<true, 32>::kStride : PointImages<true, 64>::kStride)
                         : (g.D == 16 ? PointImages<false, 16>::kStride : PointImages<false, 32>::kStride);
   return (size_t)g.BH() * ((g.G + 63) / 64) * ch * 16;
 }
@@ -502,22 +636,26 @@ namespace {
 template <int ROLE>
 hipError_t run_point_role(const Geom& g, const PassArgs& a, hipStream_t st) {
   const PassCfg cfg = pick_cfg(g, PASS_POINT);
-  if (cfg.NP != FS_POINT_WAVES || g.D > 32) return hipErrorInvalidConfiguration;
+  const int nw = g.D > 32 ? FS_POINT_WAVES_WIDE : FS_POINT_WAVES;
+  if (cfg.NP != nw || g.D > 64 || (g.D > 32 && ROLE != 0)) return hipErrorInvalidConfiguration;
   uint4* img = static_cast<uint4*>(const_cast<void*>(a.img));
   const dim3 igrid(((g.G + 63) / 64) * g.BH()), iblock(64 * 11);
-  const dim3 grid(cfg.chunks * g.BH()), block(64 * FS_POINT_WAVES);
-#define FS_POINT(BF_, D_)                                                                  \
+  const dim3 grid(cfg.chunks * g.BH()), block(64 * nw);
+#define FS_POINT(BF_, D_, NW_)                                                             \
   {                                                                                        \
     hipLaunchKernelGGL((k_point_images<BF_, D_, ROLE>), igrid, iblock, 0, st, a, img);     \
     hipError_t e = hipGetLastError();                                                      \
     if (e != hipSuccess) return e;                                                         \
-    hipLaunchKernelGGL((k_point<BF_, D_, FS_POINT_WAVES, ROLE>), grid, block, 0, st, a);   \
+    hipLaunchKernelGGL((k_point<BF_, D_, NW_, ROLE>), grid, block, 0, st, a);              \
     return hipGetLastError();                                                              \
   }
-  if (g.bf16 && g.D == 16) FS_POINT(true, 16)
-  if (g.bf16 && g.D == 32) FS_POINT(true, 32)
-  if (!g.bf16 && g.D == 16) FS_POINT(false, 16)
-  if (!g.bf16 && g.D == 32) FS_POINT(false, 32)
+  if (g.bf16 && g.D == 16) FS_POINT(true, 16, FS_POINT_WAVES)
+  if (g.bf16 && g.D == 32) FS_POINT(true, 32, FS_POINT_WAVES)
+  if (!g.bf16 && g.D == 16) FS_POINT(false, 16, FS_POINT_WAVES)
+  if (!g.bf16 && g.D == 32) FS_POINT(false, 32, FS_POINT_WAVES)
+  if constexpr (ROLE == 0) {  // head width 64: bf16 and the tied path only
+    if (g.bf16 && g.D == 64) FS_POINT(true, 64, FS_POINT_WAVES_WIDE)
+  }
 #undef FS_POINT
   return hipErrorInvalidConfiguration;
 }

@@ -110,6 +110,12 @@ SMALL = [
     small("bf16_D32_G1008_lin", "bf16", 32, 1008, O.MIX_LINEAR_G, tau_mode="uniform",
           ws_mode="std3", N=700, H=2, B=1),
     small("f32_D32_G48_lin_N33", "f32", 32, 48, O.MIX_LINEAR_G, N=33),
+    # head width 64 in the slot-blocked family (bf16): streamed statistics images, 4-wave
+    # point-owned pass; a partial last block; a ragged tail
+    small("bf16_D64_G1024_lin", "bf16", 64, 1024, O.MIX_LINEAR_G, tau_mode="uniform",
+          ws_mode="std3", N=500, H=2, B=1),
+    small("bf16_D64_G176_linc", "bf16", 64, 176, O.MIX_LINEAR_C, N=700, H=2),
+    small("bf16_D64_G256_lin_N33", "bf16", 64, 256, O.MIX_LINEAR_G, N=33, H=2),
 ]
 
 
