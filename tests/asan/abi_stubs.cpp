@@ -38,6 +38,7 @@ hipError_t launch_linearno_slice(const Geom&, const void*, const void*, const fl
 hipError_t static_scratch(int, void**) { return hipErrorNoDevice; }
 // sizes only enter the workspace totals; any fixed values keep the ABI self-consistent
 size_t point_image_bytes(const Geom& g) { return (size_t)g.BH() * g.G * 64; }
+size_t stat_image_bytes(const Geom& g) { return g.D == 64 ? (size_t)g.BH() * g.G * 32 : 0; }
 bool attn_rows(const Geom& g, int kind) { return kind == 3 && g.G > 256; }
 
 }  // namespace fs
