@@ -39,6 +39,21 @@ enum Pass {
 // (once per weight set for the untied variant and LinearNO). Head widths up to 32. Below the
 // threshold every pass is one kernel whose wavefronts split the slots of a tile.
 bool blocked(const Geom& g);
+// The slot-blocked family's deslice: point-owned with streamed slot blocks (1), or the
+// cooperative kernel with one slot wave per 64 slots (0).
+#ifndef FS_DESLICE_POINT
+#define FS_DESLICE_POINT 1
+#endif
+// Above this slot count (bf16 N = 2^18: G = 512 deslice 497 -> 300 us, G = 1024 859 -> 544 us;
+// at G = 256 the four-wave cooperative kernel is faster, 151 against 176 us).
+#ifndef FS_DESLICE_POINT_MIN_G
+#define FS_DESLICE_POINT_MIN_G 256
+#endif
+// Whether the deslice runs point-owned (its launch arguments then take the chunking of
+// PASS_POINT, not PASS_DESLICE).
+inline bool deslice_point_owned(const Geom& g) {
+  return FS_DESLICE_POINT && blocked(g) && g.G > FS_DESLICE_POINT_MIN_G;
+}
 // Wavefronts per workgroup of the point-owned pass, and the range of resident wavefronts per
 // SIMD it is compiled for (the minimum caps its registers). Twelve wavefronts with three per
 // SIMD (a few registers spilled) measured 5-8% faster than eight with two; six and four

@@ -110,7 +110,7 @@ hipError_t launch_linearno_slice(const Geom& g, const void* x, const void* fx, c
 hipError_t launch_deslice(const Geom& g, const void* x, const float* Ws, const float* bias,
                           const float* tau, const float* zmix, const float* lse, float* lse_out,
                           void* out, hipStream_t st) {
-  PassArgs a = base_args(g, PASS_DESLICE);
+  PassArgs a = base_args(g, deslice_point_owned(g) ? PASS_POINT : PASS_DESLICE);
   a.x = x;
   a.Ws = Ws;
   a.bias = bias;

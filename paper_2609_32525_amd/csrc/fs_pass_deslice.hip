@@ -10,6 +10,7 @@
 #define FS_DESLICE_STAGE 1
 #endif
 
+
 namespace fs {
 namespace {
 
@@ -221,6 +222,170 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(D 
       ntile, load_tile, [&](Tile& cur, int t) { body(cur.xo, cur.lse2, t); });
 }
 
+// =======================================================================================
+// Point-owned deslice of the slot-blocked family (G > 128): every wavefront owns a 32-point
+// tile per step and sweeps all slot blocks, out += w z' per block, with no exchange between
+// wavefronts. A block's operand images (W_s scaled by log2(e)/tau, split in two bf16 parts;
+// z' as the contraction-over-slots operand; the scaled bias), in halves of 32 slots, are
+// built by four of the workgroup's wavefronts into the free half of a double-buffered LDS
+// area while the block before is computed (one part each; the loads go out before the
+// block's arithmetic, the LDS writes after it). ST: the normaliser is computed in the same
+// sweep, online: a running maximum per point, with the sum and the output accumulator
+// rescaled whenever the maximum grows.
+// =======================================================================================
+template <bool BF, int D>
+struct DesliceImages {
+  static constexpr int GBH = 2, VB = D / 16;
+  using SOp = SlotOp<BF, D, GBH>;
+  using ZOp = GOp<BF, GBH, VB>;
+  static constexpr int kW = lds_chunks<SOp>(), kZ = lds_chunks<ZOp>();
+  // [W half 0][W half 1][z' half 0][z' half 1][64 scaled biases]
+  static constexpr int kChunks = 2 * kW + 2 * kZ + 64 / 4;
+};
+
+template <bool BF, int D, int NW, bool ST>
+__global__ __launch_bounds__(64 * NW) void k_deslice_pt(PassArgs a) {
+  static_assert(NW >= 4, "four wavefronts build the image parts of a block");
+  using IM = DesliceImages<BF, D>;
+  using SOp = typename IM::SOp;
+  using ZOp = typename IM::ZOp;
+  constexpr int GBH = IM::GBH, VB = IM::VB;
+  using T = typename Store<BF>::T;
+  __shared__ uint4 img[2][IM::kChunks];
+  const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
+  const int wpu = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const HeadCtx c = head_ctx<D>(a, 0, 0);
+  const int NB = (a.G + 63) / 64;
+  const int64_t rs = (int64_t)a.H * D;
+  const T* xb = (const T*)a.x + c.off;
+  T* ob = (T*)a.out + c.off;
+  const float* lse = (ST ? a.lse_out : a.lse_in) + (int64_t)c.bh * a.N;
+  const bool want_lse = !ST || a.lse_out != nullptr;
+  const float* zm = a.zmix + (int64_t)c.bh * a.G * D;
+
+  const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
+  const int64_t pend = min(a.N, pbeg + a.chunk_pts);
+  const int npts = pend > pbeg ? (int)(pend - pbeg) : 0;
+  const int nstep = (npts + 32 * NW - 1) / (32 * NW);
+  const int rsb = (int)(rs * sizeof(T));
+  const auto rx = rows_rsrc(xb + pbeg * rs, npts, (int)rs, D);
+  const auto ro = rows_rsrc(ob + pbeg * rs, npts, (int)rs, D);
+  const auto rl = rows_rsrc(want_lse ? lse + pbeg : a.Ws, npts, 1, 1);
+
+  // this wavefront's part of a block image: W half (waves 0, 1), z' half (2, 3), bias (0)
+  SOp wpart;
+  ZOp zpart;
+  float bpart = 0.f;
+  auto build = [&](int blk) {
+    const int g0 = 64 * blk;
+    if (wpu < 2) load_slotop<BF, D, GBH, true, BF>(wpart, c.W, a.G, g0 + 32 * wpu, slot_lim(a), c.sc, i, j);
+    else if (wpu < 4) load_gop<BF, GBH, VB, false>(zpart, zm, D, g0 + 32 * (wpu - 2), slot_lim(a), 1.0f, i, j);
+    if (wpu == 0) bpart = slot_bias_at(c, a, g0 + lane);
+  };
+  auto put = [&](uint4* dst) {
+    if (wpu < 2) lds_put(wpart, dst + wpu * IM::kW, lane);
+    else if (wpu < 4) lds_put(zpart, dst + 2 * IM::kW + (wpu - 2) * IM::kZ, lane);
+    if (wpu == 0) reinterpret_cast<float*>(dst + 2 * IM::kW + 2 * IM::kZ)[lane] = bpart;
+  };
+
+  if (nstep == 0) return;  // uniform over the workgroup
+  build(0);
+  put(img[0]);
+  __syncthreads();
+  int kbuf = 0;
+  for (int step = 0; step < nstep; ++step) {
+    const int tb = (step * NW + wpu) * 32;
+    RowOp<BF, D> xo[2];
+    float lse2[2] = {0.f, 0.f};
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      load_row_buf<BF, D>(xo[pb], rx, i * rsb, (tb + 16 * pb) * rsb, j);
+      if constexpr (!ST) {
+        const float l = bld32(rl, 4 * i, 4 * (tb + 16 * pb));
+        lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
+      }
+    }
+    // lane (i, j): point 16 pb + i; o[vb][pb] holds its outputs 16 vb + 4 j + r
+    f4 o[VB][2];
+    float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
+#pragma unroll
+    for (int vb = 0; vb < VB; ++vb) o[vb][0] = o[vb][1] = zero4();
+    for (int blk = 0; blk < NB; ++blk) {
+      const bool more = blk + 1 < NB || step + 1 < nstep;
+      if (more) build(blk + 1 < NB ? blk + 1 : 0);
+      const uint4* cbuf = img[kbuf];
+      const float* bS = reinterpret_cast<const float*>(cbuf + 2 * IM::kW + 2 * IM::kZ);
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        // T-layout logits: rows = slots 32 h + 16 gb + 4 j + r of the block, cols = points
+        f4 w[GBH][2];
+        {
+          SOp wop;
+          lds_get(wop, cbuf + h * IM::kW, lane);
+#pragma unroll
+          for (int gb = 0; gb < GBH; ++gb) {
+            const f4 bT = *reinterpret_cast<const f4*>(bS + 32 * h + 16 * gb + 4 * j);
+#pragma unroll
+            for (int pb = 0; pb < 2; ++pb) w[gb][pb] = mm_slot_row<BF, D, GBH, BF>(wop, gb, xo[pb], bT);
+          }
+        }
+#pragma unroll
+        for (int pb = 0; pb < 2; ++pb) {
+          if constexpr (ST) {
+            float bm = w[0][pb][0];
+#pragma unroll
+            for (int gb = 0; gb < GBH; ++gb)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) bm = vmax(bm, w[gb][pb][r]);
+            const float mn = vmax(m[pb], col4_max(bm));
+            const float f = __builtin_amdgcn_exp2f(m[pb] - mn);
+            m[pb] = mn;
+            float sum = 0.f;
+#pragma unroll
+            for (int gb = 0; gb < GBH; ++gb)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) {
+                const float e = __builtin_amdgcn_exp2f(w[gb][pb][r] - mn);
+                w[gb][pb][r] = e;
+                sum += e;
+              }
+            l[pb] = l[pb] * f + col4_sum(sum);
+#pragma unroll
+            for (int vb = 0; vb < VB; ++vb) o[vb][pb] *= f;
+          } else {
+#pragma unroll
+            for (int gb = 0; gb < GBH; ++gb)
+#pragma unroll
+              for (int r = 0; r < 4; ++r) w[gb][pb][r] = __builtin_amdgcn_exp2f(w[gb][pb][r] - lse2[pb]);
+          }
+        }
+        ZOp zop;
+        lds_get(zop, cbuf + 2 * IM::kW + h * IM::kZ, lane);
+        const TileB<BF, GBH, 2> wt = tile_b<BF, GBH, 2>(w);
+#pragma unroll
+        for (int vb = 0; vb < VB; ++vb)
+#pragma unroll
+          for (int pb = 0; pb < 2; ++pb) o[vb][pb] = mm_gop_b<BF, GBH, VB, 2>(zop, vb, wt, pb, o[vb][pb]);
+      }
+      if (more) put(img[kbuf ^ 1]);
+      __syncthreads();
+      kbuf ^= 1;
+    }
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb) {
+      if constexpr (ST) {
+        const float inv = __builtin_amdgcn_rcpf(l[pb]);
+#pragma unroll
+        for (int vb = 0; vb < VB; ++vb) o[vb][pb] *= inv;
+        if (want_lse && j == 0) bst32(rl, m[pb] + __log2f(l[pb]), 4 * i, 4 * (tb + 16 * pb));
+      }
+#pragma unroll
+      for (int vb = 0; vb < VB; ++vb)
+        bst_row4<BF>(ro, o[vb][pb], i * rsb + (16 * vb + 4 * j) * (int)sizeof(T), (tb + 16 * pb) * rsb);
+    }
+  }
+}
+
 template <bool ST>
 struct Run_k_deslice_ {
   template <bool BF, int D, int GS, int NS, int NP, int PB>
@@ -235,7 +400,33 @@ struct Run_k_deslice_ {
 
 }  // namespace
 
+namespace {
+template <bool ST>
+hipError_t run_deslice_pt(const Geom& g, const PassArgs& a, hipStream_t st) {
+  const int nw = g.D > 32 ? FS_POINT_WAVES_WIDE : FS_POINT_WAVES;
+  const PassCfg cfg = pick_cfg(g, PASS_POINT);
+  if (cfg.NP != nw) return hipErrorInvalidConfiguration;
+  const dim3 grid(cfg.chunks * g.BH()), block(64 * nw);
+#define FS_DPT(BF_, D_, NW_)                                                              \
+  {                                                                                       \
+    hipLaunchKernelGGL((k_deslice_pt<BF_, D_, NW_, ST>), grid, block, 0, st, a);          \
+    return hipGetLastError();                                                             \
+  }
+  if (g.bf16 && g.D == 16) FS_DPT(true, 16, FS_POINT_WAVES)
+  if (g.bf16 && g.D == 32) FS_DPT(true, 32, FS_POINT_WAVES)
+  if (g.bf16 && g.D == 64) FS_DPT(true, 64, FS_POINT_WAVES_WIDE)
+  if (!g.bf16 && g.D == 16) FS_DPT(false, 16, FS_POINT_WAVES)
+  if (!g.bf16 && g.D == 32) FS_DPT(false, 32, FS_POINT_WAVES)
+#undef FS_DPT
+  return hipErrorInvalidConfiguration;
+}
+}  // namespace
+
 hipError_t run_pass_deslice(const Geom& g, const PassArgs& a, hipStream_t st) {
+  // the slot-blocked family: point-owned, slot blocks streamed (with the normaliser computed
+  // online when none is given); a carries the point-owned passes' chunking
+  if (deslice_point_owned(g))
+    return a.lse_in == nullptr ? run_deslice_pt<true>(g, a, st) : run_deslice_pt<false>(g, a, st);
   if (a.lse_in == nullptr) return run_pass_tilings<PASS_DESLICE, Run_k_deslice_<true>::R>(g, a, st);
   return run_pass_tilings<PASS_DESLICE, Run_k_deslice_<false>::R>(g, a, st);
 }
