@@ -5,6 +5,11 @@
 
 #include "fs_stream.h"
 
+// The point groups' end-of-kernel reduction in the LDS of the loop's exchange buffers (1) or
+// in an allocation of its own (0).
+#ifndef FS_BWDB_LDS_ALIAS
+#define FS_BWDB_LDS_ALIAS 1
+#endif
 // bf16 head width 32 (the fused pass B, not the slot-owned parameter pass): dW_s's
 // point-ordered x operand from the loaded rows through LDS (1), or a second, point-by-point
 // load of x (0).
@@ -141,7 +146,12 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
   constexpr int kDaWords = BF ? (GS * 40 + 1) / 2 : TP * (GS + 1);
   constexpr size_t kGxBytes = NS > 1 ? (size_t)NP * NS * VB * PB * 64 * sizeof(f4) : 0;
   constexpr size_t kDaBytes = (size_t)NS * NP * kDaWords * sizeof(float);
-  __shared__ __attribute__((aligned(16))) char smem[kGxBytes > kDaBytes ? kGxBytes : kDaBytes];
+  // the end-of-kernel reduction over the point groups reuses the same allocation
+  constexpr size_t kRedBytes = NP > 1 ? (size_t)(NP - 1) * NS * DB * GB * 64 * sizeof(f4) +
+                                            (size_t)(NP - 1) * NS * GB * 4 * 16 * sizeof(float)
+                                      : 0;
+  constexpr size_t kSmem0 = kGxBytes > kDaBytes ? kGxBytes : kDaBytes;
+  __shared__ __attribute__((aligned(16))) char smem[FS_BWDB_LDS_ALIAS && kRedBytes > kSmem0 ? kRedBytes : kSmem0];
   f4* gx = reinterpret_cast<f4*>(smem);
   float* myda = reinterpret_cast<float*>(smem) + (size_t)wave * kDaWords;
   // XT: bf16 with head width 32 forms dW_s's point-ordered x operand from the row operand the
@@ -440,8 +450,15 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
 
   float* pp = a.part + ((int64_t)c.bh * a.chunks + c.chunk) * ((int64_t)D * a.G + a.G + 2 * a.nblk);
   if constexpr (NP > 1) {
+#if FS_BWDB_LDS_ALIAS
+    __syncthreads();  // every wave is done with the loop's buffers
+    auto& red = *reinterpret_cast<f4(*)[NP - 1][NS][DB][GB][64]>(smem);
+    auto& redb = *reinterpret_cast<float(*)[NP - 1][NS][GB][4][16]>(
+        smem + (size_t)(NP - 1) * NS * DB * GB * 64 * sizeof(f4));
+#else
     __shared__ f4 red[NP - 1][NS][DB][GB][64];
     __shared__ float redb[NP - 1][NS][GB][4][16];
+#endif
     if (wp > 0) {
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb) {
