@@ -142,8 +142,8 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
   // The dfx / dx exchange buffer (NS > 1) and the per-wave da transpose buffer are never live
   // at the same time (a workgroup barrier separates every exchange from the transposes of
   // the previous and the next tile), so they share one LDS allocation.
-  // gx: [NP][NS][VB][PB][64] f4; da transpose: fp32 [TP points][GS + 1], bf16 [GS slots][40].
-  constexpr int kDaWords = BF ? (GS * 40 + 1) / 2 : TP * (GS + 1);
+  // gx: [NP][NS][VB][PB][64] f4; da transpose: fp32 [TP points][GS + 1], bf16 [GS slots][36].
+  constexpr int kDaWords = da_words<BF, GS, TP>();
   constexpr size_t kGxBytes = NS > 1 ? (size_t)NP * NS * VB * PB * 64 * sizeof(f4) : 0;
   constexpr size_t kDaBytes = (size_t)NS * NP * kDaWords * sizeof(float);
   // the end-of-kernel reduction over the point groups reuses the same allocation
@@ -389,13 +389,12 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
     }
     const KGather<BF, DB, PB>& XK = cur.xk;
     if constexpr (!BF) {
-      // myda[p * (GS + 1) + gl]
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb)
 #pragma unroll
         for (int pb = 0; pb < PB; ++pb)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) myda[(16 * pb + i) * (GS + 1) + 16 * gb + 4 * j + r] = dw[gb][pb][r];
+          for (int r = 0; r < 4; ++r) myda[da_at<GS>(16 * pb + i, 16 * gb + 4 * j + r)] = dw[gb][pb][r];
       wave_lds_sync();
 #pragma unroll
       for (int pb = 0; pb < PB; ++pb)
@@ -407,27 +406,20 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
           for (int d = 0; d < DB; ++d) xv[d] = XK.v[pb][r][d];
 #pragma unroll
           for (int gb = 0; gb < GB; ++gb) {
-            const float bv = myda[pl * (GS + 1) + 16 * gb + i];
+            const float bv = myda[da_at<GS>(pl, 16 * gb + i)];
 #pragma unroll
             for (int d = 0; d < DB; ++d) dW[d][gb] = mfma_f32(xv[d], bv, dW[d][gb]);
           }
         }
       wave_lds_sync();
     } else {
-      unsigned short* t16 = reinterpret_cast<unsigned short*>(myda);  // [GS][40]
-#pragma unroll
-      for (int gb = 0; gb < GB; ++gb)
-#pragma unroll
-        for (int pb = 0; pb < PB; ++pb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) t16[(16 * gb + 4 * j + r) * 40 + 16 * pb + i] = f_to_bf(dw[gb][pb][r]);
+      unsigned short* t16 = reinterpret_cast<unsigned short*>(myda);
+      da_put_bf<GB, PB>(t16, dw, i, j);
       wave_lds_sync();
       const bf8(&xa)[DB] = XK.v;
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb) {
-        const uint2 lo = *reinterpret_cast<const uint2*>(t16 + (16 * gb + i) * 40 + 4 * j);
-        const uint2 hi = *reinterpret_cast<const uint2*>(t16 + (16 * gb + i) * 40 + 16 + 4 * j);
-        const bf8 bt = __builtin_bit_cast(bf8, uint4{lo.x, lo.y, hi.x, hi.y});
+        const bf8 bt = da_get_bf(t16, gb, i, j);
 #pragma unroll
         for (int d = 0; d < DB; ++d) dW[d][gb] = mfma_bf16(xa[d], bt, dW[d][gb]);
       }

@@ -101,8 +101,8 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(GS
       for (int d = 0; d < DB; ++d) dW[q][d][gb] = zero4();
     }
 
-  // per-wave da transpose buffer: fp32 [TP points][GS + 1], bf16 [GS slots][40]
-  constexpr int kDaWords = BF ? (GS * 40 + 1) / 2 : TP * (GS + 1);
+  // per-wave da transpose buffer: fp32 [TP points][GS + 1], bf16 [GS slots][36]
+  constexpr int kDaWords = da_words<BF, GS, TP>();
   __shared__ __attribute__((aligned(16))) float dabuf[NP][kDaWords];
   float* myda = dabuf[wp];
 
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(GS
 #pragma unroll
         for (int pb = 0; pb < PB; ++pb)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) myda[(16 * pb + i) * (GS + 1) + 16 * gb + 4 * j + r] = da[gb][pb][r];
+          for (int r = 0; r < 4; ++r) myda[da_at<GS>(16 * pb + i, 16 * gb + 4 * j + r)] = da[gb][pb][r];
       wave_lds_sync();
 #pragma unroll
       for (int pb = 0; pb < PB; ++pb)
@@ -167,27 +167,20 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(GS
           for (int d = 0; d < DB; ++d) xv[d] = XK.v[pb][r][d];
 #pragma unroll
           for (int gb = 0; gb < GB; ++gb) {
-            const float bv = myda[pl * (GS + 1) + 16 * gb + i];
+            const float bv = myda[da_at<GS>(pl, 16 * gb + i)];
 #pragma unroll
             for (int d = 0; d < DB; ++d) dWq[d][gb] = mfma_f32(xv[d], bv, dWq[d][gb]);
           }
         }
       wave_lds_sync();
     } else {
-      unsigned short* t16 = reinterpret_cast<unsigned short*>(myda);  // [GS][40]
-#pragma unroll
-      for (int gb = 0; gb < GB; ++gb)
-#pragma unroll
-        for (int pb = 0; pb < PB; ++pb)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) t16[(16 * gb + 4 * j + r) * 40 + 16 * pb + i] = f_to_bf(da[gb][pb][r]);
+      unsigned short* t16 = reinterpret_cast<unsigned short*>(myda);
+      da_put_bf<GB, PB>(t16, da, i, j);
       wave_lds_sync();
       const bf8(&xa)[DB] = cur.xk.v;
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb) {
-        const uint2 lo = *reinterpret_cast<const uint2*>(t16 + (16 * gb + i) * 40 + 4 * j);
-        const uint2 hi = *reinterpret_cast<const uint2*>(t16 + (16 * gb + i) * 40 + 16 + 4 * j);
-        const bf8 bt = __builtin_bit_cast(bf8, uint4{lo.x, lo.y, hi.x, hi.y});
+        const bf8 bt = da_get_bf(t16, gb, i, j);
 #pragma unroll
         for (int d = 0; d < DB; ++d) dWq[d][gb] = mfma_bf16(xa[d], bt, dWq[d][gb]);
       }

@@ -143,6 +143,42 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// ---- da transposes through a wavefront's LDS rows (dW_s = X^T da needs the points on the
+// MFMA k index, da comes out of the logits product with the slots there). The LDS serves 32
+// banks of 4 bytes; 4-byte accesses go 32 lanes a pass, 8-byte ones 16.
+//  bf16: one row per slot, its 32 points in 36 halves (18 words), so the 16 rows that one
+//        8-byte read pass touches start on 16 distinct even banks (no pass meets a bank
+//        twice);
+//  fp32: one row per point, GS + 1 words: two lanes share a bank in each pass. The layouts
+//        without that (the slot index XORed with the point's low bits) cost the fp32 kernels
+//        an address register per row offset, and spills where the registers are tight.
+constexpr int kDaPitchBf = 36;
+template <bool BF, int GS, int TP>
+constexpr int da_words() {
+  return BF ? GS * kDaPitchBf / 2 : TP * (GS + 1);
+}
+template <int GS>
+__device__ __forceinline__ int da_at(int p, int g) {
+  return p * (GS + 1) + g;
+}
+// da tile (T layout: slot 16 gb + 4 j + r, point 16 pb + i) into the bf16 rows
+template <int GB, int PB>
+__device__ __forceinline__ void da_put_bf(unsigned short* t16, const f4 (&da)[GB][PB], int i, int j) {
+#pragma unroll
+  for (int gb = 0; gb < GB; ++gb)
+#pragma unroll
+    for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) t16[(16 * gb + 4 * j + r) * kDaPitchBf + 16 * pb + i] = f_to_bf(da[gb][pb][r]);
+}
+// the B operand of slot block gb: slot 16 gb + i, points 4 j .. 4 j + 3 and 16 + 4 j .. + 3
+__device__ __forceinline__ bf8 da_get_bf(const unsigned short* t16, int gb, int i, int j) {
+  const unsigned short* row = t16 + (16 * gb + i) * kDaPitchBf;
+  const uint2 lo = *reinterpret_cast<const uint2*>(row + 4 * j);
+  const uint2 hi = *reinterpret_cast<const uint2*>(row + 16 + 4 * j);
+  return __builtin_bit_cast(bf8, uint4{lo.x, lo.y, hi.x, hi.y});
+}
+
 template <bool BF>
 struct Store;
 template <>
