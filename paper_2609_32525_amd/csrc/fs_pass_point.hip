@@ -176,14 +176,7 @@ __device__ __forceinline__ SplitB<BF, GBH> split_b(const f4 (*t)[2]) {
 #pragma unroll
     for (int q = 0; q < GBH / 2; ++q)
 #pragma unroll
-      for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float v = t[2 * q + e / 4][pb][e % 4];
-          const __bf16 h = (__bf16)v;
-          o.hi[q][pb][e] = h;
-          o.lo[q][pb][e] = (__bf16)(v - (float)h);
-        }
+      for (int pb = 0; pb < 2; ++pb) split_bf8(t[2 * q][pb], t[2 * q + 1][pb], o.hi[q][pb], o.lo[q][pb]);
   }
   return o;
 }

@@ -63,6 +63,32 @@ __device__ __forceinline__ float bf_to_f(unsigned short h) {
 __device__ __forceinline__ unsigned short f_to_bf(float f) {
   return __builtin_bit_cast(unsigned short, (__bf16)f);  // round to nearest even
 }
+typedef float fl2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bfl2 __attribute__((ext_vector_type(2)));
+// Two floats rounded to bf16 (nearest even) in one 32-bit word, the first in the low half.
+__device__ __forceinline__ unsigned bf_pair(float a, float b) {
+  return __builtin_bit_cast(unsigned, __builtin_convertvector(fl2{a, b}, bfl2));
+}
+// The 8 values a[0..3], b[0..3] as one bf16 MFMA operand (element e from a for e < 4).
+__device__ __forceinline__ bf8 to_bf8(const f4& a, const f4& b) {
+  return __builtin_bit_cast(bf8, uint4{bf_pair(a[0], a[1]), bf_pair(a[2], a[3]), bf_pair(b[0], b[1]),
+                                       bf_pair(b[2], b[3])});
+}
+// The same 8 values in two bf16 parts, hi = RN(v) and lo = RN(v - hi), whose sum keeps about
+// 16 significant bits. Each pair's rounded high parts are read back from their packed word (a
+// shift and a mask) instead of being converted one by one.
+__device__ __forceinline__ void split_bf8(const f4& a, const f4& b, bf8& hi, bf8& lo) {
+  const float v[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  unsigned h[4], l[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    h[k] = bf_pair(v[2 * k], v[2 * k + 1]);
+    const float h0 = __uint_as_float(h[k] << 16), h1 = __uint_as_float(h[k] & 0xffff0000u);
+    l[k] = bf_pair(v[2 * k] - h0, v[2 * k + 1] - h1);
+  }
+  hi = __builtin_bit_cast(bf8, uint4{h[0], h[1], h[2], h[3]});
+  lo = __builtin_bit_cast(bf8, uint4{l[0], l[1], l[2], l[3]});
+}
 __device__ __forceinline__ f4 zero4() { return f4{0.f, 0.f, 0.f, 0.f}; }
 __device__ __forceinline__ f4 splat4(float v) { return f4{v, v, v, v}; }
 
@@ -532,12 +558,7 @@ __device__ __forceinline__ f4 mm_gop_tile(const GOp<BF, GB, CB>& o, int cb, cons
       for (int r = 0; r < 4; ++r) acc = mfma_f32(o.v[gb][r][cb], t[gb][pb][r], acc);
   } else {
 #pragma unroll
-    for (int q = 0; q < GB / 2; ++q) {
-      bf8 bt;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) bt[e] = (__bf16)t[2 * q + e / 4][pb][e % 4];
-      acc = mfma_bf16(o.v[q][cb], bt, acc);
-    }
+    for (int q = 0; q < GB / 2; ++q) acc = mfma_bf16(o.v[q][cb], to_bf8(t[2 * q][pb], t[2 * q + 1][pb]), acc);
   }
   return acc;
 }
@@ -564,9 +585,7 @@ __device__ __forceinline__ TileB<BF, GB, PB> tile_b(const f4 (*t)[PB]) {
 #pragma unroll
     for (int q = 0; q < GB / 2; ++q)
 #pragma unroll
-      for (int pb = 0; pb < PB; ++pb)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o.v[q][pb][e] = (__bf16)t[2 * q + e / 4][pb][e % 4];
+      for (int pb = 0; pb < PB; ++pb) o.v[q][pb] = to_bf8(t[2 * q][pb], t[2 * q + 1][pb]);
   }
   return o;
 }
@@ -711,9 +730,7 @@ __device__ __forceinline__ void mm_points(f4 (*acc)[CB], const f4 (*w)[GB],
   } else {
     bf8 at[GB];
 #pragma unroll
-    for (int gb = 0; gb < GB; ++gb)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) at[gb][e] = (__bf16)w[e / 4][gb][e % 4];
+    for (int gb = 0; gb < GB; ++gb) at[gb] = to_bf8(w[0][gb], w[1][gb]);
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb)
 #pragma unroll
