@@ -143,7 +143,10 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
   // at the same time (a workgroup barrier separates every exchange from the transposes of
   // the previous and the next tile), so they share one LDS allocation.
   // gx: [NP][NS][VB][PB][64] f4; da transpose: fp32 [TP points][GS + 1], bf16 [GS slots][36].
-  constexpr int kDaWords = da_words<BF, GS, TP>();
+  // bf16 tiles also stage dx and dfx there for whole-segment stores (store_tile_staged)
+  constexpr bool STAGE = FS_BWDB_STAGE && BF && PB == 2 && D == VB * 16;
+  constexpr int kDaWords = STAGE && kStageBytes<BF, D> / 4 > da_words<BF, GS, TP>() ? kStageBytes<BF, D> / 4
+                                                                                    : da_words<BF, GS, TP>();
   constexpr size_t kGxBytes = NS > 1 ? (size_t)NP * NS * VB * PB * 64 * sizeof(f4) : 0;
   constexpr size_t kDaBytes = (size_t)NS * NP * kDaWords * sizeof(float);
   // the end-of-kernel reduction over the point groups reuses the same allocation
@@ -356,18 +359,32 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
       }
     }
     if (ws == 0) {
+      if constexpr (STAGE) {
+        // through this wavefront's da rows, which the transposes below overwrite afterwards
+        char* sb = reinterpret_cast<char*>(myda);
+        if constexpr (ROLE == 2) {
 #pragma unroll
-      for (int pb = 0; pb < PB; ++pb)
+          for (int cb = 0; cb < DB; ++cb)
 #pragma unroll
-        for (int cb = 0; cb < VB; ++cb) {
-          const int vo = i * rsb + (16 * cb + 4 * j) * (int)sizeof(T), so = (tp0 + 16 * pb) * rsb;
-          if constexpr (ROLE == 2) {
-            bst_row4<BF>(rdx, gx_[cb][pb] + cur.dx0[cb][pb], vo, so);
-          } else {
-            bst_row4<BF>(rdf, gf[cb][pb], vo, so);
-            bst_row4<BF>(rdx, gx_[cb][pb], vo, so);
-          }
+            for (int pb = 0; pb < PB; ++pb) gx_[cb][pb] += cur.dx0[cb][pb];
+        } else {
+          store_tile_staged<BF, D>(sb, gf, rdf, rsb, tp0, lane);
         }
+        store_tile_staged<BF, D>(sb, gx_, rdx, rsb, tp0, lane);
+      } else {
+#pragma unroll
+        for (int pb = 0; pb < PB; ++pb)
+#pragma unroll
+          for (int cb = 0; cb < VB; ++cb) {
+            const int vo = i * rsb + (16 * cb + 4 * j) * (int)sizeof(T), so = (tp0 + 16 * pb) * rsb;
+            if constexpr (ROLE == 2) {
+              bst_row4<BF>(rdx, gx_[cb][pb] + cur.dx0[cb][pb], vo, so);
+            } else {
+              bst_row4<BF>(rdf, gf[cb][pb], vo, so);
+              bst_row4<BF>(rdx, gx_[cb][pb], vo, so);
+            }
+          }
+      }
     }
     }
     // dW_s += X^T da over the tile's points: da goes through LDS to put points on the k index.

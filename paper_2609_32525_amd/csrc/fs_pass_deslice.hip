@@ -44,14 +44,8 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(D 
   load_gop<BF, GB, VB, false>(zop, a.zmix + (int64_t)c.bh * a.G * D, D, c.g0, slot_lim(a), 1.0f, i, j);
 
   __shared__ f4 ox[NS > 1 ? NP : 1][NS > 1 ? NS : 1][VB][2][64];
-  // output staging: one 32-point tile per point group, one row of D values per point, its
-  // 16-byte chunks XOR-swizzled by row (stage_at) so that neither the chunk writes (8 lanes a
-  // pass, eight rows of one chunk column) nor the row reads (8 lanes a pass, whole rows) meet
-  // an LDS bank twice
-  constexpr int kSeg = D * (int)sizeof(T), kChunks = kSeg / 16;
-  constexpr int kSwz = kChunks < 8 ? kChunks : 8, kSwzShift = kSwz == 2 ? 2 : kSwz == 4 ? 1 : 0;
-  auto stage_at = [](int row, int chunk) { return row * kSeg + 16 * (chunk ^ ((row >> kSwzShift) & (kSwz - 1))); };
-  __shared__ __attribute__((aligned(16))) char ostage[FS_DESLICE_STAGE ? NP : 1][FS_DESLICE_STAGE ? 32 * kSeg : 16];
+  // output staging: one 32-point tile per point group (store_tile_staged)
+  __shared__ __attribute__((aligned(16))) char ostage[FS_DESLICE_STAGE ? NP : 1][FS_DESLICE_STAGE ? kStageBytes<BF, D> : 16];
   constexpr int SX = ST && NS > 1;
   __shared__ float st_m[SX ? 2 : 1][SX ? NP : 1][SX ? NS : 1][32];
   __shared__ float st_l[SX ? 2 : 1][SX ? NP : 1][SX ? NS : 1][32];
@@ -186,47 +180,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(D 
     }
     if (ws == 0) {
       if constexpr (FS_DESLICE_STAGE) {
-        // the tile's outputs pass through LDS so that every lane stores 16 contiguous bytes
-        // and each store instruction writes whole D-element row segments
-        char* sb = ostage[wp];
-        wave_lds_sync();
-        if constexpr (BF) {
-          // a lane holds 8 bytes of a chunk; lanes of rows j and j ^ 1 trade halves (one lane
-          // swap per dword: odd rows of the first operand with even rows of the second) so
-          // that every lane writes a whole chunk. Pairs: (vb, vb + 1) of one point, or, with
-          // one 16-wide block, the two point blocks.
-          auto pack = [](const f4& v) {
-            return uint2{f_to_bf(v[0]) | ((unsigned)f_to_bf(v[1]) << 16),
-                         f_to_bf(v[2]) | ((unsigned)f_to_bf(v[3]) << 16)};
-          };
-          constexpr int NQ = VB == 1 ? 1 : 2 * (VB / 2);
-#pragma unroll
-          for (int q = 0; q < NQ; ++q) {
-            const int pb = VB == 1 ? 0 : q / (VB / 2), m = VB == 1 ? 0 : q % (VB / 2);
-            const uint2 lo = VB == 1 ? pack(o[0][0]) : pack(o[2 * m][pb]);
-            const uint2 hi = VB == 1 ? pack(o[0][1]) : pack(o[2 * m + 1][pb]);
-            const auto sx = __builtin_amdgcn_permlane16_swap(lo.x, hi.x, false, false);
-            const auto sy = __builtin_amdgcn_permlane16_swap(lo.y, hi.y, false, false);
-            const int row = VB == 1 ? 16 * (j & 1) + i : 16 * pb + i;
-            const int chunk = 2 * (VB == 1 ? 0 : 2 * m + (j & 1)) + (j >> 1);
-            *reinterpret_cast<uint4*>(sb + stage_at(row, chunk)) = uint4{sx[0], sy[0], sx[1], sy[1]};
-          }
-        } else {
-#pragma unroll
-          for (int pb = 0; pb < 2; ++pb)
-#pragma unroll
-            for (int vb = 0; vb < VB; ++vb)
-              *reinterpret_cast<f4*>(sb + stage_at(16 * pb + i, 4 * vb + j)) = o[vb][pb];
-        }
-        wave_lds_sync();
-        // 32 rows of kChunks 16-byte chunks: kChunks / 2 chunks per lane
-        static_assert(kChunks % 2 == 0, "a 32-row tile spreads evenly over 64 lanes");
-#pragma unroll
-        for (int q = 0; q < kChunks / 2; ++q) {
-          const int f = 64 * q + lane, row = f / kChunks, c16 = f % kChunks;
-          const f4 v = *reinterpret_cast<const f4*>(sb + stage_at(row, c16));
-          bst128(ro, v, row * rsb + 16 * c16, tb * rsb);
-        }
+        store_tile_staged<BF, D>(ostage[wp], o, ro, rsb, tb, lane);
       } else {
 #pragma unroll
         for (int pb = 0; pb < 2; ++pb)

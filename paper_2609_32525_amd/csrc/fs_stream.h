@@ -312,6 +312,62 @@ __device__ __forceinline__ void bst_row4(__amdgpu_buffer_rsrc_t r, f4 v, int vof
   }
 }
 
+// A wavefront's 32-point output tile o[vb][pb] (point 16 pb + i, columns 16 vb + 4 j .. + 3)
+// stored through its LDS rows sb (32 rows of D values, kStageBytes<BF, D>) so that every lane
+// stores 16 contiguous bytes and each store instruction writes whole D-value row segments.
+// The rows' 16-byte chunks are XOR-swizzled by row, so that neither the chunk writes (8 lanes
+// a pass, eight rows of one chunk column) nor the row reads (8 lanes a pass, whole rows) meet
+// an LDS bank twice. bf16 lanes hold 8 bytes of a chunk: lanes of rows j and j ^ 1 first trade
+// halves (one lane swap per dword: odd rows of the first operand with even rows of the
+// second), pairing blocks (vb, vb + 1) of one point or, with one 16-wide block, the two point
+// blocks, so that each writes a whole chunk. The first point of the tile is row 0 at byte
+// offset tb * rsb of the resource. Orders sb against the wavefront's earlier and later LDS use.
+template <bool BF, int D>
+constexpr int kStageBytes = 32 * D * (BF ? 2 : 4);
+// The fused bf16 pass B of the tied path stores dx and dfx this way (1) or straight from the
+// MFMA tiles, 8 bytes per lane (0).
+#ifndef FS_BWDB_STAGE
+#define FS_BWDB_STAGE 1
+#endif
+template <bool BF, int D>
+__device__ __forceinline__ void store_tile_staged(char* sb, const f4 (&o)[D / 16][2],
+                                                  __amdgpu_buffer_rsrc_t ro, int rsb, int tb, int lane) {
+  constexpr int VB = D / 16, kSeg = D * (BF ? 2 : 4), kChunks = kSeg / 16;
+  constexpr int kSwz = kChunks < 8 ? kChunks : 8, kSwzShift = kSwz == 2 ? 2 : kSwz == 4 ? 1 : 0;
+  static_assert(kChunks % 2 == 0, "a 32-row tile spreads evenly over 64 lanes");
+  auto at = [](int row, int chunk) { return row * kSeg + 16 * (chunk ^ ((row >> kSwzShift) & (kSwz - 1))); };
+  const int i = lane & 15, j = lane >> 4;
+  wave_lds_sync();
+  if constexpr (BF) {
+    constexpr int NQ = VB == 1 ? 1 : 2 * (VB / 2);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int pb = VB == 1 ? 0 : q / (VB / 2), m = VB == 1 ? 0 : q % (VB / 2);
+      const f4& a = VB == 1 ? o[0][0] : o[2 * m][pb];
+      const f4& b = VB == 1 ? o[0][1] : o[2 * m + 1][pb];
+      const auto sx = __builtin_amdgcn_permlane16_swap(bf_pair(a[0], a[1]), bf_pair(b[0], b[1]), false, false);
+      const auto sy = __builtin_amdgcn_permlane16_swap(bf_pair(a[2], a[3]), bf_pair(b[2], b[3]), false, false);
+      const int row = VB == 1 ? 16 * (j & 1) + i : 16 * pb + i;
+      const int chunk = 2 * (VB == 1 ? 0 : 2 * m + (j & 1)) + (j >> 1);
+      *reinterpret_cast<uint4*>(sb + at(row, chunk)) = uint4{sx[0], sy[0], sx[1], sy[1]};
+    }
+  } else {
+#pragma unroll
+    for (int pb = 0; pb < 2; ++pb)
+#pragma unroll
+      for (int vb = 0; vb < VB; ++vb) *reinterpret_cast<f4*>(sb + at(16 * pb + i, 4 * vb + j)) = o[vb][pb];
+  }
+  wave_lds_sync();
+  // 32 rows of kChunks 16-byte chunks: kChunks / 2 chunks per lane
+#pragma unroll
+  for (int q = 0; q < kChunks / 2; ++q) {
+    const int f = 64 * q + lane, row = f / kChunks, c16 = f % kChunks;
+    const f4 v = *reinterpret_cast<const f4*>(sb + at(row, c16));
+    bst128(ro, v, row * rsb + 16 * c16, tb * rsb);
+  }
+  wave_lds_sync();
+}
+
 // Four values of one row in the storage dtype (the counterpart of bst_row4), as fp32.
 template <bool BF>
 __device__ __forceinline__ f4 bld_row4(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
