@@ -66,7 +66,7 @@ bool blocked(const Geom& g) {
   return g.G > FS_BLOCKED_MIN_G && (g.D <= 32 || (g.D == 64 && g.bf16 && !g.untied));
 }
 
-PassCfg pick_cfg(const Geom& g, Pass pass) {
+PassCfg pick_cfg(const Geom& g, Pass pass, int np) {
   PassCfg c{};
   c.nblk = 1;
   const bool blk = blocked(g);
@@ -85,7 +85,7 @@ PassCfg pick_cfg(const Geom& g, Pass pass) {
   } else if (pass == PASS_POINT) {
     c.GS = 64;  // slot block streamed through LDS
     c.NS = 1;
-    c.NP = g.D > 32 ? FS_POINT_WAVES_WIDE : FS_POINT_WAVES;
+    c.NP = np > 0 ? np : g.D > 32 ? FS_POINT_WAVES_WIDE : FS_POINT_WAVES;
   } else {
     c.GS = 64;
     c.NS = 2;  // the slot-wave counts with a tiling: 2, 4, 8, 16

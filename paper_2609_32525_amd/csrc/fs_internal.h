@@ -54,6 +54,11 @@ bool blocked(const Geom& g);
 inline bool deslice_point_owned(const Geom& g) {
   return FS_DESLICE_POINT && blocked(g) && g.G > FS_DESLICE_POINT_MIN_G;
 }
+// Wavefronts per workgroup of the point-owned deslice at head width up to 32 (16 measured 3%
+// faster than 12 and 8 at G = 512 and 1024).
+#ifndef FS_DESLICE_PT_WAVES
+#define FS_DESLICE_PT_WAVES 16
+#endif
 // Wavefronts per workgroup of the point-owned pass, and the range of resident wavefronts per
 // SIMD it is compiled for (the minimum caps its registers). Twelve wavefronts with three per
 // SIMD (a few registers spilled) measured 5-8% faster than eight with two; six and four
@@ -66,6 +71,7 @@ inline bool deslice_point_owned(const Geom& g) {
 #ifndef FS_POINT_WAVES_WIDE
 #define FS_POINT_WAVES_WIDE 4
 #endif
+inline int deslice_pt_waves(const Geom& g) { return g.D > 32 ? FS_POINT_WAVES_WIDE : FS_DESLICE_PT_WAVES; }
 #ifndef FS_POINT_WPE
 #define FS_POINT_WPE 3
 #endif
@@ -97,7 +103,10 @@ struct PassCfg {
   int64_t nsub, sub_pts;
 };
 
-PassCfg pick_cfg(const Geom& g, Pass pass);
+// np > 0: the point group count of PASS_POINT's chunking (the point-owned kernels sweep a
+// chunk in steps of 32 np points; a chunk that is a whole number of them leaves no wavefront
+// idle in its last step)
+PassCfg pick_cfg(const Geom& g, Pass pass, int np = 0);
 
 // ---------------------------------------------------------------------------------------
 // Kernel arguments

@@ -24,9 +24,9 @@ hipError_t timed(int pass, hipStream_t st, F&& f) {
   return e;
 }
 
-PassArgs base_args(const Geom& g, Pass p) {
+PassArgs base_args(const Geom& g, Pass p, int np = 0) {
   PassArgs a{};
-  const PassCfg cfg = pick_cfg(g, p);
+  const PassCfg cfg = pick_cfg(g, p, np);
   a.N = g.N;
   a.H = g.H;
   a.G = g.G;
@@ -110,7 +110,8 @@ hipError_t launch_linearno_slice(const Geom& g, const void* x, const void* fx, c
 hipError_t launch_deslice(const Geom& g, const void* x, const float* Ws, const float* bias,
                           const float* tau, const float* zmix, const float* lse, float* lse_out,
                           void* out, hipStream_t st) {
-  PassArgs a = base_args(g, deslice_point_owned(g) ? PASS_POINT : PASS_DESLICE);
+  const bool pt = deslice_point_owned(g);
+  PassArgs a = base_args(g, pt ? PASS_POINT : PASS_DESLICE, pt ? deslice_pt_waves(g) : 0);
   a.x = x;
   a.Ws = Ws;
   a.bias = bias;

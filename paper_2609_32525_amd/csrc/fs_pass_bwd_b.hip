@@ -10,9 +10,8 @@
 #ifndef FS_BWDB_LDS_ALIAS
 #define FS_BWDB_LDS_ALIAS 1
 #endif
-// bf16 head width 32 (the fused pass B, not the slot-owned parameter pass): dW_s's
-// point-ordered x operand from the loaded rows through LDS (1), or a second, point-by-point
-// load of x (0).
+// bf16 head width 32: dW_s's point-ordered x operand from the loaded rows through LDS (1), or
+// a second, point-by-point load of x (0).
 #ifndef FS_BWDB_XT
 #define FS_BWDB_XT 1
 #endif
@@ -159,7 +158,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
   float* myda = reinterpret_cast<float*>(smem) + (size_t)wave * kDaWords;
   // XT: bf16 with head width 32 forms dW_s's point-ordered x operand from the row operand the
   // logits already loaded, through this wavefront's LDS rows, instead of loading x again
-  constexpr bool XT = FS_BWDB_XT && BF && D == 32 && PB == 2 && !PM;
+  constexpr bool XT = FS_BWDB_XT && BF && D == 32 && PB == 2;
   constexpr int kXP = 80;  // LDS row pitch
   __shared__ __attribute__((aligned(16))) char xts[XT ? NS * NP : 1][XT ? 32 * kXP : 16];
 

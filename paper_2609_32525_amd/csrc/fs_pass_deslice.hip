@@ -194,11 +194,6 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(D 
       ntile, load_tile, [&](Tile& cur, int t) { body(cur.xo, cur.lse2, t); });
 }
 
-// Wavefronts per workgroup of the point-owned deslice (head width up to 32; 16 measured 3%
-// faster than 12 and 8 at G = 512 and 1024).
-#ifndef FS_DESLICE_PT_WAVES
-#define FS_DESLICE_PT_WAVES 16
-#endif
 
 // =======================================================================================
 // Point-owned deslice of the slot-blocked family (G > 128): every wavefront owns a 32-point
@@ -381,10 +376,11 @@ struct Run_k_deslice_ {
 namespace {
 template <bool ST>
 hipError_t run_deslice_pt(const Geom& g, const PassArgs& a, hipStream_t st) {
-  // the point-owned passes' chunking; each workgroup sweeps its chunk in steps of 32 NW points
-  const int nw = g.D > 32 ? FS_POINT_WAVES_WIDE : FS_DESLICE_PT_WAVES;
-  const PassCfg cfg = pick_cfg(g, PASS_POINT);
-  if (cfg.NP != (g.D > 32 ? FS_POINT_WAVES_WIDE : FS_POINT_WAVES)) return hipErrorInvalidConfiguration;
+  // the point-owned chunking with this kernel's wavefront count: each workgroup sweeps its
+  // chunk in steps of 32 nw points
+  const int nw = deslice_pt_waves(g);
+  const PassCfg cfg = pick_cfg(g, PASS_POINT, nw);
+  if (cfg.NP != nw) return hipErrorInvalidConfiguration;
   const dim3 grid(cfg.chunks * g.BH()), block(64 * nw);
 #define FS_DPT(BF_, D_, NW_)                                                              \
   {                                                                                       \
