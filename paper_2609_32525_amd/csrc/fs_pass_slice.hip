@@ -132,15 +132,21 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
         for (int r = 0; r < 4; ++r) l[pb][r] = sm[4 * pb + r];
     }
 
-    float f[2][4], lse2[2][4];
+    // the lse store: lane i < 8 of row group j writes point 16 (i / 4) + 4 j + i % 4 (every
+    // lane of a group holds the group's statistics), one store for the tile's 32 points
+    auto pick = [i](float a0, float a1, float a2, float a3, float b0, float b1, float b2, float b3) {
+      const bool o = i & 1, t = i & 2;
+      const float va = t ? (o ? a3 : a2) : (o ? a1 : a0), vb = t ? (o ? b3 : b2) : (o ? b1 : b0);
+      return (i & 4) ? vb : va;
+    };
+    float f[2][4], lse2[2][4], lse_st;
     if constexpr (NS == 1) {
 #pragma unroll
       for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          f[pb][r] = __builtin_amdgcn_rcpf(l[pb][r]);
-          lse2[pb][r] = m[pb][r] + __log2f(l[pb][r]);
-        }
+        for (int r = 0; r < 4; ++r) f[pb][r] = __builtin_amdgcn_rcpf(l[pb][r]);
+      lse_st = pick(m[0][0], m[0][1], m[0][2], m[0][3], m[1][0], m[1][1], m[1][2], m[1][3]) +
+               __log2f(pick(l[0][0], l[0][1], l[0][2], l[0][3], l[1][0], l[1][1], l[1][2], l[1][3]));
     } else {
       const int par = t & 1;
       if (i == 0) {
@@ -172,6 +178,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
           f[pb][r] = __builtin_amdgcn_exp2f(m[pb][r] - M) * __builtin_amdgcn_rcpf(L);
           lse2[pb][r] = M + __log2f(L);
         }
+      lse_st = pick(lse2[0][0], lse2[0][1], lse2[0][2], lse2[0][3], lse2[1][0], lse2[1][1], lse2[1][2], lse2[1][3]);
     }
 
 #pragma unroll
@@ -182,8 +189,8 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
         const float fr = tb + q < npts ? f[pb][r] : 0.f;
 #pragma unroll
         for (int gb = 0; gb < GB; ++gb) w[pb][gb][r] *= fr;
-        if (want_lse && ws == 0 && i == 0) bst32(rl, lse2[pb][r], 4 * q, 4 * tb);
       }
+    if (want_lse && ws == 0 && i < 8) bst32(rl, lse_st, 4 * (16 * (i >> 2) + 4 * j + (i & 3)), 4 * tb);
     if constexpr (ST) return;
 #pragma unroll
     for (int gb = 0; gb < GB; ++gb) {
