@@ -141,22 +141,25 @@ __global__ __launch_bounds__(64 * 11) void k_point_images(PassArgs a, uint4* img
 }
 
 // A thread's share of one block's image set on its way from global memory to LDS: chunks
-// t, t + NT, ... (compile-time recursion keeps every index constant, so it stays in registers).
+// t, t + NT, ... (compile-time recursion keeps every index constant). Held as native 4-lane
+// vectors: copies of HIP's uint4 struct are memcpys, which kept the array in memory (the
+// compiler placed it in LDS, and every load was waited for where it was issued).
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 template <int N>
 struct Stage {
-  uint4 v[N];
+  u32x4 v[N];
 };
 template <int U, int N, int NT>
 __device__ __forceinline__ void stage_load(Stage<N>& s, const uint4* src) {
   if constexpr (U < N) {
-    s.v[U] = src[threadIdx.x + U * NT];
+    s.v[U] = reinterpret_cast<const u32x4*>(src)[threadIdx.x + U * NT];
     stage_load<U + 1, N, NT>(s, src);
   }
 }
 template <int U, int N, int NT>
 __device__ __forceinline__ void stage_put(const Stage<N>& s, uint4* dst) {
   if constexpr (U < N) {
-    dst[threadIdx.x + U * NT] = s.v[U];
+    reinterpret_cast<u32x4*>(dst)[threadIdx.x + U * NT] = s.v[U];
     stage_put<U + 1, N, NT>(s, dst);
   }
 }
@@ -272,11 +275,13 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(D > 32 
     }
 
     for (int blk = 0; blk < NB; ++blk) {
-      // global loads of the next block's share (block 0 of the next step after the last)
+      // global loads of the next block's share (block 0 of the next step after the last),
+      // in flight over this block's arithmetic; fp32 head width 32 has no registers to hold
+      // them and loads them at the end of the block
       const bool more = blk + 1 < NB || step + 1 < nstep;
-      if (more)
-        stage_load<0, kCopy, 64 * NW>(
-            stg, himg + (int64_t)(blk + 1 < NB ? blk + 1 : 0) * IM::kStride);
+      const uint4* next = himg + (int64_t)(blk + 1 < NB ? blk + 1 : 0) * IM::kStride;
+      constexpr bool kEarly = BF || D < 32;
+      if (kEarly && more) stage_load<0, kCopy, 64 * NW>(stg, next);
       const uint4* cb = img[kbuf];
       const float* bS = reinterpret_cast<const float*>(cb + 2 * IM::kHalf);
 #pragma unroll 1
@@ -352,7 +357,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(D > 32 
           }
         }
       }
-      if (more) stage_put<0, kCopy, 64 * NW>(stg, img[kbuf ^ 1]);
+      if (more) {
+        if constexpr (!kEarly) stage_load<0, kCopy, 64 * NW>(stg, next);
+        stage_put<0, kCopy, 64 * NW>(stg, img[kbuf ^ 1]);
+      }
       __syncthreads();
       kbuf ^= 1;
     }
