@@ -31,6 +31,11 @@ namespace {
 
 constexpr int kHS = 32;  // slots per half block: operands are imaged per half (GB = 2)
 
+// Image buffers of the point pass: a ring of four where LDS allows (4), or two (2).
+#ifndef FS_POINT_RING
+#define FS_POINT_RING 4
+#endif
+
 template <bool BF, int D>
 struct PointImages {
   static constexpr int GBH = kHS / 16;
@@ -224,7 +229,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(D > 32 
   const float* lse = a.lse_in + (int64_t)c.bh * a.N;
   const int NB = (a.G + 63) / 64;
 
-  __shared__ uint4 img[2][IM::kStride];
+  // image buffers: a ring of four where they fit in LDS (blocks staged two ahead, a workgroup
+  // barrier after every second block), else two (one ahead, a barrier after every block)
+  constexpr int RING = FS_POINT_RING == 4 && 4 * IM::kStride * 16 <= 160 * 1024 ? 4 : 2;
+  constexpr int LA = RING / 2;
+  __shared__ uint4 img[RING][IM::kStride];
 
   const int64_t pbeg = (int64_t)c.chunk * a.chunk_pts;
   const int64_t pend = min(a.N, pbeg + a.chunk_pts);
@@ -246,11 +255,16 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(D > 32 
   Stage<kCopy> stg;
 
   if (nstep == 0) return;  // uniform over the workgroup
-  stage_load<0, kCopy, 64 * NW>(stg, himg);
-  stage_put<0, kCopy, 64 * NW>(stg, img[0]);
+  const int nu = nstep * NB;  // block visits of the workgroup, u = step NB + blk
+#pragma unroll
+  for (int u = 0; u < LA; ++u)
+    if (u < nu) {
+      stage_load<0, kCopy, 64 * NW>(stg, himg + (int64_t)u * IM::kStride);
+      stage_put<0, kCopy, 64 * NW>(stg, img[u]);
+    }
   __syncthreads();
 
-  int kbuf = 0;
+  int u = 0;
   for (int step = 0; step < nstep; ++step) {
     const int tp0 = (step * NW + wpu) * 32;
     RowOp<BF, D> xo[2], go[2], fo[2];
@@ -278,11 +292,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(D > 32 
       // global loads of the next block's share (block 0 of the next step after the last),
       // in flight over this block's arithmetic; fp32 head width 32 has no registers to hold
       // them and loads them at the end of the block
-      const bool more = blk + 1 < NB || step + 1 < nstep;
-      const uint4* next = himg + (int64_t)(blk + 1 < NB ? blk + 1 : 0) * IM::kStride;
+      const bool more = u + LA < nu;
+      const int nblk = blk + LA < NB ? blk + LA : blk + LA - NB;
+      const uint4* next = himg + (int64_t)nblk * IM::kStride;
       constexpr bool kEarly = BF || D < 32;
       if (kEarly && more) stage_load<0, kCopy, 64 * NW>(stg, next);
-      const uint4* cb = img[kbuf];
+      const uint4* cb = img[u % RING];
       const float* bS = reinterpret_cast<const float*>(cb + 2 * IM::kHalf);
 #pragma unroll 1
       for (int h = 0; h < 2; ++h) {
@@ -359,10 +374,12 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(D > 32 
       }
       if (more) {
         if constexpr (!kEarly) stage_load<0, kCopy, 64 * NW>(stg, next);
-        stage_put<0, kCopy, 64 * NW>(stg, img[kbuf ^ 1]);
+        stage_put<0, kCopy, 64 * NW>(stg, img[(u + LA) % RING]);
       }
-      __syncthreads();
-      kbuf ^= 1;
+      // with the ring of four the buffer written here held block u - 2, which every
+      // wavefront finished before the barrier after block u - 1 (u even) or u - 2 (u odd)
+      if (RING == 2 || (u & 1)) __syncthreads();
+      ++u;
     }
 
     // per point: c and tb over the four lane rows; dx = P - c Q; stores
