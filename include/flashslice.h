@@ -107,7 +107,8 @@ typedef struct {
  * this problem. It holds per-workgroup partial sums (a bounded number of workgroups) and
  * token-sized buffers (G x V per sample and head). The slot-blocked kernels (G > 128 with
  * D <= 32, tied path) add per-point state: 4 bytes per (point, head) in the forward (the
- * normaliser) and 8 in the backward (the softmax correction and the weighted mean logit),
+ * normaliser) and 16 in the backward (the softmax correction, the weighted mean logit and
+ * the normaliser again, one record per point for the parameter pass),
  * plus per-head operand images (G x (2D + 3V) values). No size grows with N * G.
  * Returns FS_OK and writes *bytes, or a validation error (FS_ERR_ARG for another
  * for_backward). (A status return with an out-parameter, so that an invalid problem is an

@@ -226,7 +226,7 @@ BwdWs bwd_ws_layout(const Geom& g, int kind) {
                 ? (attn_rows(g, kind) ? 6 : 3) * tok + sizeof(float) * (size_t)g.BH() * g.G * g.G
                 : 0);
   L.cpt = off;
-  off += up(blocked(g) ? 2 * sizeof(float) * (size_t)g.BH() * (size_t)g.N : 0);
+  off += up(blocked(g) ? 4 * sizeof(float) * (size_t)g.BH() * (size_t)g.N : 0);
   L.img = off;
   off += up(blocked(g) ? point_image_bytes(g) : 0);
   L.partP2 = off;  // the deslice weights' parameter partials (untied variant)

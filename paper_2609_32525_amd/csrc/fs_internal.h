@@ -136,8 +136,8 @@ struct PassArgs {
   float* part;   // slice: U partials; bwd_a: dzmix partials; bwd_b: parameter partials
   float* part2;  // slice: s partials
   const void* img;   // point-owned pass: per-(b, h) operand images of the slot blocks
-  const float* cpt;  // blocked bwd_b: per point (c, tb) from the point-owned pass
-  float* cpt_out;    // point-owned pass: per point (c, tb), [BH][N][2]
+  const float* cpt;  // blocked bwd_b: per point (c, tb, lse2, 0) from the point-owned pass
+  float* cpt_out;    // point-owned pass: per point (c, tb, lse2, 0), [BH][N][4]
   int64_t N;
   int H, G;
   int ws_per_head;

@@ -173,7 +173,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
   const auto rdx = rows_rsrc(dxb + pbeg * rs, npts, (int)rs, D);
   const auto rdf = rows_rsrc(dfb + pbeg * rs, npts, (int)rs, D);
   const auto rl = rows_rsrc(lse + pbeg, npts, 1, 1);
-  const auto rc = rows_rsrc(PM ? a.cpt + ((int64_t)c.bh * a.N + pbeg) * 2 : a.Ws, npts, 2, 2);
+  const auto rc = rows_rsrc(PM ? a.cpt + ((int64_t)c.bh * a.N + pbeg) * 4 : a.Ws, npts, 4, 4);
   const int wpu = __builtin_amdgcn_readfirstlane(wp);
 
   struct Tile {
@@ -198,12 +198,17 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
             tt.dx0[cb][pb] = bld_row4<BF>(rdx, i * rsb + (16 * cb + 4 * j) * (int)sizeof(T), so);
         }
       }
-      const float l = COLN ? 0.f : bld32(rl, 4 * i, 4 * (tb + 16 * pb));
-      tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
-      if constexpr (PM) {
-        tt.ct[pb][0] = bld32(rc, 8 * i, 8 * (tb + 16 * pb));
-        tt.ct[pb][1] = bld32(rc, 8 * i + 4, 8 * (tb + 16 * pb));
+      float l;
+      if constexpr (PM && !COLN) {
+        // (c, tb, lse2) of the point as the point-owned pass wrote them
+        const f4 rec = bld128(rc, 16 * i, 16 * (tb + 16 * pb));
+        tt.ct[pb][0] = rec[0];
+        tt.ct[pb][1] = rec[1];
+        l = rec[2];
+      } else {
+        l = COLN ? 0.f : bld32(rl, 4 * i, 4 * (tb + 16 * pb));
       }
+      tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
     }
     if constexpr (!XT) gather_k<BF, DB, PB>(tt.xk, rx, rsb, tb, i, j);
   };

@@ -246,7 +246,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(D > 32 
   const auto rdx = rows_rsrc(dxb + pbeg * rs, npts, (int)rs, D);
   const auto rdf = rows_rsrc(dfb + pbeg * rs, npts, (int)rs, D);
   const auto rl = rows_rsrc(lse + pbeg, npts, 1, 1);
-  const auto rc = rows_rsrc(a.cpt_out + ((int64_t)c.bh * a.N + pbeg) * 2, npts, 2, 2);
+  const auto rc = rows_rsrc(a.cpt_out + ((int64_t)c.bh * a.N + pbeg) * 4, npts, 4, 4);
 
   // staging: thread t copies chunks t, t + 64 NW, ... of a block's image set
   static_assert(IM::kStride % (64 * NW) == 0, "image stride must be whole copy rounds");
@@ -402,10 +402,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(D > 32 
         if constexpr (ROLE == 2) v += bld_row4<BF>(rdx, vo, so);  // the slice weights' dx part
         bst_row4<BF>(rdx, v, vo, so);
       }
-      if (!COLN && j == 0) {
-        bst32(rc, cc, 8 * i, 8 * (tp0 + 16 * pb));
-        bst32(rc, tb, 8 * i + 4, 8 * (tp0 + 16 * pb));
-      }
+      // the parameter pass's per-point record: c, tb and the normaliser in one 16-byte load
+      if (!COLN && j == pb) bst128(rc, f4{cc, tb, lse2[pb], 0.f}, 16 * i, 16 * (tp0 + 16 * pb));
       csum[pb] = tsum[pb] = 0.f;
     }
   }
