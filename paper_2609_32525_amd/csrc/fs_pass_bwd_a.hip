@@ -67,7 +67,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
     float lse2[2][4];
     PtGather<BF, VB> g;
     uint4 grow[TR ? 2 : 1];
-    float l1[TR ? 2 : 1];
+    float l1;  // TR: lse of point 16 (j % 2) + i of the tile
   };
   auto load_tile = [&](Tile& tt, int t) {
     const int tb = (t * NP + wpu) * 32;
@@ -76,8 +76,6 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
       load_row_buf<BF, D>(tt.xo[pb], rx, i * rsb, (tb + 16 * pb) * rsb, j);
       if constexpr (TR) {
         tt.grow[pb] = bld128u(rg, i * rsb + 16 * j, (tb + 16 * pb) * rsb);
-        const float l = bld32(rl, 4 * i, 4 * (tb + 16 * pb));
-        tt.l1[pb] = tb + 16 * pb + i < npts ? l : kMasked;
       } else {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -86,7 +84,14 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
         }
       }
     }
-    if constexpr (!TR) gather_points_buf<BF, VB>(tt.g, rg, rsb, tb * rsb, i, j);
+    if constexpr (TR) {
+      // the tile's 32 normalisers in one load, spread over the lanes by shuffles
+      const int p = 16 * (j & 1) + i;
+      const float l = bld32(rl, 4 * p, 4 * tb);
+      tt.l1 = tb + p < npts ? l : kMasked;
+    } else {
+      gather_points_buf<BF, VB>(tt.g, rg, rsb, tb * rsb, i, j);
+    }
   };
   pipeline<(NS >= FS_NS_NOPF ? 0 : FS_PF_BWD_A), Tile>(ntile, load_tile, [&](Tile& cur, int t) {
     const RowOp<BF, D>* xo = cur.xo;
@@ -109,7 +114,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS
 #pragma unroll
       for (int pb = 0; pb < 2; ++pb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) cur.lse2[pb][r] = __shfl(cur.l1[pb], 4 * j + r);
+        for (int r = 0; r < 4; ++r) cur.lse2[pb][r] = __shfl(cur.l1, 16 * pb + 4 * j + r);
     }
     const float(*lse2)[4] = cur.lse2;
     f4 w[2][GB];

@@ -179,6 +179,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
   struct Tile {
     RowOp<BF, D> xo[PB], go[PB], fo[PB];
     float lse2[PB];
+    float l1;  // lse_load (bf16 tiles of the fused pass)
     float ct[PM ? PB : 1][2];
     f4 dx0[ROLE == 2 ? DB : 1][PB];  // the dx already written (untied deslice part)
     KGather<BF, DB, PB> xk;          // X again, points on the k index, for dW_s
@@ -198,18 +199,18 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
             tt.dx0[cb][pb] = bld_row4<BF>(rdx, i * rsb + (16 * cb + 4 * j) * (int)sizeof(T), so);
         }
       }
-      float l;
       if constexpr (PM && !COLN) {
         // (c, tb, lse2) of the point as the point-owned pass wrote them
         const f4 rec = bld128(rc, 16 * i, 16 * (tb + 16 * pb));
         tt.ct[pb][0] = rec[0];
         tt.ct[pb][1] = rec[1];
-        l = rec[2];
-      } else {
-        l = COLN ? 0.f : bld32(rl, 4 * i, 4 * (tb + 16 * pb));
+        tt.lse2[pb] = tb + 16 * pb + i < npts ? rec[2] : kMasked;
+      } else if constexpr (COLN || PB == 1) {
+        const float l = COLN ? 0.f : bld32(rl, 4 * i, 4 * (tb + 16 * pb));
+        tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
       }
-      tt.lse2[pb] = tb + 16 * pb + i < npts ? l : kMasked;
     }
+    if constexpr (!PM && !COLN && PB == 2) tt.l1 = lse_load(rl, tb, i, j);
     if constexpr (!XT) gather_k<BF, DB, PB>(tt.xk, rx, rsb, tb, i, j);
   };
   // fp32 with 64-slot waves has the longest tiles to cover: one more tile in flight there
@@ -219,6 +220,7 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
     const RowOp<BF, D>(&xo)[PB] = cur.xo;
     const RowOp<BF, D>(&go)[PB] = cur.go;
     const RowOp<BF, D>(&fo)[PB] = cur.fo;
+    if constexpr (!PM && !COLN && PB == 2) lse_pair(cur.lse2, cur.l1, tp0, npts, i);
     const float(&lse2)[PB] = cur.lse2;
     // T-layout tiles: rows = slots g0 + 16 gb + 4 j + r, cols = points 16 pb + i
     f4 tl[GB][PB], w[GB][PB], dw[GB][PB];

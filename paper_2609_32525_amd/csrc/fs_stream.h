@@ -368,6 +368,19 @@ __device__ __forceinline__ void store_tile_staged(char* sb, const f4 (&o)[D / 16
   wave_lds_sync();
 }
 
+// The base-2 normalisers of a 32-point tile for the T layout (lane 16 j + i: point 16 pb + i of
+// block pb) from one load: lane 16 j + i reads point 16 (j % 2) + i (lse_load, issued with the
+// tile's other loads), and at use a lane swap of rows j and j ^ 1 gives every lane both
+// blocks' values (lse_pair). Points at or past npts get kMasked.
+__device__ __forceinline__ float lse_load(__amdgpu_buffer_rsrc_t rl, int tb, int i, int j) {
+  return bld32(rl, 4 * (16 * (j & 1) + i), 4 * tb);
+}
+__device__ __forceinline__ void lse_pair(float (&l2)[2], float raw, int tb, int npts, int i) {
+  const auto s = __builtin_amdgcn_permlane16_swap(__float_as_uint(raw), __float_as_uint(raw), false, false);
+  l2[0] = tb + i < npts ? __uint_as_float(s[0]) : kMasked;
+  l2[1] = tb + 16 + i < npts ? __uint_as_float(s[1]) : kMasked;
+}
+
 // Four values of one row in the storage dtype (the counterpart of bst_row4), as fp32.
 template <bool BF>
 __device__ __forceinline__ f4 bld_row4(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
