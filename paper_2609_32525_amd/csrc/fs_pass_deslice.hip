@@ -6,6 +6,10 @@
 
 // Output tiles staged through LDS for whole-segment 16-byte stores (1) or stored straight
 // from the MFMA result layout, 4 values per lane (0).
+// Block images of the point-owned deslice: a ring of four (4) or two buffers (2).
+#ifndef FS_DESLICE_PT_RING
+#define FS_DESLICE_PT_RING 4
+#endif
 #ifndef FS_DESLICE_STAGE
 #define FS_DESLICE_STAGE 1
 #endif
@@ -224,7 +228,11 @@ __global__ __launch_bounds__(64 * NW) void k_deslice_pt(PassArgs a) {
   using ZOp = typename IM::ZOp;
   constexpr int GBH = IM::GBH, VB = IM::VB;
   using T = typename Store<BF>::T;
-  __shared__ uint4 img[2][IM::kChunks];
+  // block images: a ring of four (blocks built two ahead, a workgroup barrier after every
+  // second block) or two (one ahead, a barrier after every block; head width 64, whose two
+  // workgroups per compute unit would not fit four)
+  constexpr int RING = FS_DESLICE_PT_RING == 4 && D <= 32 ? 4 : 2, LA = RING / 2;
+  __shared__ uint4 img[RING][IM::kChunks];
   const int lane = threadIdx.x & 63, i = lane & 15, j = lane >> 4;
   const int wpu = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const HeadCtx c = head_ctx<D>(a, 0, 0);
@@ -262,10 +270,15 @@ __global__ __launch_bounds__(64 * NW) void k_deslice_pt(PassArgs a) {
   };
 
   if (nstep == 0) return;  // uniform over the workgroup
-  build(0);
-  put(img[0]);
+  const int nu = nstep * NB;  // block visits, u = step NB + blk
+#pragma unroll
+  for (int u = 0; u < LA; ++u)
+    if (u < nu) {
+      build(u % NB);
+      put(img[u]);
+    }
   __syncthreads();
-  int kbuf = 0;
+  int u = 0;
   for (int step = 0; step < nstep; ++step) {
     const int tb = (step * NW + wpu) * 32;
     RowOp<BF, D> xo[2];
@@ -284,9 +297,9 @@ __global__ __launch_bounds__(64 * NW) void k_deslice_pt(PassArgs a) {
 #pragma unroll
     for (int vb = 0; vb < VB; ++vb) o[vb][0] = o[vb][1] = zero4();
     for (int blk = 0; blk < NB; ++blk) {
-      const bool more = blk + 1 < NB || step + 1 < nstep;
-      if (more) build(blk + 1 < NB ? blk + 1 : 0);
-      const uint4* cbuf = img[kbuf];
+      const bool more = u + LA < nu;
+      if (more) build(blk + LA < NB ? blk + LA : blk + LA - NB);
+      const uint4* cbuf = img[u % RING];
       const float* bS = reinterpret_cast<const float*>(cbuf + 2 * IM::kW + 2 * IM::kZ);
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
@@ -340,9 +353,11 @@ __global__ __launch_bounds__(64 * NW) void k_deslice_pt(PassArgs a) {
 #pragma unroll
           for (int pb = 0; pb < 2; ++pb) o[vb][pb] = mm_gop_b<BF, GBH, VB, 2>(zop, vb, wt, pb, o[vb][pb]);
       }
-      if (more) put(img[kbuf ^ 1]);
-      __syncthreads();
-      kbuf ^= 1;
+      if (more) put(img[(u + LA) % RING]);
+      // with the ring of four the buffer written here held block u - 2, which every
+      // wavefront finished before the barrier after block u - 1 (u even) or u - 2 (u odd)
+      if (RING == 2 || (u & 1)) __syncthreads();
+      ++u;
     }
 #pragma unroll
     for (int pb = 0; pb < 2; ++pb) {
