@@ -59,15 +59,15 @@ struct PointImages {
 
 template <class Op>
 __device__ __forceinline__ void put_first(const Op& o, uint4* base, int lane, int nchunks) {
-  const uint4* src = reinterpret_cast<const uint4*>(&o);
+  const u32x4* src = reinterpret_cast<const u32x4*>(&o);
 #pragma unroll
-  for (int q = 0; q < nchunks; ++q) base[q * 64 + lane] = src[q];
+  for (int q = 0; q < nchunks; ++q) reinterpret_cast<u32x4*>(base)[q * 64 + lane] = src[q];
 }
 template <class Op>
 __device__ __forceinline__ void get_first(Op& o, const uint4* base, int lane, int nchunks) {
-  uint4* dst = reinterpret_cast<uint4*>(&o);
+  u32x4* dst = reinterpret_cast<u32x4*>(&o);
 #pragma unroll
-  for (int q = 0; q < nchunks; ++q) dst[q] = base[q * 64 + lane];
+  for (int q = 0; q < nchunks; ++q) dst[q] = reinterpret_cast<const u32x4*>(base)[q * 64 + lane];
 }
 
 // Builds job q (q < 11) of slot block blk's image set for one (b, h) into `out` (global or
@@ -147,9 +147,8 @@ __global__ __launch_bounds__(64 * 11) void k_point_images(PassArgs a, uint4* img
 
 // A thread's share of one block's image set on its way from global memory to LDS: chunks
 // t, t + NT, ... (compile-time recursion keeps every index constant). Held as native 4-lane
-// vectors: copies of HIP's uint4 struct are memcpys, which kept the array in memory (the
-// compiler placed it in LDS, and every load was waited for where it was issued).
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+// vectors: as uint4 structs the array stayed in memory (the compiler placed it in LDS, and
+// every load was waited for where it was issued).
 template <int N>
 struct Stage {
   u32x4 v[N];

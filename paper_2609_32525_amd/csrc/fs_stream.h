@@ -63,6 +63,9 @@ __device__ __forceinline__ float bf_to_f(unsigned short h) {
 __device__ __forceinline__ unsigned short f_to_bf(float f) {
   return __builtin_bit_cast(unsigned short, (__bf16)f);  // round to nearest even
 }
+// 16 bytes as a native vector: copies of HIP's uint4 struct are memcpys, which can keep the
+// array they read or write in memory instead of registers
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 typedef float fl2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bfl2 __attribute__((ext_vector_type(2)));
 // Two floats rounded to bf16 (nearest even) in one 32-bit word, the first in the low half.
@@ -812,15 +815,15 @@ __device__ __forceinline__ void mm_points(f4 (*acc)[CB], const f4 (*w)[GB],
 template <class Op>
 __device__ __forceinline__ void lds_put(const Op& o, uint4* base, int lane) {
   static_assert(sizeof(Op) % 16 == 0, "operand image must be whole 16-byte chunks");
-  const uint4* src = reinterpret_cast<const uint4*>(&o);
+  const u32x4* src = reinterpret_cast<const u32x4*>(&o);
 #pragma unroll
-  for (int q = 0; q < (int)(sizeof(Op) / 16); ++q) base[q * 64 + lane] = src[q];
+  for (int q = 0; q < (int)(sizeof(Op) / 16); ++q) reinterpret_cast<u32x4*>(base)[q * 64 + lane] = src[q];
 }
 template <class Op>
 __device__ __forceinline__ void lds_get(Op& o, const uint4* base, int lane) {
-  uint4* dst = reinterpret_cast<uint4*>(&o);
+  u32x4* dst = reinterpret_cast<u32x4*>(&o);
 #pragma unroll
-  for (int q = 0; q < (int)(sizeof(Op) / 16); ++q) dst[q] = base[q * 64 + lane];
+  for (int q = 0; q < (int)(sizeof(Op) / 16); ++q) dst[q] = reinterpret_cast<const u32x4*>(base)[q * 64 + lane];
 }
 template <class Op>
 constexpr int lds_chunks() {
