@@ -5,8 +5,10 @@
 
 #include "fs_stream.h"
 
-// The point groups' end-of-kernel reduction in the LDS of the loop's exchange buffers (1) or
-// in an allocation of its own (0).
+// bf16: the point groups' end-of-kernel reduction in the LDS of the loop's exchange buffers
+// (1) or in an allocation of its own (0). fp32 keeps its own: with the smaller LDS footprint
+// two workgroups fit a compute unit, and the kernel compiled for that spilled (head width 32,
+// G = 64: pass B 1035 -> 1165 us).
 #ifndef FS_BWDB_LDS_ALIAS
 #define FS_BWDB_LDS_ALIAS 1
 #endif
@@ -153,7 +155,8 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
                                             (size_t)(NP - 1) * NS * GB * 4 * 16 * sizeof(float)
                                       : 0;
   constexpr size_t kSmem0 = kGxBytes > kDaBytes ? kGxBytes : kDaBytes;
-  __shared__ __attribute__((aligned(16))) char smem[FS_BWDB_LDS_ALIAS && kRedBytes > kSmem0 ? kRedBytes : kSmem0];
+  constexpr bool kAlias = FS_BWDB_LDS_ALIAS && BF;
+  __shared__ __attribute__((aligned(16))) char smem[kAlias && kRedBytes > kSmem0 ? kRedBytes : kSmem0];
   f4* gx = reinterpret_cast<f4*>(smem);
   float* myda = reinterpret_cast<float*>(smem) + (size_t)wave * kDaWords;
   // XT: bf16 with head width 32 forms dW_s's point-ordered x operand from the row operand the
@@ -465,15 +468,14 @@ __global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(PM
 
   float* pp = a.part + ((int64_t)c.bh * a.chunks + c.chunk) * ((int64_t)D * a.G + a.G + 2 * a.nblk);
   if constexpr (NP > 1) {
-#if FS_BWDB_LDS_ALIAS
-    __syncthreads();  // every wave is done with the loop's buffers
-    auto& red = *reinterpret_cast<f4(*)[NP - 1][NS][DB][GB][64]>(smem);
-    auto& redb = *reinterpret_cast<float(*)[NP - 1][NS][GB][4][16]>(
-        smem + (size_t)(NP - 1) * NS * DB * GB * 64 * sizeof(f4));
-#else
-    __shared__ f4 red[NP - 1][NS][DB][GB][64];
-    __shared__ float redb[NP - 1][NS][GB][4][16];
-#endif
+    constexpr int kRed = (NP - 1) * NS * DB * GB * 64, kRedb = (NP - 1) * NS * GB * 4 * 16;
+    __shared__ f4 red_own[kAlias ? 1 : kRed];
+    __shared__ float redb_own[kAlias ? 1 : kRedb];
+    if constexpr (kAlias) __syncthreads();  // every wave is done with the loop's buffers
+    f4* redp = kAlias ? reinterpret_cast<f4*>(smem) : red_own;
+    float* redbp = kAlias ? reinterpret_cast<float*>(smem + (size_t)kRed * sizeof(f4)) : redb_own;
+    auto& red = *reinterpret_cast<f4(*)[NP - 1][NS][DB][GB][64]>(redp);
+    auto& redb = *reinterpret_cast<float(*)[NP - 1][NS][GB][4][16]>(redbp);
     if (wp > 0) {
 #pragma unroll
       for (int gb = 0; gb < GB; ++gb) {
