@@ -19,7 +19,7 @@ namespace {
 // fx in place of dout, plus the weight sums s (the slot-owned slice).
 // =======================================================================================
 template <bool BF, int D, int GS, int NS, int NP, bool SL>
-__global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(FS_WPE_BWD_A))) void k_bwd_a(
+__global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(D > 32 ? 1 : FS_WPE_BWD_A))) void k_bwd_a(
     PassArgs a) {
   constexpr int GB = GS / 16, VB = D / 16;
   constexpr bool SPLIT = BF;

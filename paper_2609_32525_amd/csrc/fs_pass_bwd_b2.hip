@@ -18,7 +18,7 @@ constexpr bool bwd_b2_fits(bool, int D, int GS) { return D < 64 || GS < 64; }
 // COLN: LinearNO's slice weights. Partials per workgroup as in k_bwd_b, the slice set into
 // a.part and the deslice set into a.part_d.
 template <bool BF, int D, int GS, int NS, int NP, int PB, bool COLN>
-__global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(GS <= 32 ? FS_WPE_BWD_B2_G32 : FS_WPE_BWD_B))) void k_bwd_b2(
+__global__ __launch_bounds__(64 * NS * NP) __attribute__((amdgpu_waves_per_eu(GS <= 32 && D <= 32 ? FS_WPE_BWD_B2_G32 : FS_WPE_BWD_B))) void k_bwd_b2(
     PassArgs a) {
   static_assert(NS == 1, "one wavefront covers the tile's slots");
   static_assert(PB == 2 || !BF, "bf16 contracts over 32 points");
