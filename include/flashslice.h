@@ -106,7 +106,7 @@ typedef struct {
  * fs_linearno_slice_fwd (for_backward = 3) or by fs_linearno_bwd (for_backward = 4), for
  * this problem. It holds per-workgroup partial sums (a bounded number of workgroups) and
  * token-sized buffers (G x V per sample and head). The slot-blocked kernels (G > 128 with
- * D <= 32, tied path) add per-point state: 4 bytes per (point, head) in the forward (the
+ * D <= 32, or G > 64 with D = 64 in bf16; tied path) add per-point state: 4 bytes per (point, head) in the forward (the
  * normaliser) and 16 in the backward (the softmax correction, the weighted mean logit and
  * the normaliser again, one record per point for the parameter pass),
  * plus per-head operand images (G x (2D + 3V) values). No size grows with N * G.

@@ -60,10 +60,16 @@ PassEvents& pass_events() {
   return ev;
 }
 
+// Head width 64 takes the slot-blocked family above 64 slots: the cooperative kernels with two
+// 64-slot waves per tile spill at that width (bf16, N = 2^18, G = 128: 2.65 -> 1.93 ms).
+#ifndef FS_BLOCKED_MIN_G_D64
+#define FS_BLOCKED_MIN_G_D64 64
+#endif
 bool blocked(const Geom& g) {
   // head width 64: bf16 storage and the tied path (fp32 images of a 64-slot block would not
   // fit twice in LDS)
-  return g.G > FS_BLOCKED_MIN_G && (g.D <= 32 || (g.D == 64 && g.bf16 && !g.untied));
+  return g.G > (g.D == 64 ? FS_BLOCKED_MIN_G_D64 : FS_BLOCKED_MIN_G) &&
+         (g.D <= 32 || (g.D == 64 && g.bf16 && !g.untied));
 }
 
 PassCfg pick_cfg(const Geom& g, Pass pass, int np) {

@@ -116,6 +116,8 @@ SMALL = [
           ws_mode="std3", N=500, H=2, B=1),
     small("bf16_D64_G176_linc", "bf16", 64, 176, O.MIX_LINEAR_C, N=700, H=2),
     small("bf16_D64_G256_lin_N33", "bf16", 64, 256, O.MIX_LINEAR_G, N=33, H=2),
+    # head width 64 takes the slot-blocked family from 80 slots: two whole 64-slot blocks
+    small("bf16_D64_G128_lin", "bf16", 64, 128, O.MIX_LINEAR_G, N=900, H=2),
 ]
 
 
